@@ -1,0 +1,255 @@
+/*
+ * libnmdlm — the block-denoising step of a neuromorphic masked diffusion
+ * language model (N-MDLM), for AMD Instinct MI355X (gfx950).
+ *
+ * Plain C ABI: device pointers, sizes and a HIP stream (passed as void*,
+ * NULL = the default stream).  No call allocates or frees memory; scratch
+ * memory is a caller-provided workspace whose size is given by the
+ * *_workspace_size functions.  Every call validates its arguments on the
+ * host first and, on error, returns a status without enqueueing any work.
+ * Calls are asynchronous with respect to the host: outputs (and statistics)
+ * are valid once the stream has reached them.  The library keeps no global
+ * mutable state; two calls may run concurrently on different streams when
+ * their workspaces and outputs do not overlap.
+ *
+ * Spike tensors are {0,1}^{T x M x K} packed little-endian into uint64
+ * words: tensor [T][M][ceil(K/64)], bit j of word w is channel 64*w + j.
+ * Padding bits must be zero on input and are written as zero on output.
+ *
+ * Weight matrices are int8 [K][ldw] row-major: row k holds the weights that
+ * leave input neuron k (its fan-out), so the products below skip whole rows.
+ * ldw is a multiple of 16 and >= N; bytes [N, ldw) of a row may be read and
+ * are ignored.  K * ldw must be below 2^31.
+ */
+#ifndef NMDLM_H
+#define NMDLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NMDLM_ABI_VERSION 1
+
+typedef enum nmdlm_status {
+  NMDLM_OK = 0,
+  NMDLM_ERR_INVALID_ARG = 1,  /* null pointer, size <= 0, threshold <= 0, ... */
+  NMDLM_ERR_UNSUPPORTED = 2,  /* valid but outside the supported envelope     */
+  NMDLM_ERR_WORKSPACE = 3,    /* workspace missing or smaller than required   */
+  NMDLM_ERR_HIP = 4           /* a HIP launch reported an error               */
+} nmdlm_status;
+
+/* flags (bitwise OR) */
+#define NMDLM_FORCE_DENSE 0x1u   /* read every weight row: the un-skipped product */
+#define NMDLM_NO_HEAD     0x2u   /* block step without head/confidence/unmask    */
+/* bits 8..15 of the flags of nmdlm_qbsm: force the number of K splits
+ * (0 = automatic).  Results do not depend on it. */
+#define NMDLM_SPLIT_SHIFT 8u
+/* bits 16..19: force rows per tile group (0 = automatic; 1,2,4,8 = 16..128
+ * rows).  Results do not depend on it. */
+#define NMDLM_ROWTILE_SHIFT 16u
+
+/* Supported envelope (NMDLM_ERR_UNSUPPORTED beyond it). */
+#define NMDLM_MAX_T 8
+#define NMDLM_MAX_K 65536
+
+/*
+ * Statistics of one spike product, written by the device (int64 so the
+ * host can sum them).  weight_bytes is the number of weight bytes the
+ * product reads: k_active * n (the per-block load of Eq. (13)).
+ */
+typedef struct nmdlm_qbsm_stats {
+  int64_t k_total;       /* K                                             */
+  int64_t k_active;      /* input neurons that spike at least once in the
+                            block (rows of W that are read)               */
+  int64_t n;             /* N                                             */
+  int64_t weight_bytes;  /* k_active * n                                  */
+} nmdlm_qbsm_stats;
+
+/* ------------------------------------------------------------------------
+ * nmdlm_qbsm — quantised-weight x binary-spike product with row skipping
+ *
+ * Sec. IV-A: the linear operation over the B*T rows of a block,
+ *     I[t,m,n] = bias[n] + sum_k S[t,m,k] * W[k,n],
+ * where, by assumption (ii), row k of W is read only if input neuron k
+ * spikes at least once among all T*M rows.  The result is identical to the
+ * dense product (integer arithmetic, no overflow for K*127 + |bias| < 2^31).
+ *
+ * Optional fused integrate-and-fire epilogue (Sec. II-B, Eqs. (3)-(4),
+ * integrate-then-fire with soft reset, membrane starting at 0):
+ *     V = 0; for t: V += I[t]; s[t] = (V >= theta); V -= s[t]*theta.
+ *
+ *   s_in      device, spikes [T][M][ceil(K/64)]
+ *   T, M, K   1 <= T <= 8, M >= 1, T*M <= 2^19, 1 <= K <= 65536
+ *   W, N, ldw device int8 [K][ldw] (see above), N >= 1
+ *   bias      device int32 [N] or NULL (zero)
+ *   cur_out   device int32 [T][M][N] or NULL: the currents I
+ *   theta     threshold (> 0) used when s_out is given; ignored otherwise
+ *   theta_vec device int32 [N] per-neuron thresholds (> 0) or NULL (use theta)
+ *   s_out     device spikes [T][M][ceil(N/64)] or NULL; at least one of
+ *             cur_out / s_out must be given
+ *   stats     device, one nmdlm_qbsm_stats, or NULL
+ *   flags     NMDLM_FORCE_DENSE, split/row-tile overrides
+ *   ws        device workspace of ws_bytes >= nmdlm_qbsm_workspace_size();
+ *             zero-filled before its first use; every call leaves its
+ *             counter region zero again
+ *   stream    hipStream_t or NULL
+ * ------------------------------------------------------------------------ */
+nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K,
+                        const int8_t* W, int N, int64_t ldw,
+                        const int32_t* bias, int32_t* cur_out,
+                        int32_t theta, const int32_t* theta_vec,
+                        uint64_t* s_out, nmdlm_qbsm_stats* stats,
+                        unsigned flags, void* ws, size_t ws_bytes, void* stream);
+
+size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_if_neuron — integrate-and-fire with soft reset (Sec. II-B,
+ * Eqs. (3)-(4)), integrate-then-fire order, equality fires, no lower clamp:
+ *     V = v_in (or 0); for t: V += cur[t] + theta*resid[t];
+ *                             s[t] = (V >= theta); V -= s[t]*theta.
+ *
+ *   cur       device int32 [T][M][N]
+ *   theta     threshold (> 0); theta_vec device int32 [N] or NULL
+ *   resid     device spikes [T][M][ceil(N/64)] or NULL: membrane shortcut
+ *   v_inout   device int32 [M][N] or NULL: initial membrane in, final out
+ *   s_out     device spikes [T][M][ceil(N/64)]
+ * ------------------------------------------------------------------------ */
+nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N,
+                             int32_t theta, const int32_t* theta_vec,
+                             const uint64_t* resid, int32_t* v_inout,
+                             uint64_t* s_out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_qnl_lut — 8-bit-in / 8-bit-out table non-linearity (the quantised
+ * non-linearity of the paper's op list).
+ *   NMDLM_QNL_S8: index = byte of clamp(floor(x / 2^shift), -128, 127)
+ *   NMDLM_QNL_U8: index = clamp(x, 0, 255)            (shift ignored)
+ *   y[i] = lut[index]  (the raw table byte; read it as int8 in S8 mode)
+ *
+ *   x    device int32 [n];  lut device uint8 [256];  y device uint8 [n]
+ *   0 <= shift <= 31
+ * ------------------------------------------------------------------------ */
+#define NMDLM_QNL_S8 0
+#define NMDLM_QNL_U8 1
+nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode,
+                           const uint8_t* lut, uint8_t* y, void* stream);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_bbm_attn — attention on spike operands (binary-binary products,
+ * table weights, fixed-point normalisation).  For every timestep t, head h,
+ * block query i < M and key j < C+M:
+ *     s = popcount(Q[t,i,head h] AND K[t,j,head h])       in [0, dh]
+ *     p = lut_att[s]                                       (uint8)
+ *     a[t,i,c] = floor(256 * sum_j p * V[t,j,c] / sum_j p)   (0 if sum_j p = 0)
+ * then optionally A = IF(a, theta_a) over t.  The block's own keys/values
+ * must already be in rows [C, C+M) of the caches.
+ *
+ *   q         device spikes [T][M][d/64], d = H*dh
+ *   k_cache   device spikes [T][cache_cap][d/64]  (token-major)
+ *   vt_cache  device spikes, channel-major: [T][d][cache_cap/64], bit j%64
+ *             of word j/64 of row (t, c) is V[t,j,c]
+ *   cache_cap multiple of 64, >= C+M
+ *   dh        64 or 128 (else NMDLM_ERR_UNSUPPORTED): scores stay within
+ *             the 256-entry table
+ *   lut_att   device uint8 [256]
+ *   a_out     device int32 [T][M][d] or NULL
+ *   theta_a   threshold (> 0) when s_out is given
+ *   s_out     device spikes [T][M][d/64] or NULL (at least one output)
+ *   ws        workspace of nmdlm_bbm_attn_workspace_size() bytes (used when
+ *             a_out is NULL)
+ * ------------------------------------------------------------------------ */
+nmdlm_status nmdlm_bbm_attn(const uint64_t* q, const uint64_t* k_cache,
+                            const uint64_t* vt_cache, int64_t cache_cap,
+                            int T, int M, int C, int H, int dh,
+                            const uint8_t* lut_att, int32_t* a_out,
+                            int32_t theta_a, uint64_t* s_out,
+                            void* ws, size_t ws_bytes, void* stream);
+
+size_t nmdlm_bbm_attn_workspace_size(int T, int M, int H, int dh);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_block_step — one denoising step z_{s+1} = f_dec(z_s, h) of block
+ * diffusion (Sec. III-A, Eq. (6)) through a stack of spiking layers, or a
+ * context prefill (Eq. (5): the same stack over the context tokens with
+ * C = 0 and NMDLM_NO_HEAD).
+ *
+ * Per layer (Fig. 1: IF neurons in every layer; the wiring below is this
+ * library's reading, the paper gives no layer internals):
+ *   Q,K,V = IF(QBSM(X, W_qkv))   (thresholds q, k, v; K,V -> cache rows [C,C+M))
+ *   A     = IF(attn(Q, caches), theta_a)
+ *   X1    = IF(QBSM(A, W_o), theta_o, residual X)
+ *   H     = IF(lut_act[QBSM(X1, W_up) >> s_up], theta_up)
+ *   Y     = IF(QBSM(H, W_dn), theta_dn, residual X1)
+ * Head (unless NMDLM_NO_HEAD): acc[m,v] = sum_t sum_c Y[t,m,c] W_head[c,v],
+ * logit = (float)acc * head_scale[v]; pred = argmax (ties: smallest id);
+ * conf = 1 / sum_v exp(logit_v - logit_pred) (fp64); then the k_unmask
+ * masked positions of highest confidence (ties: lower position) take their
+ * predicted token (B/S tokens per step, Sec. III-A).
+ * ------------------------------------------------------------------------ */
+typedef struct nmdlm_layer {
+  const int8_t* w_qkv;   /* device [d][3d]: columns Q | K | V */
+  const int8_t* w_o;     /* device [d][d]  */
+  const int8_t* w_up;    /* device [d][F]  */
+  const int8_t* w_dn;    /* device [F][d]  */
+  int32_t theta_q, theta_k, theta_v, theta_a, theta_o, theta_up, theta_dn;
+  int32_t s_up;          /* right shift before lut_act (0..31) */
+  const uint8_t* lut_att;/* device [256] attention score table */
+  const uint8_t* lut_act;/* device [256] activation table (int8 bytes) */
+  uint64_t* k_cache;     /* device [T][cache_cap][d/64]      */
+  uint64_t* vt_cache;    /* device [T][d][cache_cap/64]      */
+} nmdlm_layer;
+
+typedef struct nmdlm_model {
+  int n_layers, d, H, F, V, T;
+  int64_t cache_cap;          /* multiple of 64 */
+  int max_pos;                /* rows of pos_ch */
+  const nmdlm_layer* layers;  /* HOST array [n_layers] */
+  const uint64_t* emb;        /* device [V+1][T][d/64]; row V = mask token */
+  const int32_t* pos_ch;      /* device [max_pos][T]: channel of the single
+                                 position spike ORed into the token spikes */
+  const int8_t* w_head;       /* device [d][V] (NULL allowed with NO_HEAD) */
+  const float* head_scale;    /* device [V]                                */
+} nmdlm_model;
+
+typedef struct nmdlm_step_io {
+  int M;                   /* tokens in the block (or context, in prefill)   */
+  int C;                   /* cache rows already holding context            */
+  int pos0;                /* sequence position of the first block token    */
+  unsigned flags;          /* NMDLM_NO_HEAD, NMDLM_FORCE_DENSE              */
+  const uint64_t* x_in;    /* device [T][M][d/64] block input spikes, or NULL:
+                              assemble from tokens/masked, emb and pos_ch   */
+  int32_t* tokens;         /* device [M] in/out (may be NULL with x_in and
+                              NO_HEAD)                                       */
+  uint8_t* masked;         /* device [M] in/out, 1 = still masked           */
+  int k_unmask;            /* tokens revealed by this step                  */
+  uint64_t* y_out;         /* device [T][M][d/64] last layer spikes or NULL */
+  float* logits;           /* device [M][V] or NULL (workspace is used)     */
+  int32_t* pred;           /* device [M] or NULL                            */
+  double* conf;            /* device [M] or NULL                            */
+  int32_t* unmasked_pos;   /* device [k_unmask] or NULL: chosen positions in
+                              selection order, -1 when fewer were masked    */
+  nmdlm_qbsm_stats* stats; /* device [4*n_layers + 1] or NULL: per product
+                              (QKV, O, up, down per layer, then the head)  */
+} nmdlm_step_io;
+
+nmdlm_status nmdlm_block_step(const nmdlm_model* model, nmdlm_step_io* io,
+                              void* ws, size_t ws_bytes, void* stream);
+
+size_t nmdlm_block_step_workspace_size(const nmdlm_model* model, int M,
+                                       unsigned flags);
+
+/* Clears a workspace region with a fill kernel on the stream (use once on a
+ * new workspace). */
+nmdlm_status nmdlm_workspace_clear(void* ws, size_t ws_bytes, void* stream);
+
+const char* nmdlm_status_string(nmdlm_status s);
+int nmdlm_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NMDLM_H */

@@ -1,0 +1,206 @@
+// C ABI of libnmdlm: argument validation (before any HIP call), workspace
+// sizing and dispatch to the launchers.
+#include <algorithm>
+
+#include "common.h"
+
+namespace nmdlm {
+size_t block_step_ws_size(const nmdlm_model* md, int M, unsigned flags);
+nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws, size_t ws_bytes,
+                             hipStream_t st);
+}  // namespace nmdlm
+
+using namespace nmdlm;
+
+namespace {
+
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t qbsm_ws(int T, int M, int K, int N) {
+  Carver cv{nullptr, 0, (size_t)-1, true};
+  QbsmScratch s;
+  carve_qbsm_scratch(cv, qbsm_limits_single(T, M, K, N), &s);
+  return align_up(cv.off, 256);
+}
+
+bool weights_ok(const int8_t* W, int K, int N, int64_t ldw) {
+  if (!W || !aligned(W, 16)) return false;
+  if (ldw < N || (ldw % 16) != 0) return false;
+  if ((int64_t)K * ldw >= (int64_t)1 << 31) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nmdlm_abi_version(void) { return NMDLM_ABI_VERSION; }
+
+const char* nmdlm_status_string(nmdlm_status s) {
+  switch (s) {
+    case NMDLM_OK: return "ok";
+    case NMDLM_ERR_INVALID_ARG: return "invalid argument";
+    case NMDLM_ERR_UNSUPPORTED: return "unsupported shape or layout";
+    case NMDLM_ERR_WORKSPACE: return "workspace missing or too small";
+    case NMDLM_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N) {
+  if (T < 1 || T > NMDLM_MAX_T || M < 1 || K < 1 || K > NMDLM_MAX_K || N < 1) return 0;
+  return qbsm_ws(T, M, K, N);
+}
+
+nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t* W, int N,
+                        int64_t ldw, const int32_t* bias, int32_t* cur_out, int32_t theta,
+                        const int32_t* theta_vec, uint64_t* s_out, nmdlm_qbsm_stats* stats,
+                        unsigned flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!s_in || T < 1 || M < 1 || K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T || K > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
+  if (!weights_ok(W, K, N, ldw)) return NMDLM_ERR_INVALID_ARG;
+  if (!cur_out && !s_out) return NMDLM_ERR_INVALID_ARG;
+  if (s_out && !theta_vec && theta <= 0) return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)T * M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
+  if (!ws || !aligned(ws, 256) || ws_bytes < qbsm_ws(T, M, K, N)) return NMDLM_ERR_WORKSPACE;
+
+  const int Nw = (N + 63) / 64;
+  QbsmCall c;
+  c.s_in = s_in;
+  c.T = T;
+  c.M = M;
+  c.K = K;
+  c.W = W;
+  c.ldw = ldw;
+  c.N = N;
+  c.mode = s_out ? EPI_IF : EPI_CUR;
+  c.bias = bias;
+  c.cur_out = cur_out;
+  c.theta_vec = theta_vec;
+  c.nseg = 1;
+  c.seg_w = 1 << 30;
+  for (int i = 0; i < kMaxSeg; ++i) {
+    c.seg[i].ptr = s_out;
+    c.seg[i].ld_t = (int64_t)M * Nw;
+    c.seg[i].ld_m = Nw;
+    c.seg[i].theta = theta;
+    c.seg[i].transposed = 0;
+    c.seg[i].pos0 = 0;
+    c.seg[i].pad_ = 0;
+  }
+  c.resid = nullptr;
+  c.rld_t = c.rld_m = 0;
+  c.lut = nullptr;
+  c.lut_shift = 0;
+  c.logits = nullptr;
+  c.scale = nullptr;
+  c.stats = stats;
+  c.flags = flags;
+
+  Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
+  QbsmScratch scr;
+  carve_qbsm_scratch(cv, qbsm_limits_single(T, M, K, N), &scr);
+  if (!cv.ok) return NMDLM_ERR_WORKSPACE;
+  return launch_qbsm(c, scr, static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N, int32_t theta,
+                             const int32_t* theta_vec, const uint64_t* resid, int32_t* v_inout,
+                             uint64_t* s_out, void* stream) {
+  if (!cur || !s_out || T < 1 || M < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T * 1024) return NMDLM_ERR_UNSUPPORTED;
+  if (!theta_vec && theta <= 0) return NMDLM_ERR_INVALID_ARG;
+  return launch_if(cur, T, M, N, theta, theta_vec, resid, v_inout, s_out,
+                   static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode, const uint8_t* lut,
+                           uint8_t* y, void* stream) {
+  if (n < 0 || !lut || (n > 0 && (!x || !y))) return NMDLM_ERR_INVALID_ARG;
+  if (shift < 0 || shift > 31) return NMDLM_ERR_INVALID_ARG;
+  if (mode != NMDLM_QNL_S8 && mode != NMDLM_QNL_U8) return NMDLM_ERR_INVALID_ARG;
+  return launch_qnl(x, n, shift, mode, lut, y, static_cast<hipStream_t>(stream));
+}
+
+size_t nmdlm_bbm_attn_workspace_size(int T, int M, int H, int dh) {
+  if (T < 1 || M < 1 || H < 1 || dh < 1) return 0;
+  return align_up((size_t)T * M * H * dh * sizeof(int32_t), 256);
+}
+
+nmdlm_status nmdlm_bbm_attn(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,
+                            int64_t cache_cap, int T, int M, int C, int H, int dh,
+                            const uint8_t* lut_att, int32_t* a_out, int32_t theta_a,
+                            uint64_t* s_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!q || !k_cache || !vt_cache || !lut_att) return NMDLM_ERR_INVALID_ARG;
+  if (T < 1 || M < 1 || C < 0 || H < 1 || dh < 1) return NMDLM_ERR_INVALID_ARG;
+  if (!a_out && !s_out) return NMDLM_ERR_INVALID_ARG;
+  if (s_out && theta_a <= 0) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T) return NMDLM_ERR_UNSUPPORTED;
+  if (dh != 64 && dh != 128) return NMDLM_ERR_UNSUPPORTED;
+  if (cache_cap % 64 != 0 || cache_cap < (int64_t)C + M) return NMDLM_ERR_INVALID_ARG;
+  int32_t* a = a_out;
+  if (!a) {
+    if (!ws || !aligned(ws, 256) || ws_bytes < nmdlm_bbm_attn_workspace_size(T, M, H, dh))
+      return NMDLM_ERR_WORKSPACE;
+    a = static_cast<int32_t*>(ws);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  nmdlm_status rc = launch_attn(q, k_cache, vt_cache, cache_cap, T, M, C, H, dh, lut_att, a, st);
+  if (rc != NMDLM_OK || !s_out) return rc;
+  return launch_if(a, T, M, H * dh, theta_a, nullptr, nullptr, nullptr, s_out, st);
+}
+
+size_t nmdlm_block_step_workspace_size(const nmdlm_model* model, int M, unsigned flags) {
+  if (!model || M < 1 || model->T < 1 || model->d < 64) return 0;
+  return block_step_ws_size(model, M, flags);
+}
+
+nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (!md || !io) return NMDLM_ERR_INVALID_ARG;
+  if (md->n_layers < 0 || md->T < 1 || md->d < 64 || md->H < 1 || md->F < 1 || md->V < 1)
+    return NMDLM_ERR_INVALID_ARG;
+  if (md->T > NMDLM_MAX_T) return NMDLM_ERR_UNSUPPORTED;
+  if (md->d % 64 != 0 || md->d % md->H != 0) return NMDLM_ERR_UNSUPPORTED;
+  const int dh = md->d / md->H;
+  if (dh != 64 && dh != 128) return NMDLM_ERR_UNSUPPORTED;
+  if (md->d > NMDLM_MAX_K || md->F > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
+  if (io->M < 1 || io->C < 0 || io->pos0 < 0) return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)md->T * io->M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
+  if (md->cache_cap % 64 != 0 || md->cache_cap < (int64_t)io->C + io->M)
+    return NMDLM_ERR_INVALID_ARG;
+  if (md->n_layers > 0 && !md->layers) return NMDLM_ERR_INVALID_ARG;
+  for (int l = 0; l < md->n_layers; ++l) {
+    const nmdlm_layer& L = md->layers[l];
+    if (!weights_ok(L.w_qkv, md->d, 3 * md->d, 3 * (int64_t)md->d) ||
+        !weights_ok(L.w_o, md->d, md->d, md->d) || !weights_ok(L.w_up, md->d, md->F, md->F) ||
+        !weights_ok(L.w_dn, md->F, md->d, md->d))
+      return NMDLM_ERR_INVALID_ARG;
+    if (!L.lut_att || !L.lut_act || !L.k_cache || !L.vt_cache) return NMDLM_ERR_INVALID_ARG;
+    if (L.theta_q <= 0 || L.theta_k <= 0 || L.theta_v <= 0 || L.theta_a <= 0 || L.theta_o <= 0 ||
+        L.theta_up <= 0 || L.theta_dn <= 0)
+      return NMDLM_ERR_INVALID_ARG;
+    if (L.s_up < 0 || L.s_up > 31) return NMDLM_ERR_INVALID_ARG;
+  }
+  if (!io->x_in) {
+    if (!md->emb || !md->pos_ch) return NMDLM_ERR_INVALID_ARG;
+    if (!io->tokens && !io->masked) return NMDLM_ERR_INVALID_ARG;
+    if ((int64_t)io->pos0 + io->M > md->max_pos) return NMDLM_ERR_INVALID_ARG;
+  }
+  const bool head = !(io->flags & NMDLM_NO_HEAD);
+  if (head) {
+    if (!weights_ok(md->w_head, md->d, md->V, md->V) || !md->head_scale)
+      return NMDLM_ERR_INVALID_ARG;
+    if (!io->tokens || !io->masked || io->k_unmask < 0) return NMDLM_ERR_INVALID_ARG;
+  }
+  if (!ws || !aligned(ws, 256) || ws_bytes < block_step_ws_size(md, io->M, io->flags))
+    return NMDLM_ERR_WORKSPACE;
+  return block_step_impl(md, io, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_workspace_clear(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws || !aligned(ws, 16) || ws_bytes % 16 != 0) return NMDLM_ERR_INVALID_ARG;
+  return launch_fill_zero(ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,151 @@
+// Internal declarations shared by the libnmdlm HIP sources (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "nmdlm.h"
+
+namespace nmdlm {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kMaxSeg = 3;
+constexpr int kChunkSteps = 16;   // k-steps (of 64 active rows) staged per LDS chunk
+constexpr int kTileLd = 68;       // LDS row stride (ints) of the 64-column output tile
+
+enum EpiMode : int {
+  EPI_CUR = 0,     // write int32 currents only
+  EPI_IF = 1,      // integrate-and-fire -> packed spikes
+  EPI_QNL_IF = 2,  // table non-linearity, then integrate-and-fire
+  EPI_HEAD = 3     // sum over t, fp32 dequantisation -> logits
+};
+
+// Destination of the spikes of one column segment of a product.
+//   natural    : word (t, m, w) at ptr[t*ld_t + m*ld_m + w]
+//   transposed : channel-major cache, bit (pos0+m)%64 of word (pos0+m)/64 of
+//                row ptr + t*ld_t + ch*ld_m  (ld_m = words per channel row)
+struct SpikeSeg {
+  uint64_t* ptr;
+  int64_t ld_t;
+  int64_t ld_m;
+  int32_t theta;
+  int32_t transposed;
+  int32_t pos0;
+  int32_t pad_;
+};
+
+struct QbsmArgs {
+  // operand prepared by the union/compaction kernels
+  const uint64_t* sc;        // compacted spike bits [KSmax][R], R = T*M
+  const uint32_t* act_off;   // byte offsets k*ldw of the active rows (padded with 0)
+  const int32_t* kact;       // number of active rows
+  // weights
+  const int8_t* W;
+  int64_t ldw;
+  int K, N;
+  int T, M, Mb;              // Mb tokens per row block
+  int P;                     // K splits
+  // epilogue
+  int mode;
+  const int32_t* bias;       // [N] or null
+  int32_t* cur_out;          // [T][M][N] or null
+  const int32_t* theta_vec;  // [N] or null
+  int nseg, seg_w;           // column segments of seg_w columns (multiple of 64)
+  SpikeSeg seg[kMaxSeg];
+  const uint64_t* resid;     // natural spikes, word (t, m, w) at resid[t*rld_t + m*rld_m + w]
+  int64_t rld_t, rld_m;
+  const uint8_t* lut;        // activation table (EPI_QNL_IF)
+  int lut_shift;
+  float* logits;             // EPI_HEAD: [M][N]
+  const float* scale;        // EPI_HEAD: [N]
+  int32_t* part;             // split accumulators [R][N] (zero between calls)
+  int32_t* counters;         // [gx*gy] arrival counters (zeroed by the prep kernel)
+};
+
+// Scratch used by one product (carved from a workspace).
+struct QbsmScratch {
+  uint32_t* act_off;   // [round_up(K,64)]
+  int32_t* act_idx;    // [round_up(K,64)]
+  int32_t* kact;       // [1]
+  uint64_t* sc;        // [ceil(K/64)][R]
+  int32_t* part;       // [R][N] (split products only)
+  int32_t* counters;   // [tiles]
+  size_t part_elems;
+  size_t n_counters;
+};
+
+// One product request (host side).
+struct QbsmCall {
+  const uint64_t* s_in;   // [T][M][ceil(K/64)]
+  int T, M, K;
+  const int8_t* W;
+  int64_t ldw;
+  int N;
+  int mode;
+  const int32_t* bias;
+  int32_t* cur_out;
+  const int32_t* theta_vec;
+  int nseg, seg_w;
+  SpikeSeg seg[kMaxSeg];
+  const uint64_t* resid;
+  int64_t rld_t, rld_m;
+  const uint8_t* lut;
+  int lut_shift;
+  float* logits;
+  const float* scale;
+  nmdlm_qbsm_stats* stats;
+  unsigned flags;
+};
+
+// Workspace layout helpers -------------------------------------------------
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Carver {
+  char* base;
+  size_t off;
+  size_t cap;
+  bool ok;
+  template <typename T>
+  T* take(size_t n) {
+    size_t o = align_up(off, 256);
+    size_t bytes = align_up(n * sizeof(T), 256);
+    off = o + bytes;
+    if (off > cap) ok = false;
+    return base ? reinterpret_cast<T*>(base + o) : nullptr;
+  }
+};
+
+// Sizes of the product scratch for the largest call of a sequence.
+struct QbsmLimits {
+  int Kmax;       // largest K
+  int Rmax;       // largest T*M
+  int Nmax;       // largest N
+  int tiles_max;  // largest number of (column tile, row block) tiles
+  int split_rows; // largest R that may use K splits (0: splits never used)
+  int split_N;    // largest N that may use K splits
+};
+
+QbsmLimits qbsm_limits_single(int T, int M, int K, int N);
+void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s);
+
+// Launchers (enqueue only; arguments already validated).
+nmdlm_status launch_qbsm(const QbsmCall& call, const QbsmScratch& scr, hipStream_t st);
+nmdlm_status launch_if(const int32_t* cur, int T, int M, int N, int32_t theta,
+                       const int32_t* theta_vec, const uint64_t* resid,
+                       int32_t* v_inout, uint64_t* s_out, hipStream_t st);
+nmdlm_status launch_qnl(const int32_t* x, int64_t n, int shift, int mode,
+                        const uint8_t* lut, uint8_t* y, hipStream_t st);
+nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache,
+                         const uint64_t* vt_cache, int64_t cap, int T, int M, int C,
+                         int H, int dh, const uint8_t* lut, int32_t* a_out,
+                         hipStream_t st);
+nmdlm_status launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+
+inline nmdlm_status hip_status() {
+  return hipGetLastError() == hipSuccess ? NMDLM_OK : NMDLM_ERR_HIP;
+}
+
+}  // namespace nmdlm

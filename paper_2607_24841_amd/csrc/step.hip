@@ -1,0 +1,291 @@
+// One block-denoising step (Sec. III-A, Eq. (6)) through a stack of spiking
+// layers: block input assembly, per-layer products/attention/neurons, head,
+// confidence and unmasking.  Everything stays on the device; the host only
+// enqueues work on the caller's stream.
+#include <float.h>
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace nmdlm {
+
+// X[t,m,:] = E[token_m][t] OR the position spike of (pos0+m, t); masked
+// positions use the mask token (id V).
+__global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ emb,
+                                                  const int32_t* __restrict__ pos_ch,
+                                                  const int32_t* __restrict__ tokens,
+                                                  const uint8_t* __restrict__ masked, int V, int T,
+                                                  int M, int dw, int pos0,
+                                                  uint64_t* __restrict__ X) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long total = (long long)T * M * dw;
+  if (i >= total) return;
+  const int w = (int)(i % dw);
+  const int m = (int)((i / dw) % M);
+  const int t = (int)(i / ((long long)dw * M));
+  int tok = (masked && masked[m]) ? V : (tokens ? tokens[m] : V);
+  tok = min(max(tok, 0), V);
+  uint64_t word = emb[((size_t)tok * T + t) * dw + w];
+  const int pc = pos_ch[(size_t)(pos0 + m) * T + t];
+  if ((pc >> 6) == w) word |= 1ull << (pc & 63);
+  X[i] = word;
+}
+
+// Per token: argmax of the logits (ties -> smallest id) and the largest
+// softmax probability 1 / sum_v exp(l_v - l_max) in fp64.
+__global__ __launch_bounds__(256) void k_conf(const float* __restrict__ logits, int V,
+                                              int32_t* __restrict__ pred,
+                                              double* __restrict__ conf) {
+  __shared__ float sBest[256];
+  __shared__ int sIdx[256];
+  __shared__ double sSum[256];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const float* row = logits + (size_t)m * V;
+  float best = -FLT_MAX;
+  int bi = 0x7fffffff;
+  for (int v = tid; v < V; v += 256) {
+    const float x = row[v];
+    if (x > best || (x == best && v < bi)) {
+      best = x;
+      bi = v;
+    }
+  }
+  sBest[tid] = best;
+  sIdx[tid] = bi;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) {
+      const float ob = sBest[tid + s];
+      const int oi = sIdx[tid + s];
+      if (ob > sBest[tid] || (ob == sBest[tid] && oi < sIdx[tid])) {
+        sBest[tid] = ob;
+        sIdx[tid] = oi;
+      }
+    }
+    __syncthreads();
+  }
+  const double mx = (double)sBest[0];
+  double acc = 0.0;
+  for (int v = tid; v < V; v += 256) acc += exp((double)row[v] - mx);
+  sSum[tid] = acc;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) sSum[tid] += sSum[tid + s];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    pred[m] = sIdx[0];
+    conf[m] = 1.0 / sSum[0];
+  }
+}
+
+// Reveal the k most confident masked positions (ties -> lower position).
+__global__ void k_unmask(int32_t* __restrict__ tokens, uint8_t* __restrict__ masked,
+                         const int32_t* __restrict__ pred, const double* __restrict__ conf, int M,
+                         int k, int32_t* __restrict__ chosen) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  for (int r = 0; r < k; ++r) {
+    int best = -1;
+    for (int m = 0; m < M; ++m)
+      if (masked[m] && (best < 0 || conf[m] > conf[best])) best = m;
+    if (best >= 0) {
+      tokens[best] = pred[best];
+      masked[best] = 0;
+    }
+    if (chosen) chosen[r] = best;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// workspace layout of a block step
+// ---------------------------------------------------------------------------
+struct StepBuffers {
+  uint64_t* X;      // assembled input [T][M][dw]
+  uint64_t* Q;      // [T][M][dw]
+  uint64_t* A;
+  uint64_t* X1;
+  uint64_t* Hs;     // [T][M][Fw]
+  uint64_t* Y[2];
+  int32_t* a;       // attention output [T][M][d]
+  float* logits;    // [M][V]
+  int32_t* pred;
+  double* conf;
+  QbsmScratch qs;
+};
+
+static QbsmLimits step_limits(const nmdlm_model* md, int M, unsigned flags) {
+  QbsmLimits L;
+  const int T = md->T, d = md->d, F = md->F;
+  const bool head = !(flags & NMDLM_NO_HEAD);
+  L.Kmax = std::max(d, F);
+  L.Rmax = T * M;
+  int nmax = std::max(3 * d, F);
+  if (head) nmax = std::max(nmax, md->V);
+  L.Nmax = nmax;
+  L.tiles_max = ((nmax + 63) / 64) * M;
+  L.split_rows = (T * M <= 256) ? T * M : 0;
+  L.split_N = std::max(3 * d, F);
+  return L;
+}
+
+static void carve_step(Carver& cv, const nmdlm_model* md, int M, unsigned flags, bool need_x,
+                       bool need_logits, bool need_pred, bool need_conf, StepBuffers* b) {
+  const int T = md->T, dw = md->d / 64, Fw = (md->F + 63) / 64;
+  const size_t sp = (size_t)T * M * dw;
+  b->X = need_x ? cv.take<uint64_t>(sp) : nullptr;
+  b->Q = cv.take<uint64_t>(sp);
+  b->A = cv.take<uint64_t>(sp);
+  b->X1 = cv.take<uint64_t>(sp);
+  b->Hs = cv.take<uint64_t>((size_t)T * M * Fw);
+  b->Y[0] = cv.take<uint64_t>(sp);
+  b->Y[1] = cv.take<uint64_t>(sp);
+  b->a = cv.take<int32_t>((size_t)T * M * md->d);
+  const bool head = !(flags & NMDLM_NO_HEAD);
+  b->logits = (head && need_logits) ? cv.take<float>((size_t)M * md->V) : nullptr;
+  b->pred = (head && need_pred) ? cv.take<int32_t>(M) : nullptr;
+  b->conf = (head && need_conf) ? cv.take<double>(M) : nullptr;
+  carve_qbsm_scratch(cv, step_limits(md, M, flags), &b->qs);
+}
+
+size_t block_step_ws_size(const nmdlm_model* md, int M, unsigned flags) {
+  Carver cv{nullptr, 0, (size_t)-1, true};
+  StepBuffers b;
+  carve_step(cv, md, M, flags, true, true, true, true, &b);
+  return align_up(cv.off, 256);
+}
+
+static SpikeSeg natural_seg(uint64_t* p, int64_t ld_t, int64_t ld_m, int32_t theta) {
+  SpikeSeg s;
+  s.ptr = p;
+  s.ld_t = ld_t;
+  s.ld_m = ld_m;
+  s.theta = theta;
+  s.transposed = 0;
+  s.pos0 = 0;
+  s.pad_ = 0;
+  return s;
+}
+
+static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_t* W, int64_t ldw,
+                          int N, int mode, unsigned flags, nmdlm_qbsm_stats* stats) {
+  QbsmCall c;
+  c.s_in = s_in;
+  c.T = T;
+  c.M = M;
+  c.K = K;
+  c.W = W;
+  c.ldw = ldw;
+  c.N = N;
+  c.mode = mode;
+  c.bias = nullptr;
+  c.cur_out = nullptr;
+  c.theta_vec = nullptr;
+  c.nseg = 1;
+  c.seg_w = 1 << 30;
+  for (int i = 0; i < kMaxSeg; ++i) c.seg[i] = natural_seg(nullptr, 0, 0, 1);
+  c.resid = nullptr;
+  c.rld_t = 0;
+  c.rld_m = 0;
+  c.lut = nullptr;
+  c.lut_shift = 0;
+  c.logits = nullptr;
+  c.scale = nullptr;
+  c.stats = stats;
+  c.flags = flags & NMDLM_FORCE_DENSE;
+  return c;
+}
+
+nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws, size_t ws_bytes,
+                             hipStream_t st) {
+  const int T = md->T, M = io->M, C = io->C, d = md->d, F = md->F, H = md->H;
+  const int dh = d / H, dw = d / 64, Fw = (F + 63) / 64;
+  const int64_t cap = md->cache_cap, capw = cap / 64;
+  const bool head = !(io->flags & NMDLM_NO_HEAD);
+
+  Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
+  StepBuffers b;
+  carve_step(cv, md, M, io->flags, io->x_in == nullptr, io->logits == nullptr,
+             io->pred == nullptr, io->conf == nullptr, &b);
+  if (!cv.ok) return NMDLM_ERR_WORKSPACE;
+
+  nmdlm_status rc = NMDLM_OK;
+  const uint64_t* X = io->x_in;
+  if (!X) {
+    const long long total = (long long)T * M * dw;
+    hipLaunchKernelGGL(k_assemble, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+                       md->emb, md->pos_ch, io->tokens, io->masked, md->V, T, M, dw, io->pos0, b.X);
+    if ((rc = hip_status()) != NMDLM_OK) return rc;
+    X = b.X;
+  }
+  const int64_t sp_t = (int64_t)M * dw;
+  for (int l = 0; l < md->n_layers; ++l) {
+    const nmdlm_layer& ly = md->layers[l];
+    nmdlm_qbsm_stats* stl = io->stats ? io->stats + 4 * l : nullptr;
+
+    // Q | K | V, keys and values straight into cache rows [C, C+M)
+    QbsmCall qkv = base_call(X, T, M, d, ly.w_qkv, 3 * (int64_t)d, 3 * d, EPI_IF, io->flags,
+                             stl ? stl + 0 : nullptr);
+    qkv.nseg = 3;
+    qkv.seg_w = d;
+    qkv.seg[0] = natural_seg(b.Q, sp_t, dw, ly.theta_q);
+    qkv.seg[1] = natural_seg(ly.k_cache + (int64_t)C * dw, cap * dw, dw, ly.theta_k);
+    qkv.seg[2] = natural_seg(ly.vt_cache, (int64_t)d * capw, capw, ly.theta_v);
+    qkv.seg[2].transposed = 1;
+    qkv.seg[2].pos0 = C;
+    if ((rc = launch_qbsm(qkv, b.qs, st)) != NMDLM_OK) return rc;
+
+    if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att, b.a,
+                          st)) != NMDLM_OK)
+      return rc;
+    if ((rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st)) != NMDLM_OK)
+      return rc;
+
+    QbsmCall o = base_call(b.A, T, M, d, ly.w_o, d, d, EPI_IF, io->flags, stl ? stl + 1 : nullptr);
+    o.seg[0] = natural_seg(b.X1, sp_t, dw, ly.theta_o);
+    o.resid = X;
+    o.rld_t = sp_t;
+    o.rld_m = dw;
+    if ((rc = launch_qbsm(o, b.qs, st)) != NMDLM_OK) return rc;
+
+    QbsmCall up = base_call(b.X1, T, M, d, ly.w_up, F, F, EPI_QNL_IF, io->flags,
+                            stl ? stl + 2 : nullptr);
+    up.seg[0] = natural_seg(b.Hs, (int64_t)M * Fw, Fw, ly.theta_up);
+    up.lut = ly.lut_act;
+    up.lut_shift = ly.s_up;
+    if ((rc = launch_qbsm(up, b.qs, st)) != NMDLM_OK) return rc;
+
+    uint64_t* Yl = (l == md->n_layers - 1 && io->y_out) ? io->y_out : b.Y[l & 1];
+    QbsmCall dn = base_call(b.Hs, T, M, F, ly.w_dn, d, d, EPI_IF, io->flags,
+                            stl ? stl + 3 : nullptr);
+    dn.seg[0] = natural_seg(Yl, sp_t, dw, ly.theta_dn);
+    dn.resid = b.X1;
+    dn.rld_t = sp_t;
+    dn.rld_m = dw;
+    if ((rc = launch_qbsm(dn, b.qs, st)) != NMDLM_OK) return rc;
+    X = Yl;
+  }
+
+  if (!head) {
+    if (io->y_out && md->n_layers == 0)
+      if (hipMemcpyAsync(io->y_out, X, (size_t)T * M * dw * 8, hipMemcpyDeviceToDevice, st) !=
+          hipSuccess)
+        return NMDLM_ERR_HIP;
+    return NMDLM_OK;
+  }
+  float* logits = io->logits ? io->logits : b.logits;
+  int32_t* pred = io->pred ? io->pred : b.pred;
+  double* conf = io->conf ? io->conf : b.conf;
+  QbsmCall hc = base_call(X, T, M, d, md->w_head, md->V, md->V, EPI_HEAD, io->flags,
+                          io->stats ? io->stats + 4 * md->n_layers : nullptr);
+  hc.logits = logits;
+  hc.scale = md->head_scale;
+  if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
+  hipLaunchKernelGGL(k_conf, dim3(M), dim3(256), 0, st, logits, md->V, pred, conf);
+  if ((rc = hip_status()) != NMDLM_OK) return rc;
+  hipLaunchKernelGGL(k_unmask, dim3(1), dim3(64), 0, st, io->tokens, io->masked, pred, conf, M,
+                     io->k_unmask, io->unmasked_pos);
+  return hip_status();
+}
+
+}  // namespace nmdlm

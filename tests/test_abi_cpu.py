@@ -1,0 +1,120 @@
+"""The C ABI on the host: the library loads, exports every function the
+header declares, sizes workspaces and rejects bad arguments before any HIP
+call (so these run without a GPU)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nmdlm.h")
+
+torch = pytest.importorskip("torch")
+from paper_2607_24841_amd import binding as B  # noqa: E402
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(nmdlm_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libnmdlm.so not built")
+    return B.load()
+
+
+def test_exports_every_declared_function(lib):
+    names = _declared()
+    assert set(B.EXPORTS) <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.nmdlm_abi_version() == 1
+    assert lib.nmdlm_status_string(0) == b"ok"
+    assert lib.nmdlm_status_string(3).startswith(b"workspace")
+
+
+def test_single_hip_runtime(lib):
+    assert len(B._hip_runtimes_mapped()) <= 1
+
+
+def test_workspace_sizes(lib):
+    s1 = lib.nmdlm_qbsm_workspace_size(4, 8, 512, 512)
+    s2 = lib.nmdlm_qbsm_workspace_size(4, 64, 14336, 4096)
+    assert 0 < s1 < s2 and s1 % 256 == 0
+    assert lib.nmdlm_qbsm_workspace_size(0, 8, 512, 512) == 0
+    assert lib.nmdlm_qbsm_workspace_size(4, 8, 70000, 512) == 0
+    assert lib.nmdlm_bbm_attn_workspace_size(4, 16, 16, 64) == 4 * 16 * 1024 * 4
+
+
+FAKE = 1 << 40   # never dereferenced: every call below fails validation first
+
+
+def _qbsm(lib, **kw):
+    a = dict(s_in=FAKE, T=4, M=8, K=512, W=FAKE, N=512, ldw=512, bias=None, cur=FAKE,
+             theta=256, theta_vec=None, s_out=None, stats=None, flags=0, ws=FAKE, ws_bytes=1 << 30,
+             stream=None)
+    a.update(kw)
+    return lib.nmdlm_qbsm(a["s_in"], a["T"], a["M"], a["K"], a["W"], a["N"], a["ldw"], a["bias"],
+                          a["cur"], a["theta"], a["theta_vec"], a["s_out"], a["stats"], a["flags"],
+                          a["ws"], a["ws_bytes"], a["stream"])
+
+
+def test_qbsm_argument_errors(lib):
+    assert _qbsm(lib, s_in=None) == B.NMDLM_ERR_INVALID_ARG
+    assert _qbsm(lib, T=0) == B.NMDLM_ERR_INVALID_ARG
+    assert _qbsm(lib, M=-1) == B.NMDLM_ERR_INVALID_ARG
+    assert _qbsm(lib, T=9) == B.NMDLM_ERR_UNSUPPORTED
+    assert _qbsm(lib, K=70000) == B.NMDLM_ERR_UNSUPPORTED
+    assert _qbsm(lib, ldw=500) == B.NMDLM_ERR_INVALID_ARG          # < N
+    assert _qbsm(lib, ldw=520) == B.NMDLM_ERR_INVALID_ARG          # not a multiple of 16
+    assert _qbsm(lib, W=FAKE + 4) == B.NMDLM_ERR_INVALID_ARG       # misaligned weights
+    assert _qbsm(lib, cur=None) == B.NMDLM_ERR_INVALID_ARG         # no output
+    assert _qbsm(lib, cur=None, s_out=FAKE, theta=0) == B.NMDLM_ERR_INVALID_ARG
+    assert _qbsm(lib, ws=None) == B.NMDLM_ERR_WORKSPACE
+    assert _qbsm(lib, ws_bytes=16) == B.NMDLM_ERR_WORKSPACE
+    assert _qbsm(lib, ws=FAKE + 8) == B.NMDLM_ERR_WORKSPACE        # misaligned workspace
+    assert _qbsm(lib, K=40000, N=60000, ldw=60000) == B.NMDLM_ERR_INVALID_ARG  # K*ldw >= 2^31
+
+
+def test_other_argument_errors(lib):
+    assert lib.nmdlm_if_neuron(None, 4, 1, 1, 256, None, None, None, FAKE, None) == 1
+    assert lib.nmdlm_if_neuron(FAKE, 4, 1, 1, 0, None, None, None, FAKE, None) == 1
+    assert lib.nmdlm_qnl_lut(FAKE, 10, 32, 0, FAKE, FAKE, None) == 1
+    assert lib.nmdlm_qnl_lut(FAKE, 10, 3, 7, FAKE, FAKE, None) == 1
+    assert lib.nmdlm_qnl_lut(FAKE, -1, 3, 0, FAKE, FAKE, None) == 1
+    assert lib.nmdlm_qnl_lut(None, 0, 3, 0, FAKE, None, None) == 0   # empty input: nothing to do
+    a = lambda **k: lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, k.get("cap", 576), 4, k.get("M", 16),
+                                       k.get("C", 512), 16, k.get("dh", 64), FAKE, FAKE, 256, None,
+                                       None, 0, None)
+    assert a(dh=96) == B.NMDLM_ERR_UNSUPPORTED
+    assert a(cap=512) == B.NMDLM_ERR_INVALID_ARG                   # C + M > cap
+    assert a(cap=600) == B.NMDLM_ERR_INVALID_ARG                   # cap not a multiple of 64
+    assert lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, 576, 4, 16, 512, 16, 64, FAKE, None, 256, None,
+                              None, 0, None) == 1                  # no output requested
+    assert lib.nmdlm_workspace_clear(FAKE, 17, None) == 1
+
+
+def test_block_step_argument_errors(lib):
+    L = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 200, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE, FAKE)
+    layers = (B.Layer * 1)(L)
+    m = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, layers, None, None, None, None)
+    io = B.step_io(16, 512, flags=B.NMDLM_NO_HEAD, x_in=FAKE)
+    ws_need = lib.nmdlm_block_step_workspace_size(C.byref(m), 16, B.NMDLM_NO_HEAD)
+    assert ws_need > 0
+    call = lambda mm, ii, ws=FAKE, nb=ws_need: lib.nmdlm_block_step(C.byref(mm), C.byref(ii), ws, nb, None)
+    assert lib.nmdlm_block_step(None, C.byref(io), FAKE, ws_need, None) == 1
+    assert call(m, io, nb=ws_need - 256) == B.NMDLM_ERR_WORKSPACE
+    bad = B.step_io(16, 600, flags=B.NMDLM_NO_HEAD, x_in=FAKE)      # C + M > cache_cap
+    assert call(m, bad) == 1
+    L2 = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 0, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE, FAKE)
+    m2 = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, (B.Layer * 1)(L2), None, None, None, None)
+    assert call(m2, io) == 1                                        # threshold 0
+    m3 = B.Model(1, 1024, 12, 4096, 32000, 4, 576, 0, layers, None, None, None, None)
+    assert call(m3, io) == B.NMDLM_ERR_UNSUPPORTED                  # d/H not a multiple of 64
+    head_io = B.step_io(16, 512, flags=0, x_in=FAKE)                # head without weights
+    assert call(m, head_io) == 1
+    no_in = B.step_io(16, 512, flags=B.NMDLM_NO_HEAD)               # no input and no tables
+    assert call(m, no_in) == 1

@@ -1,0 +1,105 @@
+"""GPU parity of nmdlm_qbsm (with and without the fused IF epilogue) against
+the oracle: bit-exact currents, spikes and skip statistics."""
+import numpy as np
+import pytest
+
+from oracle import nmdlm_oracle as O
+from workloads import synth
+
+from ._gpu import need_gpu, padding_bits_zero, run_qbsm
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # T, M, K, N, density
+    (1, 1, 1, 1, 0.5),
+    (4, 3, 16, 16, 0.3),
+    (2, 5, 13, 9, 0.3),
+    (4, 1, 63, 65, 0.2),
+    (4, 2, 64, 64, 0.2),
+    (4, 5, 65, 200, 0.1),
+    (3, 7, 200, 63, 0.1),
+    (1, 17, 100, 130, 0.05),
+    (4, 40, 300, 70, 0.1),       # two row blocks
+    (8, 20, 129, 190, 0.1),      # T = 8
+    (4, 8, 1000, 333, 0.005),    # heavy skipping
+    (4, 16, 1024, 1024, 0.1),
+]
+
+
+def _check(case, flags=0, theta_vec=None):
+    I_ref = O.qbsm(case.S, case.W, case.bias)
+    th = case.theta if theta_vec is None else np.asarray(theta_vec)
+    s_ref, _ = O.if_neuron(I_ref, th)
+    cur, spk, st, words, _ = run_qbsm(case.S, case.W, case.bias, theta=case.theta,
+                                      theta_vec=theta_vec, flags=flags)
+    assert np.array_equal(cur, I_ref)
+    assert np.array_equal(spk, s_ref)
+    assert padding_bits_zero(words, case.N)
+    dense = bool(flags & 1)
+    k_act = case.K if dense else O.active_rows(case.S).size
+    assert st["k_total"] == case.K and st["k_active"] == k_act and st["n"] == case.N
+    assert st["weight_bytes"] == k_act * case.N
+
+
+def test_config1_bit_exact():
+    need_gpu()
+    _check(synth.config1())
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"T{s[0]}M{s[1]}K{s[2]}N{s[3]}" for s in SHAPES])
+def test_tiny_and_ragged_shapes(shape):
+    need_gpu()
+    T, M, K, N, p = shape
+    _check(synth.make_qbsm_case(100 + K + N, T, M, K, N, p))
+
+
+@pytest.mark.parametrize("flags", [0x1, 1 << 8, 2 << 8, 7 << 8, 1 << 16, 2 << 16, 4 << 16, 8 << 16,
+                                   (3 << 8) | (1 << 16)],
+                         ids=["dense", "P1", "P2", "P7", "RT1", "RT2", "RT4", "RT8", "P3RT1"])
+def test_forced_paths_equal(flags):
+    need_gpu()
+    case = synth.make_qbsm_case(5, 4, 24, 700, 300, 0.05)
+    _check(case, flags=flags)
+
+
+def test_degenerate_inputs():
+    need_gpu()
+    c = synth.make_qbsm_case(9, 4, 8, 256, 128, 0.1)
+    c.S[:] = False                   # no spike: K_active = 0, currents = bias
+    _check(c)
+    c.S[:] = True                    # every row active
+    _check(c)
+
+
+def test_per_neuron_thresholds_and_currents_only():
+    need_gpu()
+    c = synth.make_qbsm_case(12, 4, 8, 300, 100, 0.2)
+    tv = synth.int_uniform(synth.stream(3, 3), 128, 512, (100,))
+    _check(c, theta_vec=tv)
+    cur, spk, _, _, _ = run_qbsm(c.S, c.W, None, theta=None)
+    assert spk is None and np.array_equal(cur, O.qbsm(c.S, c.W))
+
+
+def test_workspace_reuse_across_calls():
+    torch, B = need_gpu()
+    c1 = synth.make_qbsm_case(21, 4, 16, 512, 256, 0.1)
+    c2 = synth.make_qbsm_case(22, 4, 16, 512, 256, 0.3)
+    ws = B.workspace(B.nmdlm_qbsm_workspace_size(4, 16, 512, 256))
+    outs = []
+    for c in (c1, c2, c1):
+        s_in = B.to_dev_bits(synth.pack_bits(c.S))
+        W = torch.from_numpy(c.W).cuda()
+        cur = torch.empty((4, 16, 256), dtype=torch.int32, device="cuda")
+        B.nmdlm_qbsm(s_in, 4, 16, 512, W, 256, 256, cur_out=cur, flags=4 << 8, ws=ws)
+        torch.cuda.synchronize()
+        outs.append(cur.cpu().numpy())
+    assert np.array_equal(outs[0], O.qbsm(c1.S, c1.W)) and np.array_equal(outs[1], O.qbsm(c2.S, c2.W))
+    assert np.array_equal(outs[2], outs[0])
+
+
+def test_determinism():
+    need_gpu()
+    c = synth.make_qbsm_case(33, 4, 32, 2048, 2048, 0.1)
+    a = run_qbsm(c.S, c.W, c.bias, theta=300)
+    b = run_qbsm(c.S, c.W, c.bias, theta=300)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[3], b[3])
