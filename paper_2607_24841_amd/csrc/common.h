@@ -15,6 +15,8 @@ constexpr int kWave = 64;
 constexpr int kMaxSeg = 3;
 constexpr int kChunkSteps = 16;   // k-steps (of 64 active rows) staged per LDS chunk
 constexpr int kTileLd = 68;       // LDS row stride (ints) of the 64-column output tile
+constexpr int kSplitMaxRows = 256;  // K splits only for blocks of at most this many rows
+constexpr int kSplitSlots = 8;      // split slots reserved per (rows x columns) of output
 
 enum EpiMode : int {
   EPI_CUR = 0,     // write int32 currents only
@@ -61,7 +63,7 @@ struct QbsmArgs {
   int lut_shift;
   float* logits;             // EPI_HEAD: [M][N]
   const float* scale;        // EPI_HEAD: [N]
-  int32_t* part;             // split accumulators [R][N] (zero between calls)
+  int32_t* part;             // split slots [P][gy*gx][16*RT*64]
   int32_t* counters;         // [gx*gy] arrival counters (zeroed by the prep kernel)
 };
 
@@ -71,7 +73,7 @@ struct QbsmScratch {
   int32_t* act_idx;    // [round_up(K,64)]
   int32_t* kact;       // [1]
   uint64_t* sc;        // [ceil(K/64)][R]
-  int32_t* part;       // [R][N] (split products only)
+  int32_t* part;       // split slots (split products only)
   int32_t* counters;   // [tiles]
   size_t part_elems;
   size_t n_counters;

@@ -235,28 +235,28 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
   __syncthreads();
 
   if (a.P > 1) {
-    // K split across workgroups: exact int32 atomics into the zeroed
-    // accumulator; the last arriving workgroup takes (and re-zeroes) the sums.
-    for (int i = tid; i < ROWS * 64; i += 256) {
-      const int row = i >> 6, col = i & 63;
-      const int t = row / a.Mb, ml = row - t * a.Mb, m = y * a.Mb + ml, n = n0 + col;
-      if (t < a.T && m < a.M && n < a.N) {
-        const int v = sTile[row * kTileLd + phys_col(col)];
-        if (v) atomicAdd(&a.part[(size_t)(t * a.M + m) * a.N + n], v);
-      }
-    }
+    // K split across workgroups: every split stores its whole tile (zeros
+    // included) into its own slot; the last workgroup to arrive sums the
+    // slots in split order.  No slot has to be zero beforehand.
+    const size_t tile_id = (size_t)y * gridDim.x + x;
+    const size_t slot_elems = (size_t)ROWS * 64;
+    const size_t n_tiles = (size_t)gridDim.x * gridDim.y;
+    int* mine = a.part + ((size_t)z * n_tiles + tile_id) * slot_elems;
+    for (int i = tid; i < ROWS * 64; i += 256)
+      __hip_atomic_store(&mine[i], sTile[(i >> 6) * kTileLd + phys_col(i & 63)], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     __threadfence();
     __syncthreads();
-    if (tid == 0) sLast = (atomicAdd(&a.counters[y * gridDim.x + x], 1) == a.P - 1) ? 1 : 0;
+    if (tid == 0) sLast = (atomicAdd(&a.counters[tile_id], 1) == a.P - 1) ? 1 : 0;
     __syncthreads();
     if (!sLast) return;
     __threadfence();
     for (int i = tid; i < ROWS * 64; i += 256) {
-      const int row = i >> 6, col = i & 63;
-      const int t = row / a.Mb, ml = row - t * a.Mb, m = y * a.Mb + ml, n = n0 + col;
       int v = 0;
-      if (t < a.T && m < a.M && n < a.N) v = atomicExch(&a.part[(size_t)(t * a.M + m) * a.N + n], 0);
-      sTile[row * kTileLd + phys_col(col)] = v;
+      for (int p = 0; p < a.P; ++p)
+        v += __hip_atomic_load(a.part + ((size_t)p * n_tiles + tile_id) * slot_elems + i,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      sTile[(i >> 6) * kTileLd + phys_col(i & 63)] = v;
     }
     __syncthreads();
   }
@@ -364,7 +364,7 @@ QbsmLimits qbsm_limits_single(int T, int M, int K, int N) {
   L.Rmax = T * M;
   L.Nmax = N;
   L.tiles_max = ((N + 63) / 64) * M;
-  L.split_rows = (T * M <= 256) ? T * M : 0;
+  L.split_rows = (T * M <= kSplitMaxRows) ? T * M : 0;
   L.split_N = N;
   return L;
 }
@@ -375,7 +375,10 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->act_idx = cv.take<int32_t>(kpad);
   s->kact = cv.take<int32_t>(1);
   s->sc = cv.take<uint64_t>((size_t)((L.Kmax + 63) / 64) * (size_t)L.Rmax);
-  s->part_elems = (size_t)L.split_rows * (size_t)L.split_N;
+  // split slots: up to kSplitSlots tiles of (row tiles x 64 columns) per column
+  size_t rows_cap = 0;
+  if (L.split_rows > 0) rows_cap = L.split_rows <= 128 ? 16 * (size_t)pick_rt(L.split_rows) : 256;
+  s->part_elems = (size_t)kSplitSlots * rows_cap * align_up((size_t)L.split_N, 64);
   s->part = s->part_elems ? cv.take<int32_t>(s->part_elems) : nullptr;
   s->n_counters = (size_t)L.tiles_max;
   s->counters = cv.take<int32_t>(s->n_counters);
@@ -406,7 +409,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     P = std::min(P, std::max(1, Kw / 4));
   }
   P = std::max(1, std::min(P, Kw));
-  if (P > 1 && (scr.part == nullptr || (size_t)R * (size_t)c.N > scr.part_elems)) P = 1;
+  const size_t slot_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one tile slot per split
+  if (P > 1) {
+    const size_t cap = scr.part ? scr.part_elems / slot_elems : 0;
+    P = (int)std::min<size_t>((size_t)P, cap);
+    if (P < 2) P = 1;
+  }
 
   hipLaunchKernelGGL(k_union_scan, dim3(1), dim3(kPrepThreads), 0, st, c.s_in, R, Kw, c.K, dense,
                      (uint32_t)c.ldw, c.N, scr.act_off, scr.act_idx, scr.kact, c.stats,

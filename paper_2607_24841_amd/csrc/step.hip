@@ -124,7 +124,7 @@ static QbsmLimits step_limits(const nmdlm_model* md, int M, unsigned flags) {
   if (head) nmax = std::max(nmax, md->V);
   L.Nmax = nmax;
   L.tiles_max = ((nmax + 63) / 64) * M;
-  L.split_rows = (T * M <= 256) ? T * M : 0;
+  L.split_rows = (T * M <= kSplitMaxRows) ? T * M : 0;
   L.split_N = std::max(3 * d, F);
   return L;
 }
@@ -192,7 +192,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.logits = nullptr;
   c.scale = nullptr;
   c.stats = stats;
-  c.flags = flags & NMDLM_FORCE_DENSE;
+  c.flags = flags & (NMDLM_FORCE_DENSE | (0xFFu << NMDLM_SPLIT_SHIFT) | (0xFu << NMDLM_ROWTILE_SHIFT));
   return c;
 }
 

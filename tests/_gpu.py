@@ -58,3 +58,16 @@ def padding_bits_zero(words: np.ndarray, N: int) -> bool:
         return True
     last = words[..., -1]
     return bool(np.all((last >> np.uint64(N % 64)) == 0))
+
+
+def assert_same(got, want, what="array"):
+    """Element-wise equality with a short report of the first differences."""
+    got = np.asarray(got)
+    want = np.asarray(want)
+    assert got.shape == want.shape, f"{what}: shape {got.shape} != {want.shape}"
+    bad = np.argwhere(got != want)
+    if bad.size:
+        first = [tuple(int(v) for v in b) for b in bad[:5]]
+        vals = [(got[tuple(b)].item(), want[tuple(b)].item()) for b in bad[:5]]
+        raise AssertionError(f"{what}: {len(bad)} of {got.size} differ; first at {first}: "
+                             f"(got, want) = {vals}")

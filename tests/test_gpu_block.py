@@ -1,0 +1,137 @@
+"""GPU parity of nmdlm_block_step: a spiking transformer block at one
+denoising step (configuration 2, full size, with its context prefill), and a
+small MDLM with head, confidence, unmasking and block-diffusion generation."""
+import numpy as np
+import pytest
+
+from oracle import nmdlm_oracle as O
+from workloads import synth
+
+from ._gpu import assert_same, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _caches_to_host(dm, T, d, J):
+    from paper_2607_24841_amd import binding as B
+    ks, vs = [], []
+    for l in dm.layers:
+        ks.append(synth.unpack_bits(B.from_dev_bits(l.k_cache), d)[:, :J])
+        vt = synth.unpack_bits(B.from_dev_bits(l.vt_cache), dm.cache_cap)   # [T][d][cap]
+        vs.append(vt.transpose(0, 2, 1)[:, :J])
+    return ks, vs
+
+
+def _run_block_case(case, flags=0):
+    torch, B = need_gpu()
+    L = case.layer
+    T, C, M, d = case.T, case.C, case.M, L.d
+    dm = B.DeviceModel([L], T, C + M, d, L.H, L.F)
+    nb = max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
+             B.nmdlm_block_step_workspace_size(dm, M, B.NMDLM_NO_HEAD))
+    ws = B.workspace(nb)
+    xc = B.to_dev_bits(synth.pack_bits(case.X_ctx))
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD | flags, x_in=xc), ws)
+    xb = B.to_dev_bits(synth.pack_bits(case.X_blk))
+    y = torch.zeros((T, M, d // 64), dtype=torch.int64, device="cuda")
+    stats = torch.zeros((4, 4), dtype=torch.int64, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, C, flags=B.NMDLM_NO_HEAD | flags, x_in=xb, y_out=y,
+                                     stats=stats), ws)
+    torch.cuda.synchronize()
+    return dm, synth.unpack_bits(B.from_dev_bits(y), d), stats.cpu().numpy()
+
+
+def _oracle_block_case(case):
+    L = case.layer
+    kc, vc = O.new_caches(1, case.T, case.C + case.M, L.d)
+    O.prefill(case.X_ctx, [L], kc, vc)
+    tr = O.layer_forward(case.X_blk, L, kc[0], vc[0], case.C)
+    return tr, kc[0], vc[0]
+
+
+def _check_block(case, flags=0):
+    dm, Y, stats = _run_block_case(case, flags)
+    tr, kref, vref = _oracle_block_case(case)
+    assert_same(Y, tr.Y, 'Y')
+    ks, vs = _caches_to_host(dm, case.T, case.layer.d, case.C + case.M)
+    assert_same(ks[0], kref, 'K cache')
+    assert_same(vs[0], vref, 'V cache')
+    dense = bool(flags & 1)
+    for i, key in enumerate(("qkv", "o", "up", "dn")):
+        K = tr.unions[key].size
+        assert stats[i, 0] == K
+        assert stats[i, 1] == (K if dense else int(tr.unions[key].sum()))
+
+
+def test_block_small_shapes():
+    need_gpu()
+    case = synth.config2(seed=7, C=70, M=5, d=128, H=2, F=256)
+    _check_block(case)
+    _check_block(case, flags=1)
+
+
+def test_config2_full_size():
+    need_gpu()
+    _check_block(synth.config2())
+
+
+@pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16)], ids=["P1", "P3", "P2RT1"])
+def test_config2_forced_paths(flags):
+    need_gpu()
+    _check_block(synth.config2(), flags=flags)
+
+
+# ----------------------------------------------------------------------------
+# small MDLM: head, confidence, unmasking, generation
+# ----------------------------------------------------------------------------
+def _tiny(seed=31, n_layers=2, V=64, d=128, F=256):
+    return synth.make_mdlm(seed, n_layers, d=d, H=2, F=F, V=V, T=4, max_pos=64)
+
+
+def test_mdlm_step_with_head():
+    torch, B = need_gpu()
+    m = _tiny()
+    emb = O.unpack_model_emb(m)
+    P, M, k = 12, 8, 3
+    prompt = synth.random_tokens(3, P, m.V)
+    # oracle
+    kc, vc = O.new_caches(m.n_layers, m.T, P + M, m.d)
+    O.prefill(O.block_input(prompt, np.arange(P), emb, m.pos_ch), m.layers, kc, vc)
+    tok0 = np.array([0, 7, 0, 0, 3, 0, 0, 0], dtype=np.int32)
+    msk0 = np.array([1, 0, 1, 1, 0, 1, 1, 1], dtype=bool)
+    ref = O.block_step(m, emb, tok0, msk0, P, P, kc, vc, k)
+    # GPU
+    dm = B.DeviceModel.from_mdlm(m, P + M)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, P, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, 0)))
+    pr = torch.from_numpy(prompt.astype(np.int32)).cuda()
+    B.nmdlm_block_step(dm, B.step_io(P, 0, flags=B.NMDLM_NO_HEAD, tokens=pr,
+                                     masked=torch.zeros(P, dtype=torch.uint8, device="cuda")), ws)
+    tok = torch.from_numpy(tok0).cuda()
+    msk = torch.from_numpy(msk0.astype(np.uint8)).cuda()
+    logits = torch.empty((M, m.V), dtype=torch.float32, device="cuda")
+    pred = torch.empty(M, dtype=torch.int32, device="cuda")
+    conf = torch.empty(M, dtype=torch.float64, device="cuda")
+    chosen = torch.empty(k, dtype=torch.int32, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, P, pos0=P, tokens=tok, masked=msk, k_unmask=k,
+                                     logits=logits, pred=pred, conf=conf, unmasked_pos=chosen), ws)
+    torch.cuda.synchronize()
+    assert_same(logits.cpu().numpy(), ref.logits, 'logits')          # exact fp32
+    assert_same(pred.cpu().numpy(), ref.pred, 'pred')
+    assert np.allclose(conf.cpu().numpy(), ref.conf, rtol=1e-12, atol=0)
+    assert np.array_equal(chosen.cpu().numpy(), ref.chosen)
+    assert np.array_equal(tok.cpu().numpy(), ref.tokens)
+    assert np.array_equal(msk.cpu().numpy().astype(bool), ref.masked)
+
+
+def test_mdlm_generation_matches_oracle():
+    need_gpu()
+    from paper_2607_24841_amd import binding as B
+    from paper_2607_24841_amd.generate import generate
+    m = _tiny(seed=32)
+    prompt = synth.random_tokens(4, 20, m.V)
+    ids_ref, log_ref = O.generate(m, prompt, n_blocks=3, B=8, steps=4, k_unmask=2)
+    dm = B.DeviceModel.from_mdlm(m, 20 + 24)
+    ids, log = generate(dm, prompt, n_blocks=3, block=8, steps=4, k_unmask=2)
+    assert_same(ids, ids_ref)
+    assert all(np.array_equal(a, b) for a, b in zip(log, log_ref))

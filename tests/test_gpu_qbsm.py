@@ -6,7 +6,7 @@ import pytest
 from oracle import nmdlm_oracle as O
 from workloads import synth
 
-from ._gpu import need_gpu, padding_bits_zero, run_qbsm
+from ._gpu import assert_same, need_gpu, padding_bits_zero, run_qbsm
 
 pytestmark = pytest.mark.gpu
 
@@ -32,8 +32,8 @@ def _check(case, flags=0, theta_vec=None):
     s_ref, _ = O.if_neuron(I_ref, th)
     cur, spk, st, words, _ = run_qbsm(case.S, case.W, case.bias, theta=case.theta,
                                       theta_vec=theta_vec, flags=flags)
-    assert np.array_equal(cur, I_ref)
-    assert np.array_equal(spk, s_ref)
+    assert_same(cur, I_ref)
+    assert_same(spk, s_ref)
     assert padding_bits_zero(words, case.N)
     dense = bool(flags & 1)
     k_act = case.K if dense else O.active_rows(case.S).size
@@ -94,7 +94,7 @@ def test_workspace_reuse_across_calls():
         torch.cuda.synchronize()
         outs.append(cur.cpu().numpy())
     assert np.array_equal(outs[0], O.qbsm(c1.S, c1.W)) and np.array_equal(outs[1], O.qbsm(c2.S, c2.W))
-    assert np.array_equal(outs[2], outs[0])
+    assert_same(outs[2], outs[0])
 
 
 def test_determinism():
