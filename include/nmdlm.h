@@ -50,6 +50,9 @@ typedef enum nmdlm_status {
 /* bits 16..19: force rows per tile group (0 = automatic; 1,2,4,8 = 16..128
  * rows).  Results do not depend on it. */
 #define NMDLM_ROWTILE_SHIFT 16u
+/* bit 20: build the active-row list in a separate pass instead of inside the
+ * product kernel.  Results do not depend on it. */
+#define NMDLM_NO_FUSE 0x100000u
 
 /* Supported envelope (NMDLM_ERR_UNSUPPORTED beyond it). */
 #define NMDLM_MAX_T 8
@@ -234,6 +237,11 @@ typedef struct nmdlm_step_io {
                               selection order, -1 when fewer were masked    */
   nmdlm_qbsm_stats* stats; /* device [4*n_layers + 1] or NULL: per product
                               (QKV, O, up, down per layer, then the head)  */
+  void** prof_events;      /* HOST array of hipEvent_t or NULL: when given,
+                              events 2i and 2i+1 are recorded on the stream
+                              just before and after the main kernel of
+                              product i (same order as stats), for timing  */
+  int n_prof_events;       /* length of prof_events                         */
 } nmdlm_step_io;
 
 nmdlm_status nmdlm_block_step(const nmdlm_model* model, nmdlm_step_io* io,

@@ -27,6 +27,7 @@ NMDLM_FORCE_DENSE = 0x1
 NMDLM_NO_HEAD = 0x2
 NMDLM_SPLIT_SHIFT = 8
 NMDLM_ROWTILE_SHIFT = 16
+NMDLM_NO_FUSE = 0x100000
 NMDLM_QNL_S8 = 0
 NMDLM_QNL_U8 = 1
 
@@ -75,7 +76,7 @@ class StepIO(C.Structure):
         ("x_in", C.c_void_p), ("tokens", C.c_void_p), ("masked", C.c_void_p),
         ("k_unmask", C.c_int), ("y_out", C.c_void_p), ("logits", C.c_void_p),
         ("pred", C.c_void_p), ("conf", C.c_void_p), ("unmasked_pos", C.c_void_p),
-        ("stats", C.c_void_p),
+        ("stats", C.c_void_p), ("prof_events", C.POINTER(C.c_void_p)), ("n_prof_events", C.c_int),
     ]
 
 
@@ -279,6 +280,42 @@ class DeviceModel:
 
 
 def step_io(M, C_, pos0=0, flags=0, x_in=None, tokens=None, masked=None, k_unmask=0, y_out=None,
-            logits=None, pred=None, conf=None, unmasked_pos=None, stats=None) -> StepIO:
+            logits=None, pred=None, conf=None, unmasked_pos=None, stats=None,
+            prof_events=None) -> StepIO:
+    """prof_events: optional ctypes array of hipEvent_t handles (see HipEvents)."""
+    ev = prof_events if prof_events is not None else None
     return StepIO(M, C_, pos0, flags, ptr(x_in), ptr(tokens), ptr(masked), k_unmask, ptr(y_out),
-                  ptr(logits), ptr(pred), ptr(conf), ptr(unmasked_pos), ptr(stats))
+                  ptr(logits), ptr(pred), ptr(conf), ptr(unmasked_pos), ptr(stats),
+                  ev, 0 if ev is None else len(ev))
+
+
+class HipEvents:
+    """Raw hipEvent_t handles from the HIP runtime already loaded by torch,
+    for timing kernels that the library launches on a stream."""
+
+    def __init__(self, n: int):
+        self.hip = C.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+        self.arr = (C.c_void_p * n)()
+        for i in range(n):
+            h = C.c_void_p()
+            if self.hip.hipEventCreate(C.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.arr[i] = h
+
+    def __len__(self):
+        return len(self.arr)
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        self.hip.hipEventSynchronize(self.arr[j])
+        out = C.c_float()
+        if self.hip.hipEventElapsedTime(C.byref(out), self.arr[i], self.arr[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(out.value)
+
+    def close(self):
+        for h in self.arr:
+            self.hip.hipEventDestroy(h)

@@ -96,6 +96,11 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
   c.scale = nullptr;
   c.stats = stats;
   c.flags = flags;
+  c.ev_begin = nullptr;
+  c.ev_end = nullptr;
+  c.u_in = nullptr;
+  c.u_nparts = 0;
+  c.u_out = nullptr;
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
   QbsmScratch scr;

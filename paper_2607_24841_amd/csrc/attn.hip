@@ -62,18 +62,25 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
   for (int jc = wave; jc < nch; jc += 4) {
     const int j0 = jc * 64 + 16 * g;
     uint32_t pk[4] = {0u, 0u, 0u, 0u};
+    // keys past C+M read a valid row (clamped) and are masked, so that all
+    // sixteen key loads are issued back to back
+    uint64_t kw[16][DHW];
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
-      const int j = j0 + s;
-      if (j < J) {
-        const uint64_t* kr = kc + ((size_t)t * cap + j) * dw + h * DHW;
-        int sc = 0;
+      const int jj = min(j0 + s, J - 1);
+      const uint64_t* kr = kc + ((size_t)t * cap + jj) * dw + h * DHW;
 #pragma unroll
-        for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & kr[w]);
-        const int p = sLut[sc];
-        den += p;
-        pk[s >> 2] |= (uint32_t)((p - 128) & 0xFF) << ((s & 3) * 8);
-      }
+      for (int w = 0; w < DHW; ++w) kw[s][w] = kr[w];
+    }
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      int sc = 0;
+#pragma unroll
+      for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & kw[s][w]);
+      const bool jv = j0 + s < J;
+      const int p = jv ? sLut[sc] : 0;
+      den += p;
+      pk[s >> 2] |= jv ? (uint32_t)((p - 128) & 0xFF) << ((s & 3) * 8) : 0u;
     }
     const v4i af = v4i{(int)pk[0], (int)pk[1], (int)pk[2], (int)pk[3]};
     const int nvalid = J - j0;

@@ -65,6 +65,14 @@ struct QbsmArgs {
   const float* scale;        // EPI_HEAD: [N]
   int32_t* part;             // split slots [P][gy*gx][16*RT*64]
   int32_t* counters;         // [gx*gy] arrival counters (zeroed by the prep kernel)
+  uint64_t* u_out;           // partial unions of the output spikes [gy][u_ld] or null
+  int u_ld;
+  // single-kernel product: union sources and statistics
+  const uint64_t* S;         // input spikes [R][ceil(K/64)]
+  const uint64_t* upart;     // partial unions [nparts][ceil(K/64)] or null
+  int nparts;
+  int dense;
+  nmdlm_qbsm_stats* stats;
 };
 
 // Scratch used by one product (carved from a workspace).
@@ -73,6 +81,7 @@ struct QbsmScratch {
   int32_t* act_idx;    // [round_up(K,64)]
   int32_t* kact;       // [1]
   uint64_t* sc;        // [ceil(K/64)][R]
+  uint64_t* U;         // [ceil(K/64)] union of a large block
   int32_t* part;       // split slots (split products only)
   int32_t* counters;   // [tiles]
   size_t part_elems;
@@ -100,6 +109,11 @@ struct QbsmCall {
   const float* scale;
   nmdlm_qbsm_stats* stats;
   unsigned flags;
+  hipEvent_t ev_begin;    // recorded around the product kernel when non-null
+  hipEvent_t ev_end;
+  const uint64_t* u_in;   // partial unions of s_in [u_nparts][ceil(K/64)] or null
+  int u_nparts;
+  uint64_t* u_out;        // where to write the partial unions of the output
 };
 
 // Workspace layout helpers -------------------------------------------------
@@ -134,10 +148,14 @@ QbsmLimits qbsm_limits_single(int T, int M, int K, int N);
 void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s);
 
 // Launchers (enqueue only; arguments already validated).
-nmdlm_status launch_qbsm(const QbsmCall& call, const QbsmScratch& scr, hipStream_t st);
+// gy_out (optional): row blocks used, i.e. the number of partial unions
+// written to call.u_out.
+nmdlm_status launch_qbsm(const QbsmCall& call, const QbsmScratch& scr, hipStream_t st,
+                         int* gy_out = nullptr);
 nmdlm_status launch_if(const int32_t* cur, int T, int M, int N, int32_t theta,
                        const int32_t* theta_vec, const uint64_t* resid,
-                       int32_t* v_inout, uint64_t* s_out, hipStream_t st);
+                       int32_t* v_inout, uint64_t* s_out, hipStream_t st,
+                       uint64_t* u_out = nullptr);
 nmdlm_status launch_qnl(const int32_t* x, int64_t n, int shift, int mode,
                         const uint8_t* lut, uint8_t* y, hipStream_t st);
 nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache,

@@ -10,7 +10,8 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
                                             int32_t theta, const int32_t* __restrict__ theta_vec,
                                             const uint64_t* __restrict__ resid,
                                             int32_t* __restrict__ v_inout,
-                                            uint64_t* __restrict__ s_out) {
+                                            uint64_t* __restrict__ s_out,
+                                            uint64_t* __restrict__ u_out) {
   const int Nw = (N + 63) / 64;
   const long long unit = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (unit >= (long long)M * Nw) return;  // wave-uniform
@@ -20,6 +21,7 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
   const bool nv = n < N;
   const long long th = theta_vec ? (nv ? theta_vec[n] : 1) : theta;
   long long V = (v_inout && nv) ? v_inout[(size_t)m * N + n] : 0;
+  uint64_t uor = 0;
   for (int t = 0; t < T; ++t) {
     long long I = nv ? cur[((size_t)t * M + m) * N + n] : 0;
     if (resid && ((resid[((size_t)t * M + m) * Nw + w] >> lane) & 1ull)) I += th;
@@ -27,9 +29,12 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
     const bool s = nv && V >= th;
     if (s) V -= th;
     const uint64_t word = __builtin_amdgcn_ballot_w64(s);
+    uor |= word;
     if (lane == 0) s_out[((size_t)t * M + m) * Nw + w] = word;
   }
   if (v_inout && nv) v_inout[(size_t)m * N + n] = (int32_t)V;
+  // partial union over t of this token's word, for a following product
+  if (u_out && lane == 0) u_out[(size_t)m * Nw + w] = uor;
 }
 
 __global__ __launch_bounds__(256) void k_qnl(const int32_t* __restrict__ x, int64_t n, int shift,
@@ -58,11 +63,11 @@ __global__ __launch_bounds__(256) void k_fill_zero(uint4* __restrict__ p, size_t
 
 nmdlm_status launch_if(const int32_t* cur, int T, int M, int N, int32_t theta,
                        const int32_t* theta_vec, const uint64_t* resid, int32_t* v_inout,
-                       uint64_t* s_out, hipStream_t st) {
+                       uint64_t* s_out, hipStream_t st, uint64_t* u_out) {
   const long long units = (long long)M * ((N + 63) / 64);
   const long long blocks = (units + 3) / 4;
   hipLaunchKernelGGL(k_if, dim3((unsigned)blocks), dim3(256), 0, st, cur, T, M, N, theta,
-                     theta_vec, resid, v_inout, s_out);
+                     theta_vec, resid, v_inout, s_out, u_out);
   return hip_status();
 }
 

@@ -2,121 +2,201 @@
 //
 // Sec. IV-A: Y = X W over the B*T spike rows of a block; by assumption (ii) a
 // weight row is read only if its input neuron spikes somewhere in the block.
-// Three kernels per product:
-//   k_union_scan  OR of all T*M spike rows -> ascending active-row list
-//   k_compact     spike bits gathered onto the active rows, k-step major
-//   k_qbsm        int8 MFMA over (T*M) x K_active x N with a fused epilogue
-//                 (currents, integrate-and-fire, table + IF, or head logits)
+// Two kernels per product:
+//   k_prep   block union (from producer partial unions or the spikes),
+//            active-row list and compaction of the spike bits onto it
+//   k_qbsm   int8 MFMA over (T*M) x K_active x N with a fused epilogue
+//            (currents, integrate-and-fire, table + IF, or head logits) that
+//            also emits the partial union of its output spikes
+// (k_union ORs very large spike blocks first, e.g. a long prefill.)
 #include "common.h"
 
 namespace nmdlm {
 
-constexpr int kPrepThreads = 1024;
 constexpr int kMaxWords = NMDLM_MAX_K / 64;
-constexpr int kCompactRows = 64;
+constexpr int kPrepRows = 64;      // rows compacted per prep workgroup
+constexpr int kUnionDirect = 8192; // words of S a prep workgroup ORs itself
 
 // ---------------------------------------------------------------------------
-// Block union and the active-row list.  One workgroup: the inputs of a block
-// step are at most a few hundred rows of <= 1024 words.
+// Column OR of a large spike block (used when R*Kw is too large for every
+// prep workgroup to recompute it): U[w] = OR_r S[r][w].  Block w.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kPrepThreads) void k_union_scan(
-    const uint64_t* __restrict__ S, int R, int Kw, int K, int dense, uint32_t ldw, int N,
-    uint32_t* __restrict__ act_off, int32_t* __restrict__ act_idx, int32_t* __restrict__ kact,
-    nmdlm_qbsm_stats* __restrict__ stats, int32_t* __restrict__ counters, int n_counters) {
-  __shared__ unsigned long long sU[kMaxWords];
-  __shared__ int sWaveSum[kPrepThreads / kWave];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-
-  for (int i = tid; i < n_counters; i += kPrepThreads) counters[i] = 0;
-  for (int w = tid; w < Kw; w += kPrepThreads) sU[w] = dense ? ~0ull : 0ull;
+__global__ __launch_bounds__(256) void k_union(const uint64_t* __restrict__ S, int R, int Kw,
+                                               uint64_t* __restrict__ U) {
+  __shared__ unsigned long long sAcc[256];
+  const int w = blockIdx.x, tid = threadIdx.x;
+  unsigned long long acc = 0;
+  for (int r = tid; r < R; r += 256) acc |= S[(size_t)r * Kw + w];
+  sAcc[tid] = acc;
   __syncthreads();
-  if (!dense) {
-    const int rg = kPrepThreads / Kw;  // row groups (Kw <= 1024)
-    const int w = tid % Kw, r0 = tid / Kw;
-    if (r0 < rg) {
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) sAcc[tid] |= sAcc[tid + s];
+    __syncthreads();
+  }
+  if (tid == 0) U[w] = sAcc[0];
+}
+
+// Position of the r-th (0-based) set bit of u (r < popcount(u)).
+__device__ __forceinline__ int select_bit(unsigned long long u, int r) {
+  int pos = 0;
+  uint32_t v = (uint32_t)u;
+  int c = __popc(v);
+  if (r >= c) {
+    r -= c;
+    pos = 32;
+    v = (uint32_t)(u >> 32);
+  }
+  c = __popc(v & 0xFFFFu);
+  if (r >= c) { r -= c; pos += 16; v >>= 16; }
+  c = __popc(v & 0xFFu);
+  if (r >= c) { r -= c; pos += 8; v >>= 8; }
+  c = __popc(v & 0xFu);
+  if (r >= c) { r -= c; pos += 4; v >>= 4; }
+  c = __popc(v & 0x3u);
+  if (r >= c) { r -= c; pos += 2; v >>= 2; }
+  if (r >= (int)(v & 1u)) pos += 1;
+  return pos;
+}
+
+struct PrepArgs {
+  const uint64_t* S;       // [R][Kw] spikes
+  int R, Kw, K;
+  const uint64_t* upart;   // [nparts][Kw] partial unions, or null (OR S directly)
+  int nparts;
+  int dense;               // every row active
+  uint32_t ldw;
+  int N;
+  uint32_t* act_off;       // [round_up(K,64)]
+  int32_t* act_idx;
+  int32_t* kact;
+  nmdlm_qbsm_stats* stats;
+  int32_t* counters;
+  int n_counters;
+  uint64_t* sc;            // [Kw][R]
+};
+
+// ---------------------------------------------------------------------------
+// Block union, active-row list and compaction in one pass.  Block (j, y):
+// every workgroup forms the union (from producer partial unions when given)
+// and its prefix popcounts, locates active rows 64j..64j+63 by binary search
+// over the prefix sums, and gathers the spike bits of rows [64y, 64y+64) onto
+// them: sc[j][r] bit i = S[r][act[64j + i]].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_prep(PrepArgs p) {
+  __shared__ unsigned long long sU[kMaxWords];
+  __shared__ int sP[kMaxWords + 1];
+  __shared__ int sWave[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Kw = p.Kw;
+
+  if (p.dense) {
+    for (int w = tid; w < Kw; w += 256) sU[w] = ~0ull;
+  } else if (p.upart) {
+    for (int w = tid; w < Kw; w += 256) {
       unsigned long long acc = 0;
-      for (int r = r0; r < R; r += rg) acc |= S[(size_t)r * Kw + w];
-      if (acc) atomicOr(&sU[w], acc);
+      for (int q = 0; q < p.nparts; ++q) acc |= p.upart[(size_t)q * Kw + w];
+      sU[w] = acc;
+    }
+  } else {
+    for (int w = tid; w < Kw; w += 256) sU[w] = 0ull;
+    __syncthreads();
+    if (Kw <= 256) {
+      const int rg = 256 / Kw, w = tid % Kw, r0 = tid / Kw;
+      if (r0 < rg) {
+        unsigned long long acc = 0;
+        for (int r = r0; r < p.R; r += rg) acc |= p.S[(size_t)r * Kw + w];
+        if (acc) atomicOr(&sU[w], acc);
+      }
+    } else {
+      for (int w = tid; w < Kw; w += 256) {
+        unsigned long long acc = 0;
+        for (int r = 0; r < p.R; ++r) acc |= p.S[(size_t)r * Kw + w];
+        sU[w] = acc;
+      }
     }
   }
   __syncthreads();
-  if (tid == 0 && (K & 63)) sU[Kw - 1] &= (1ull << (K & 63)) - 1ull;
+  if (tid == 0 && (p.K & 63)) sU[Kw - 1] &= (1ull << (p.K & 63)) - 1ull;
   __syncthreads();
 
-  // exclusive prefix sum of the per-word popcounts (one word per thread)
-  const int cnt = tid < Kw ? __popcll(sU[tid]) : 0;
-  int incl = cnt;
+  // exclusive prefix sums of popcounts: thread t owns words 4t..4t+3
+  int cw[4], s = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int w = 4 * tid + i;
+    cw[i] = w < Kw ? __popcll(sU[w]) : 0;
+    s += cw[i];
+  }
+  int incl = s;
   for (int o = 1; o < kWave; o <<= 1) {
     const int v = __shfl_up(incl, o);
     if (lane >= o) incl += v;
   }
-  if (lane == kWave - 1) sWaveSum[wave] = incl;
+  if (lane == kWave - 1) sWave[wave] = incl;
   __syncthreads();
   int before = 0, total = 0;
-  for (int i = 0; i < kPrepThreads / kWave; ++i) {
-    if (i < wave) before += sWaveSum[i];
-    total += sWaveSum[i];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (i < wave) before += sWave[i];
+    total += sWave[i];
   }
-  if (tid < Kw) {
-    unsigned long long u = sU[tid];
-    int o = before + incl - cnt;
-    while (u) {
-      const int b = __ffsll((unsigned long long)u) - 1;
-      const int k = tid * 64 + b;
-      act_off[o] = (uint32_t)k * ldw;
-      act_idx[o] = k;
-      ++o;
-      u &= u - 1ull;
-    }
+  int run = before + incl - s;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int w = 4 * tid + i;
+    if (w < Kw) sP[w] = run;
+    run += cw[i];
   }
-  // pad the list to whole k-steps with row 0 (its spike bits are zero)
-  const int padded = (total + 63) & ~63;
-  for (int i = total + tid; i < padded; i += kPrepThreads) {
-    act_off[i] = 0u;
-    act_idx[i] = -1;
-  }
-  if (tid == 0) {
-    *kact = total;
-    if (stats) {
-      stats->k_total = K;
-      stats->k_active = total;
-      stats->n = N;
-      stats->weight_bytes = (int64_t)total * (int64_t)N;
-    }
-  }
-}
+  if (tid == 0) sP[Kw] = total;
+  __syncthreads();
 
-// ---------------------------------------------------------------------------
-// Compaction: sc[j][r] bit i = S[r][act[64 j + i]].  Block (j, row range).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ S, int R, int Kw,
-                                                 const int32_t* __restrict__ act_idx,
-                                                 const int32_t* __restrict__ kact,
-                                                 uint64_t* __restrict__ sc) {
-  const int j = blockIdx.x;
-  const int ka = *kact;
-  if (j * 64 >= ka) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = blockIdx.x, y = blockIdx.y;
+  if (j == 0 && y == 0) {
+    for (int i = tid; i < p.n_counters; i += 256) p.counters[i] = 0;
+    if (tid == 0) {
+      *p.kact = total;
+      if (p.stats) {
+        p.stats->k_total = p.K;
+        p.stats->k_active = total;
+        p.stats->n = p.N;
+        p.stats->weight_bytes = (int64_t)total * (int64_t)p.N;
+      }
+    }
+  }
+  if (j * 64 >= total) return;
+
   const int i = j * 64 + lane;
-  const int idx = i < ka ? act_idx[i] : -1;
-  const int wi = idx >= 0 ? (idx >> 6) : 0;
-  const int bi = idx & 63;
-  const int r0 = blockIdx.y * kCompactRows;
-  const int r1 = min(R, r0 + kCompactRows);
-  for (int r = r0 + wave; r < r1; r += 4) {
-    const uint64_t word = S[(size_t)r * Kw + wi];
-    const bool bit = idx >= 0 && ((word >> bi) & 1ull);
+  const bool valid = i < total;
+  int k = 0;
+  if (valid) {
+    int lo = 0, hi = Kw - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (sP[mid] <= i) lo = mid;
+      else hi = mid - 1;
+    }
+    k = lo * 64 + select_bit(sU[lo], i - sP[lo]);
+  }
+  if (y == 0 && wave == 0) {
+    p.act_off[i] = valid ? (uint32_t)k * p.ldw : 0u;
+    p.act_idx[i] = valid ? k : -1;
+  }
+  const int wi = k >> 6, bi = k & 63;
+  const int r1 = min(p.R, (y + 1) * kPrepRows);
+  for (int r = y * kPrepRows + wave; r < r1; r += 4) {
+    const uint64_t word = p.S[(size_t)r * Kw + wi];
+    const bool bit = valid && ((word >> bi) & 1ull);
     const uint64_t m = __builtin_amdgcn_ballot_w64(bit);
-    if (lane == 0) sc[(size_t)j * R + r] = m;
+    if (lane == 0) p.sc[(size_t)j * p.R + r] = m;
   }
 }
 
 // ---------------------------------------------------------------------------
 // The product.
 //
-// Workgroup = 4 waves, tile = (16*RT rows of the block) x (64 columns).  The
-// waves take k-steps (64 active rows each) in turn and reduce in LDS.
+// Workgroup = NW waves, tile = (16*RT rows of the block) x (64 columns).  The
+// waves take groups of kGroup k-steps (64 active rows each) and reduce in
+// LDS; a group's weight and spike loads are all issued before any is used.
 // Per k-step a lane (g = lane/16, c = lane%16) loads, for the 16 active rows
 // k_{g,0..15}, the dword W[k][n0+4c .. n0+4c+3]; an in-register 4x4 byte
 // transpose turns these into four MFMA B operands whose column c stands for
@@ -125,6 +205,10 @@ __global__ __launch_bounds__(256) void k_compact(const uint64_t* __restrict__ S,
 // accumulates exactly in int32; output element (lane, e) is row 4g + e.
 // Block rows are ordered t-major: local row r -> (t = r / Mb, token r % Mb).
 // ---------------------------------------------------------------------------
+constexpr int kGroup = 4;
+constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
+constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
+
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
   // 4 bits -> 4 bytes of 0/1 (bit i -> byte i); the shifted copies of the
   // nibble do not overlap, so the multiply adds no carries.
@@ -133,32 +217,111 @@ __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
 
 __device__ __forceinline__ int phys_col(int col) { return (col & 3) * 16 + (col >> 2); }
 
-template <int RT>
-__global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
+template <int RT, int NW, bool FUSED>
+__global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
+  constexpr int NT = NW * 64;
+  constexpr int CH = NW * kGroup;  // k-steps staged per chunk
   __shared__ int sTile[ROWS * kTileLd];
-  __shared__ uint32_t sOff[kChunkSteps * 64];
+  __shared__ __attribute__((aligned(16))) uint32_t sOff[CH * 64];
+  __shared__ __attribute__((aligned(16))) int sIdx[FUSED ? CH * 64 : 4];
+  __shared__ unsigned long long sU[FUSED ? kFusedMaxWords : 1];
+  __shared__ int sP[FUSED ? kFusedMaxWords + 1 : 1];
+  __shared__ int sWave[NW];
+  __shared__ unsigned long long sUn[NW];
   __shared__ int sLast;
+  // FUSED: this tile's spike rows as dwords, row stride 2*Kw+1 (odd, so the
+  // 16 rows a wave gathers from fall in different banks)
+  extern __shared__ uint32_t sS[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
   const int n0 = x * 64;
   const int R = a.T * a.M;
+  const int Kw = (a.K + 63) >> 6;
 
-  for (int i = tid; i < ROWS * kTileLd; i += 256) sTile[i] = 0;
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
 
-  const int ka = *a.kact;
+  int ka;
+  if constexpr (FUSED) {
+    // this tile's spike rows, and the block union (from producer partial
+    // unions, or by OR-ing every spike row), then prefix popcounts
+    const int lds_row = 2 * Kw + 1;
+    for (int i = tid; i < ROWS * Kw; i += NT) {
+      const int lr = i / Kw, w = i - lr * Kw;
+      const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
+      const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
+      sS[lr * lds_row + 2 * w] = (uint32_t)v;
+      sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
+    }
+    if (a.dense) {
+      for (int w = tid; w < Kw; w += NT) sU[w] = ~0ull;
+    } else if (a.upart) {
+      for (int w = tid; w < Kw; w += NT) {
+        unsigned long long u = 0;
+        for (int q = 0; q < a.nparts; ++q) u |= a.upart[(size_t)q * Kw + w];
+        sU[w] = u;
+      }
+    } else {
+      // column OR of all R rows: rg row groups per word, then OR the groups
+      // (R*Kw is small here; bounded by the host)
+      const int rg = max(1, NT / Kw);
+      unsigned long long* sOr = reinterpret_cast<unsigned long long*>(sOff);  // free until staging
+      if (tid < rg * Kw) {
+        const int w = tid % Kw, r0 = tid / Kw;
+        unsigned long long u = 0;
+        for (int r = r0; r < R; r += rg) u |= a.S[(size_t)r * Kw + w];
+        sOr[r0 * Kw + w] = u;
+      }
+      __syncthreads();
+      for (int w = tid; w < Kw; w += NT) {
+        unsigned long long u = 0;
+        for (int q = 0; q < rg; ++q) u |= sOr[q * Kw + w];
+        sU[w] = u;
+      }
+    }
+    __syncthreads();
+    if (tid == 0 && (a.K & 63)) sU[Kw - 1] &= (1ull << (a.K & 63)) - 1ull;
+    __syncthreads();
+    const int cnt = tid < Kw ? __popcll(sU[tid]) : 0;
+    int incl = cnt;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    if (lane == kWave - 1) sWave[wave] = incl;
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int i = 0; i < NW; ++i) {
+      if (i < wave) before += sWave[i];
+      total += sWave[i];
+    }
+    if (tid < Kw) sP[tid] = before + incl - cnt;
+    if (tid == 0) sP[Kw] = total;
+    ka = total;
+    if (a.stats && tid == 0 && x == 0 && y == 0 && z == 0) {
+      a.stats->k_total = a.K;
+      a.stats->k_active = total;
+      a.stats->n = a.N;
+      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
+    }
+    __syncthreads();
+  } else {
+    ka = *a.kact;
+  }
   const int KS = (ka + 63) >> 6;
   const int ks0 = (int)(((long long)KS * z) / a.P);
   const int ks1 = (int)(((long long)KS * (z + 1)) / a.P);
 
   int rowq[RT];
+  bool rowv[RT];
 #pragma unroll
   for (int q = 0; q < RT; ++q) {
     const int jr = q * 16 + c;
     const int t = jr / a.Mb, ml = jr - t * a.Mb, m = y * a.Mb + ml;
-    rowq[q] = (t < a.T && m < a.M) ? t * a.M + m : -1;
+    rowv[q] = t < a.T && m < a.M;
+    rowq[q] = rowv[q] ? t * a.M + m : 0;
   }
   const uint32_t colb = (n0 + 4 * c < a.N) ? (uint32_t)(n0 + 4 * c) : (uint32_t)n0;
   const char* Wb = reinterpret_cast<const char*>(a.W) + colb;
@@ -170,49 +333,109 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
 
-  for (int cs = ks0; cs < ks1; cs += kChunkSteps) {
-    const int ce = min(cs + kChunkSteps, ks1);
+  for (int cs = ks0; cs < ks1; cs += CH) {
+    const int ce = min(cs + CH, ks1);
     __syncthreads();
-    for (int i = tid; i < (ce - cs) * 64; i += 256) sOff[i] = a.act_off[(size_t)cs * 64 + i];
+    if constexpr (FUSED) {
+      // active rows [cs*64, ce*64): every union word writes its set bits
+      // that fall in the chunk at their ranks
+      const int e0 = cs * 64, e1 = min(ce * 64, ka);
+      for (int i = tid; i < CH * 64; i += NT) {
+        sIdx[i] = -1;
+        sOff[i] = 0u;
+      }
+      __syncthreads();
+      // one union word per wave, one bit per lane; rank by masked popcount
+      for (int w = wave; w < Kw; w += NW) {
+        const int p0 = sP[w];
+        if (p0 >= e1 || sP[w + 1] <= e0) continue;  // wave-uniform
+        const unsigned long long u = sU[w];
+        const int e = p0 + __popcll(u & ((1ull << lane) - 1ull));
+        if (((u >> lane) & 1ull) && e >= e0 && e < e1) {
+          const int k = w * 64 + lane;
+          sIdx[e - e0] = k;
+          sOff[e - e0] = (uint32_t)k * (uint32_t)a.ldw;
+        }
+      }
+    } else {
+      for (int i = tid; i < CH * 64; i += NT)
+        sOff[i] = (cs * 64 + i < ce * 64) ? a.act_off[(size_t)cs * 64 + i] : 0u;
+    }
     __syncthreads();
-    for (int j = cs + wave; j < ce; j += 4) {
-      const uint4* po = reinterpret_cast<const uint4*>(sOff + (j - cs) * 64 + 16 * g);
-      uint32_t off[16];
+    const int jb = cs + wave * kGroup;
+    const int nv = min(kGroup, ce - jb);
+    if (nv <= 0) continue;  // wave-uniform
+
+    uint32_t xw[kGroup][16];
+    uint32_t bits[kGroup][RT];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const uint4* po = reinterpret_cast<const uint4*>(sOff + (wave * kGroup + i) * 64 + 16 * g);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const uint4 o = po[u];
-        off[4 * u + 0] = o.x;
-        off[4 * u + 1] = o.y;
-        off[4 * u + 2] = o.z;
-        off[4 * u + 3] = o.w;
+        xw[i][4 * u + 0] = *reinterpret_cast<const uint32_t*>(Wb + o.x);
+        xw[i][4 * u + 1] = *reinterpret_cast<const uint32_t*>(Wb + o.y);
+        xw[i][4 * u + 2] = *reinterpret_cast<const uint32_t*>(Wb + o.z);
+        xw[i][4 * u + 3] = *reinterpret_cast<const uint32_t*>(Wb + o.w);
       }
-      uint32_t xw[16];
+    }
+    if constexpr (!FUSED) {
 #pragma unroll
-      for (int s = 0; s < 16; ++s) xw[s] = *reinterpret_cast<const uint32_t*>(Wb + off[s]);
-
-      uint32_t bits[RT];
+      for (int i = 0; i < kGroup; ++i) {
+        const int j = min(jb + i, ce - 1);
 #pragma unroll
-      for (int q = 0; q < RT; ++q)
-        bits[q] = rowq[q] >= 0
-                      ? (sc32[((size_t)j * R + rowq[q]) * 2 + (g >> 1)] >> ((g & 1) * 16)) & 0xFFFFu
-                      : 0u;
-
+        for (int q = 0; q < RT; ++q) {
+          const uint32_t raw = sc32[((size_t)j * R + rowq[q]) * 2 + (g >> 1)];
+          bits[i][q] = (rowv[q] && i < nv) ? (raw >> ((g & 1) * 16)) & 0xFFFFu : 0u;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      if constexpr (FUSED) {
+        // gather the spike bits of this lane's rows at its 16 active rows
+        const int lds_row = 2 * Kw + 1;
+        const int4* pi = reinterpret_cast<const int4*>(sIdx + (wave * kGroup + i) * 64 + 16 * g);
+        int kk[16];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int4 v = pi[u];
+          kk[4 * u + 0] = v.x;
+          kk[4 * u + 1] = v.y;
+          kk[4 * u + 2] = v.z;
+          kk[4 * u + 3] = v.w;
+        }
+#pragma unroll
+        for (int q = 0; q < RT; ++q) {
+          const uint32_t* row = sS + (q * 16 + c) * lds_row;
+          uint32_t b16 = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 16; ++s2) {
+            const int k = kk[s2];
+            const uint32_t wv = row[max(k, 0) >> 5];
+            b16 |= (k >= 0 ? ((wv >> (k & 31)) & 1u) : 0u) << s2;
+          }
+          bits[i][q] = b16;
+        }
+      }
       v4i b[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const uint32_t x0 = xw[4 * u], x1 = xw[4 * u + 1], x2 = xw[4 * u + 2], x3 = xw[4 * u + 3];
+        const uint32_t x0 = xw[i][4 * u], x1 = xw[i][4 * u + 1];
+        const uint32_t x2 = xw[i][4 * u + 2], x3 = xw[i][4 * u + 3];
         const uint32_t t0 = __builtin_amdgcn_perm(x1, x0, 0x05010400u);  // x0[0] x1[0] x0[1] x1[1]
         const uint32_t t1 = __builtin_amdgcn_perm(x1, x0, 0x07030602u);  // x0[2] x1[2] x0[3] x1[3]
         const uint32_t t2 = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
         const uint32_t t3 = __builtin_amdgcn_perm(x3, x2, 0x07030602u);
-        b[0][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x05040100u);     // column 4c+0 of rows 4u..4u+3
+        b[0][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x05040100u);     // column 4c+0, rows 4u..4u+3
         b[1][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x07060302u);
         b[2][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x05040100u);
         b[3][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x07060302u);
       }
 #pragma unroll
       for (int q = 0; q < RT; ++q) {
-        const uint32_t bq = bits[q];
+        const uint32_t bq = bits[i][q];
         const v4i af = v4i{(int)expand4(bq & 0xFu), (int)expand4((bq >> 4) & 0xFu),
                            (int)expand4((bq >> 8) & 0xFu), (int)expand4(bq >> 12)};
 #pragma unroll
@@ -242,7 +465,7 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
     const size_t slot_elems = (size_t)ROWS * 64;
     const size_t n_tiles = (size_t)gridDim.x * gridDim.y;
     int* mine = a.part + ((size_t)z * n_tiles + tile_id) * slot_elems;
-    for (int i = tid; i < ROWS * 64; i += 256)
+    for (int i = tid; i < ROWS * 64; i += NT)
       __hip_atomic_store(&mine[i], sTile[(i >> 6) * kTileLd + phys_col(i & 63)], __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     __threadfence();
@@ -251,10 +474,10 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
     __syncthreads();
     if (!sLast) return;
     __threadfence();
-    for (int i = tid; i < ROWS * 64; i += 256) {
+    for (int i = tid; i < ROWS * 64; i += NT) {
       int v = 0;
-      for (int p = 0; p < a.P; ++p)
-        v += __hip_atomic_load(a.part + ((size_t)p * n_tiles + tile_id) * slot_elems + i,
+      for (int q = 0; q < a.P; ++q)
+        v += __hip_atomic_load(a.part + ((size_t)q * n_tiles + tile_id) * slot_elems + i,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       sTile[(i >> 6) * kTileLd + phys_col(i & 63)] = v;
     }
@@ -267,7 +490,7 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
   const int pc = phys_col(col);
   if (a.mode == EPI_HEAD) {
     const float sc = nv ? a.scale[n] : 0.f;
-    for (int ml = wave; ml < a.Mb; ml += 4) {
+    for (int ml = wave; ml < a.Mb; ml += NW) {
       const int m = y * a.Mb + ml;
       if (m >= a.M) break;
       int s = 0;
@@ -289,8 +512,9 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
 #pragma unroll
   for (int t = 0; t < NMDLM_MAX_T; ++t) tb0[t] = tb1[t] = 0ull;
   uint64_t tm0 = 0ull, tm1 = 0ull;
+  uint64_t uor = 0ull;  // union of this wave's output words (wave-uniform)
 
-  for (int ml = wave; ml < a.Mb; ml += 4) {
+  for (int ml = wave; ml < a.Mb; ml += NW) {
     const int m = y * a.Mb + ml;
     if (m >= a.M) break;
     int V = 0;
@@ -318,6 +542,7 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
           if (s) V -= theta;
           if (!tr) {
             const uint64_t word = __builtin_amdgcn_ballot_w64(s);
+            uor |= word;
             if (lane == 0) seg.ptr[t * seg.ld_t + (int64_t)m * seg.ld_m + wseg] = word;
           } else if (s) {
             if (rel == 0) tb0[t] |= pbit;
@@ -344,6 +569,16 @@ __global__ __launch_bounds__(256) void k_qbsm(QbsmArgs a) {
           if (tb1[t]) atomicOr(row + 1, tb1[t]);
         }
       }
+    }
+  }
+  if (a.u_out && spikes && !tr) {
+    // partial union of this row block's output word, for the next product
+    if (lane == 0) sUn[wave] = uor;
+    __syncthreads();
+    if (tid == 0) {
+      unsigned long long u = 0;
+      for (int w = 0; w < NW; ++w) u |= sUn[w];
+      a.u_out[(size_t)y * a.u_ld + x] = u;
     }
   }
 }
@@ -375,6 +610,7 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->act_idx = cv.take<int32_t>(kpad);
   s->kact = cv.take<int32_t>(1);
   s->sc = cv.take<uint64_t>((size_t)((L.Kmax + 63) / 64) * (size_t)L.Rmax);
+  s->U = cv.take<uint64_t>((size_t)((L.Kmax + 63) / 64));
   // split slots: up to kSplitSlots tiles of (row tiles x 64 columns) per column
   size_t rows_cap = 0;
   if (L.split_rows > 0) rows_cap = L.split_rows <= 128 ? 16 * (size_t)pick_rt(L.split_rows) : 256;
@@ -384,30 +620,52 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->counters = cv.take<int32_t>(s->n_counters);
 }
 
-nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t st) {
+template <int RT, int NW, bool FUSED>
+static void launch_k(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
+  hipLaunchKernelGGL((k_qbsm<RT, NW, FUSED>), grid, dim3(NW * 64), dyn, st, a);
+}
+
+// Static LDS of k_qbsm<RT, NW, true> (mirrors the declarations above).
+static size_t fused_static_lds(int RT, int NW) {
+  const size_t ch = (size_t)NW * kGroup * 64;
+  return (size_t)RT * 16 * kTileLd * 4 + ch * 4 * 2 + kFusedMaxWords * 8 + (kFusedMaxWords + 1) * 4 +
+         (size_t)NW * 12 + 64;
+}
+
+nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t st, int* gy_out) {
   const int R = c.T * c.M;
   const int Kw = (c.K + 63) / 64;
   const int dense = (c.flags & NMDLM_FORCE_DENSE) ? 1 : 0;
+  const int gx = (c.N + 63) / 64;
   bool has_tr = false;
   if (c.mode == EPI_IF || c.mode == EPI_QNL_IF)
     for (int i = 0; i < c.nseg; ++i) has_tr = has_tr || c.seg[i].transposed;
 
+  // rows per tile group: the largest that still gives >= 256 workgroups,
+  // else the smallest (most row blocks; they re-read weights from L2)
+  const int rt_full = pick_rt(R);
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
-  if (RT != 1 && RT != 2 && RT != 4 && RT != 8) RT = pick_rt(R);
+  if (RT != 1 && RT != 2 && RT != 4 && RT != 8) {
+    RT = 1;
+    for (int r = rt_full; r >= 1; r >>= 1) {
+      const int mb = (16 * r) / c.T;
+      if (mb >= 1 && (long long)gx * ((c.M + mb - 1) / mb) >= 256) {
+        RT = r;
+        break;
+      }
+    }
+  }
   while (RT > 1 && 16 * RT / 2 >= R && 16 * RT / 2 >= c.T) RT >>= 1;  // no empty tiles
   while (has_tr && RT > 1 && (16 * RT) / c.T > 64) RT >>= 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
   const int Mb = (16 * RT) / c.T;
-  const int gx = (c.N + 63) / 64, gy = (c.M + Mb - 1) / Mb;
+  const int gy = (c.M + Mb - 1) / Mb;
   const int tiles = gx * gy;
   if ((size_t)tiles > scr.n_counters) return NMDLM_ERR_WORKSPACE;
+  if (gy_out) *gy_out = gy;
 
   int P = (int)((c.flags >> NMDLM_SPLIT_SHIFT) & 0xFFu);
-  if (P == 0) {
-    P = 1;
-    if (tiles < 240) P = (480 + tiles - 1) / tiles;
-    P = std::min(P, std::max(1, Kw / 4));
-  }
+  if (P == 0) P = 1;
   P = std::max(1, std::min(P, Kw));
   const size_t slot_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one tile slot per split
   if (P > 1) {
@@ -415,12 +673,48 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     P = (int)std::min<size_t>((size_t)P, cap);
     if (P < 2) P = 1;
   }
+  // waves per workgroup: many when each workgroup has many k-steps
+  const int ks_per_wg = (Kw + P - 1) / P;
+  int NW = (ks_per_wg >= 8 * kGroup && RT <= 2) ? 16 : 4;
+  // one kernel (union, list and spike gathers in LDS) when the tile's spike
+  // rows fit; else a separate prep pass builds them in global memory
+  const size_t dyn = (size_t)16 * RT * (2 * Kw + 1) * 4;
+  bool fused = !(c.flags & NMDLM_NO_FUSE) && Kw <= kFusedMaxWords && RT <= 2;
+  if (fused && RT == 2) NW = 4;  // the 16-wave variant of RT=2 would spill registers
+  if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) NW = 4;
+  if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) fused = false;
+  if (fused && !c.u_in && !dense && (long long)R * Kw > kUnionDirect) fused = false;
 
-  hipLaunchKernelGGL(k_union_scan, dim3(1), dim3(kPrepThreads), 0, st, c.s_in, R, Kw, c.K, dense,
-                     (uint32_t)c.ldw, c.N, scr.act_off, scr.act_idx, scr.kact, c.stats,
-                     scr.counters, tiles);
-  hipLaunchKernelGGL(k_compact, dim3(Kw, (R + kCompactRows - 1) / kCompactRows), dim3(256), 0, st,
-                     c.s_in, R, Kw, scr.act_idx, scr.kact, scr.sc);
+  nmdlm_status rc0 = NMDLM_OK;
+  PrepArgs pa;
+  pa.S = c.s_in;
+  pa.R = R;
+  pa.Kw = Kw;
+  pa.K = c.K;
+  pa.upart = c.u_in;
+  pa.nparts = c.u_nparts;
+  pa.dense = dense;
+  pa.ldw = (uint32_t)c.ldw;
+  pa.N = c.N;
+  pa.act_off = scr.act_off;
+  pa.act_idx = scr.act_idx;
+  pa.kact = scr.kact;
+  pa.stats = c.stats;
+  pa.counters = scr.counters;
+  pa.n_counters = tiles;
+  pa.sc = scr.sc;
+  if (!fused) {
+    if (!dense && !pa.upart && (long long)R * Kw > kUnionDirect) {
+      hipLaunchKernelGGL(k_union, dim3(Kw), dim3(256), 0, st, c.s_in, R, Kw, scr.U);
+      pa.upart = scr.U;
+      pa.nparts = 1;
+    }
+    hipLaunchKernelGGL(k_prep, dim3(Kw, (R + kPrepRows - 1) / kPrepRows), dim3(256), 0, st, pa);
+  } else if (tiles > 0) {
+    // the fused kernel zeroes no counters: clear them for a split product
+    if (P > 1 && (rc0 = launch_fill_zero(scr.counters, align_up((size_t)tiles * 4, 16), st)) != NMDLM_OK)
+      return rc0;
+  }
 
   QbsmArgs a;
   a.sc = scr.sc;
@@ -450,15 +744,37 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.scale = c.scale;
   a.part = scr.part;
   a.counters = scr.counters;
+  a.u_out = c.u_out;
+  a.u_ld = gx;
+  a.S = c.s_in;
+  a.upart = pa.upart;
+  a.nparts = pa.nparts;
+  a.dense = dense;
+  a.stats = c.stats;
 
   const dim3 grid(gx, gy, P);
-  switch (RT) {
-    case 1: hipLaunchKernelGGL(k_qbsm<1>, grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(k_qbsm<2>, grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(k_qbsm<4>, grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL(k_qbsm<8>, grid, dim3(256), 0, st, a); break;
+  if (c.ev_begin && hipEventRecord(c.ev_begin, st) != hipSuccess) return NMDLM_ERR_HIP;
+  if (fused) {
+    if (NW == 16) {
+      launch_k<1, 16, true>(grid, a, dyn, st);
+    } else {
+      if (RT == 1) launch_k<1, 4, true>(grid, a, dyn, st);
+      else launch_k<2, 4, true>(grid, a, dyn, st);
+    }
+  } else if (NW == 16) {
+    if (RT == 1) launch_k<1, 16, false>(grid, a, 0, st);
+    else launch_k<2, 16, false>(grid, a, 0, st);
+  } else {
+    switch (RT) {
+      case 1: launch_k<1, 4, false>(grid, a, 0, st); break;
+      case 2: launch_k<2, 4, false>(grid, a, 0, st); break;
+      case 4: launch_k<4, 4, false>(grid, a, 0, st); break;
+      default: launch_k<8, 4, false>(grid, a, 0, st); break;
+    }
   }
-  return hip_status();
+  const nmdlm_status rc = hip_status();
+  if (rc == NMDLM_OK && c.ev_end && hipEventRecord(c.ev_end, st) != hipSuccess) return NMDLM_ERR_HIP;
+  return rc;
 }
 
 }  // namespace nmdlm

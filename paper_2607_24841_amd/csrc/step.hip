@@ -108,6 +108,10 @@ struct StepBuffers {
   uint64_t* Hs;     // [T][M][Fw]
   uint64_t* Y[2];
   int32_t* a;       // attention output [T][M][d]
+  uint64_t* uA;     // partial unions of A  [M][dw]
+  uint64_t* uX1;    // partial unions of X1 [M][dw] (at most one per token)
+  uint64_t* uH;     // partial unions of H  [M][Fw]
+  uint64_t* uY[2];  // partial unions of Y  [M][dw]
   float* logits;    // [M][V]
   int32_t* pred;
   double* conf;
@@ -141,6 +145,11 @@ static void carve_step(Carver& cv, const nmdlm_model* md, int M, unsigned flags,
   b->Y[0] = cv.take<uint64_t>(sp);
   b->Y[1] = cv.take<uint64_t>(sp);
   b->a = cv.take<int32_t>((size_t)T * M * md->d);
+  b->uA = cv.take<uint64_t>((size_t)M * dw);
+  b->uX1 = cv.take<uint64_t>((size_t)M * dw);
+  b->uH = cv.take<uint64_t>((size_t)M * Fw);
+  b->uY[0] = cv.take<uint64_t>((size_t)M * dw);
+  b->uY[1] = cv.take<uint64_t>((size_t)M * dw);
   const bool head = !(flags & NMDLM_NO_HEAD);
   b->logits = (head && need_logits) ? cv.take<float>((size_t)M * md->V) : nullptr;
   b->pred = (head && need_pred) ? cv.take<int32_t>(M) : nullptr;
@@ -192,8 +201,22 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.logits = nullptr;
   c.scale = nullptr;
   c.stats = stats;
-  c.flags = flags & (NMDLM_FORCE_DENSE | (0xFFu << NMDLM_SPLIT_SHIFT) | (0xFu << NMDLM_ROWTILE_SHIFT));
+  c.flags = flags & (NMDLM_FORCE_DENSE | (0xFFu << NMDLM_SPLIT_SHIFT) | (0xFu << NMDLM_ROWTILE_SHIFT) |
+                     NMDLM_NO_FUSE);
+  c.ev_begin = nullptr;
+  c.ev_end = nullptr;
+  c.u_in = nullptr;
+  c.u_nparts = 0;
+  c.u_out = nullptr;
   return c;
+}
+
+// Attach the caller's timing events of product i (if any).
+static void attach_events(QbsmCall& c, const nmdlm_step_io* io, int i) {
+  if (io->prof_events && 2 * i + 1 < io->n_prof_events) {
+    c.ev_begin = static_cast<hipEvent_t>(io->prof_events[2 * i]);
+    c.ev_end = static_cast<hipEvent_t>(io->prof_events[2 * i + 1]);
+  }
 }
 
 nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws, size_t ws_bytes,
@@ -219,9 +242,13 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     X = b.X;
   }
   const int64_t sp_t = (int64_t)M * dw;
+  // partial unions of the current layer input (null: the prep kernel ORs X)
+  const uint64_t* uX = nullptr;
+  int uX_parts = 0;
   for (int l = 0; l < md->n_layers; ++l) {
     const nmdlm_layer& ly = md->layers[l];
     nmdlm_qbsm_stats* stl = io->stats ? io->stats + 4 * l : nullptr;
+    int gy = 0;
 
     // Q | K | V, keys and values straight into cache rows [C, C+M)
     QbsmCall qkv = base_call(X, T, M, d, ly.w_qkv, 3 * (int64_t)d, 3 * d, EPI_IF, io->flags,
@@ -233,12 +260,16 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     qkv.seg[2] = natural_seg(ly.vt_cache, (int64_t)d * capw, capw, ly.theta_v);
     qkv.seg[2].transposed = 1;
     qkv.seg[2].pos0 = C;
+    qkv.u_in = uX;
+    qkv.u_nparts = uX_parts;
+    attach_events(qkv, io, 4 * l + 0);
     if ((rc = launch_qbsm(qkv, b.qs, st)) != NMDLM_OK) return rc;
 
     if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att, b.a,
                           st)) != NMDLM_OK)
       return rc;
-    if ((rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st)) != NMDLM_OK)
+    if ((rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st, b.uA)) !=
+        NMDLM_OK)
       return rc;
 
     QbsmCall o = base_call(b.A, T, M, d, ly.w_o, d, d, EPI_IF, io->flags, stl ? stl + 1 : nullptr);
@@ -246,14 +277,24 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     o.resid = X;
     o.rld_t = sp_t;
     o.rld_m = dw;
-    if ((rc = launch_qbsm(o, b.qs, st)) != NMDLM_OK) return rc;
+    o.u_in = b.uA;
+    o.u_nparts = M;
+    o.u_out = b.uX1;
+    attach_events(o, io, 4 * l + 1);
+    if ((rc = launch_qbsm(o, b.qs, st, &gy)) != NMDLM_OK) return rc;
+    const int uX1_parts = gy;
 
     QbsmCall up = base_call(b.X1, T, M, d, ly.w_up, F, F, EPI_QNL_IF, io->flags,
                             stl ? stl + 2 : nullptr);
     up.seg[0] = natural_seg(b.Hs, (int64_t)M * Fw, Fw, ly.theta_up);
     up.lut = ly.lut_act;
     up.lut_shift = ly.s_up;
-    if ((rc = launch_qbsm(up, b.qs, st)) != NMDLM_OK) return rc;
+    up.u_in = b.uX1;
+    up.u_nparts = uX1_parts;
+    up.u_out = b.uH;
+    attach_events(up, io, 4 * l + 2);
+    if ((rc = launch_qbsm(up, b.qs, st, &gy)) != NMDLM_OK) return rc;
+    const int uH_parts = gy;
 
     uint64_t* Yl = (l == md->n_layers - 1 && io->y_out) ? io->y_out : b.Y[l & 1];
     QbsmCall dn = base_call(b.Hs, T, M, F, ly.w_dn, d, d, EPI_IF, io->flags,
@@ -262,8 +303,14 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     dn.resid = b.X1;
     dn.rld_t = sp_t;
     dn.rld_m = dw;
-    if ((rc = launch_qbsm(dn, b.qs, st)) != NMDLM_OK) return rc;
+    dn.u_in = b.uH;
+    dn.u_nparts = uH_parts;
+    dn.u_out = b.uY[l & 1];
+    attach_events(dn, io, 4 * l + 3);
+    if ((rc = launch_qbsm(dn, b.qs, st, &gy)) != NMDLM_OK) return rc;
     X = Yl;
+    uX = b.uY[l & 1];
+    uX_parts = gy;
   }
 
   if (!head) {
@@ -280,6 +327,9 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
                           io->stats ? io->stats + 4 * md->n_layers : nullptr);
   hc.logits = logits;
   hc.scale = md->head_scale;
+  hc.u_in = uX;
+  hc.u_nparts = uX_parts;
+  attach_events(hc, io, 4 * md->n_layers);
   if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
   hipLaunchKernelGGL(k_conf, dim3(M), dim3(256), 0, st, logits, md->V, pred, conf);
   if ((rc = hip_status()) != NMDLM_OK) return rc;

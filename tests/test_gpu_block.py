@@ -75,7 +75,42 @@ def test_config2_full_size():
     _check_block(synth.config2())
 
 
-@pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16)], ids=["P1", "P3", "P2RT1"])
+def test_block_step_graph_replays_match_eager():
+    torch, B = need_gpu()
+    case = synth.config2()
+    L = case.layer
+    T, C, M, d = case.T, case.C, case.M, L.d
+    dm = B.DeviceModel([L], T, C + M, d, L.H, L.F)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, B.NMDLM_NO_HEAD)))
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD,
+                                     x_in=B.to_dev_bits(synth.pack_bits(case.X_ctx))), ws)
+    xb = B.to_dev_bits(synth.pack_bits(case.X_blk))
+    y = torch.zeros((T, M, d // 64), dtype=torch.int64, device="cuda")
+    io = B.step_io(M, C, flags=B.NMDLM_NO_HEAD, x_in=xb, y_out=y)
+    B.nmdlm_block_step(dm, io, ws)
+    torch.cuda.synchronize()
+    eager = y.clone()
+    tr, _, _ = _oracle_block_case(case)
+    assert_same(synth.unpack_bits(B.from_dev_bits(eager), d), tr.Y, "eager Y")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        B.nmdlm_block_step(dm, io, ws)
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        B.nmdlm_block_step(dm, io, ws)
+    for r in range(4):
+        y.fill_(-1)                                  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager), f"replay {r} differs from the eager step"
+
+
+@pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16), 0x100000],
+                         ids=["P1", "P3", "P2RT1", "nofuse"])
 def test_config2_forced_paths(flags):
     need_gpu()
     _check_block(synth.config2(), flags=flags)

@@ -53,22 +53,35 @@ def test_tiny_and_ragged_shapes(shape):
     _check(synth.make_qbsm_case(100 + K + N, T, M, K, N, p))
 
 
+NOFUSE = 0x100000
+
+
 @pytest.mark.parametrize("flags", [0x1, 1 << 8, 2 << 8, 7 << 8, 1 << 16, 2 << 16, 4 << 16, 8 << 16,
-                                   (3 << 8) | (1 << 16)],
-                         ids=["dense", "P1", "P2", "P7", "RT1", "RT2", "RT4", "RT8", "P3RT1"])
+                                   (3 << 8) | (1 << 16), NOFUSE, NOFUSE | 0x1, NOFUSE | (2 << 8),
+                                   NOFUSE | (1 << 16), NOFUSE | (8 << 16)],
+                         ids=["dense", "P1", "P2", "P7", "RT1", "RT2", "RT4", "RT8", "P3RT1", "nofuse",
+                              "nofuse-dense", "nofuse-P2", "nofuse-RT1", "nofuse-RT8"])
 def test_forced_paths_equal(flags):
     need_gpu()
     case = synth.make_qbsm_case(5, 4, 24, 700, 300, 0.05)
     _check(case, flags=flags)
 
 
-def test_degenerate_inputs():
+@pytest.mark.parametrize("flags", [0, NOFUSE], ids=["fused", "nofuse"])
+def test_degenerate_inputs(flags):
     need_gpu()
     c = synth.make_qbsm_case(9, 4, 8, 256, 128, 0.1)
     c.S[:] = False                   # no spike: K_active = 0, currents = bias
-    _check(c)
+    _check(c, flags=flags)
     c.S[:] = True                    # every row active
-    _check(c)
+    _check(c, flags=flags)
+
+
+def test_large_k_shapes():
+    need_gpu()
+    # K beyond the single-kernel limit, and a long block (many row blocks)
+    _check(synth.make_qbsm_case(41, 4, 4, 20000, 130, 0.02))
+    _check(synth.make_qbsm_case(42, 4, 300, 700, 200, 0.05))
 
 
 def test_per_neuron_thresholds_and_currents_only():
