@@ -2,13 +2,12 @@
 //
 // Sec. IV-A: Y = X W over the B*T spike rows of a block; by assumption (ii) a
 // weight row is read only if its input neuron spikes somewhere in the block.
-// Two kernels per product:
-//   k_prep   block union (from producer partial unions or the spikes),
-//            active-row list and compaction of the spike bits onto it
-//   k_qbsm   int8 MFMA over (T*M) x K_active x N with a fused epilogue
-//            (currents, integrate-and-fire, table + IF, or head logits) that
-//            also emits the partial union of its output spikes
-// (k_union ORs very large spike blocks first, e.g. a long prefill.)
+// One kernel per product (k_qbsm_fused): block union from the producer's
+// partial unions (or the spikes), active-row list and spike compaction in
+// LDS, then int8 MFMA over (T*M) x K_active x N with a fused epilogue
+// (currents, integrate-and-fire, table + IF, or head logits) that also emits
+// the partial union of its output spikes.  Blocks too large for LDS (long
+// prefills) take a prep pass (k_union, k_prep) and k_qbsm_list.
 #include "common.h"
 
 namespace nmdlm {
@@ -194,20 +193,25 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs p) {
 // ---------------------------------------------------------------------------
 // The product.
 //
-// Workgroup = NW waves, tile = (16*RT rows of the block) x (64 columns).  The
-// waves take groups of kGroup k-steps (64 active rows each) and reduce in
-// LDS; a group's weight and spike loads are all issued before any is used.
-// Per k-step a lane (g = lane/16, c = lane%16) loads, for the 16 active rows
-// k_{g,0..15}, the dword W[k][n0+4c .. n0+4c+3]; an in-register 4x4 byte
-// transpose turns these into four MFMA B operands whose column c stands for
-// weight column n0 + 4c + v (v = 0..3).  The A operand (16 spike rows x 64
-// active rows) is expanded from the compacted bits.  v_mfma_i32_16x16x64_i8
-// accumulates exactly in int32; output element (lane, e) is row 4g + e.
-// Block rows are ordered t-major: local row r -> (t = r / Mb, token r % Mb).
+// Workgroup = NW waves, tile = (16*RT rows of the block) x (64 columns).
+// Block rows are ordered t-major inside a row block: local row r ->
+// (t = r / Mb, token r % Mb), so a token's T currents land in one tile.
+// The waves take groups of kGroup k-steps (64 active rows each) and reduce in
+// LDS.  Per k-step a lane (g = lane/16, c = lane%16) loads, for the 16 active
+// rows k_{g,0..15}, the dword W[k][n0+4c .. n0+4c+3]; an in-register 4x4 byte
+// transpose turns them into four MFMA B operands whose column c stands for
+// weight column n0 + 4c + v (v = 0..3).  The A operand (16 rows x 64 active
+// rows of 0/1 bytes) is expanded from 16 compacted spike bits per lane.
+// v_mfma_i32_16x16x64_i8 accumulates exactly in int32; output element
+// (lane, e) is tile row 4g + e.
+//
+// k_qbsm_fused builds the union, the active-row list and the compacted
+// spike bits in LDS itself; k_qbsm_list reads them from the prep pass.
 // ---------------------------------------------------------------------------
 constexpr int kGroup = 4;
 constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
 constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
+constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
   // 4 bits -> 4 bytes of 0/1 (bit i -> byte i); the shifted copies of the
@@ -215,237 +219,55 @@ __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
   return (nib * 0x00204081u) & 0x01010101u;
 }
 
+__device__ __forceinline__ v4i a_operand(uint32_t b16) {
+  return v4i{(int)expand4(b16 & 0xFu), (int)expand4((b16 >> 4) & 0xFu),
+             (int)expand4((b16 >> 8) & 0xFu), (int)expand4(b16 >> 12)};
+}
+
+// Four B operands (columns 4c+v) from 16 row dwords (rows 0..15, 4 columns each).
+__device__ __forceinline__ void b_operands(const uint32_t* xw, v4i (&b)[4]) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t x0 = xw[4 * u], x1 = xw[4 * u + 1], x2 = xw[4 * u + 2], x3 = xw[4 * u + 3];
+    const uint32_t t0 = __builtin_amdgcn_perm(x1, x0, 0x05010400u);  // x0[0] x1[0] x0[1] x1[1]
+    const uint32_t t1 = __builtin_amdgcn_perm(x1, x0, 0x07030602u);  // x0[2] x1[2] x0[3] x1[3]
+    const uint32_t t2 = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
+    const uint32_t t3 = __builtin_amdgcn_perm(x3, x2, 0x07030602u);
+    b[0][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x05040100u);  // column 4c+0, rows 4u..4u+3
+    b[1][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x07060302u);
+    b[2][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x05040100u);
+    b[3][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x07060302u);
+  }
+}
+
 __device__ __forceinline__ int phys_col(int col) { return (col & 3) * 16 + (col >> 2); }
 
-template <int RT, int NW, bool FUSED>
-__global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
-  constexpr int ROWS = RT * 16;
-  constexpr int NT = NW * 64;
-  constexpr int CH = NW * kGroup;  // k-steps staged per chunk
-  __shared__ int sTile[ROWS * kTileLd];
-  __shared__ __attribute__((aligned(16))) uint32_t sOff[CH * 64];
-  __shared__ __attribute__((aligned(16))) int sIdx[FUSED ? CH * 64 : 4];
-  __shared__ unsigned long long sU[FUSED ? kFusedMaxWords : 1];
-  __shared__ int sP[FUSED ? kFusedMaxWords + 1 : 1];
-  __shared__ int sWave[NW];
-  __shared__ unsigned long long sUn[NW];
-  __shared__ int sLast;
-  // FUSED: this tile's spike rows as dwords, row stride 2*Kw+1 (odd, so the
-  // 16 rows a wave gathers from fall in different banks)
-  extern __shared__ uint32_t sS[];
+// Epilogue operands staged in LDS at kernel entry, so that the epilogue
+// issues no dependent global load.
+struct EpiStage {
+  int bias[64];
+  int theta[64];
+  unsigned long long resid[kMaxEpiTokens];  // [t * Mb + token]
+};
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 4, c = lane & 15;
-  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
-  const int n0 = x * 64;
-  const int R = a.T * a.M;
-  const int Kw = (a.K + 63) >> 6;
-
-  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
-
-  int ka;
-  if constexpr (FUSED) {
-    // this tile's spike rows, and the block union (from producer partial
-    // unions, or by OR-ing every spike row), then prefix popcounts
-    const int lds_row = 2 * Kw + 1;
-    for (int i = tid; i < ROWS * Kw; i += NT) {
-      const int lr = i / Kw, w = i - lr * Kw;
-      const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
-      const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
-      sS[lr * lds_row + 2 * w] = (uint32_t)v;
-      sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
-    }
-    if (a.dense) {
-      for (int w = tid; w < Kw; w += NT) sU[w] = ~0ull;
-    } else if (a.upart) {
-      for (int w = tid; w < Kw; w += NT) {
-        unsigned long long u = 0;
-        for (int q = 0; q < a.nparts; ++q) u |= a.upart[(size_t)q * Kw + w];
-        sU[w] = u;
-      }
-    } else {
-      // column OR of all R rows: rg row groups per word, then OR the groups
-      // (R*Kw is small here; bounded by the host)
-      const int rg = max(1, NT / Kw);
-      unsigned long long* sOr = reinterpret_cast<unsigned long long*>(sOff);  // free until staging
-      if (tid < rg * Kw) {
-        const int w = tid % Kw, r0 = tid / Kw;
-        unsigned long long u = 0;
-        for (int r = r0; r < R; r += rg) u |= a.S[(size_t)r * Kw + w];
-        sOr[r0 * Kw + w] = u;
-      }
-      __syncthreads();
-      for (int w = tid; w < Kw; w += NT) {
-        unsigned long long u = 0;
-        for (int q = 0; q < rg; ++q) u |= sOr[q * Kw + w];
-        sU[w] = u;
-      }
-    }
-    __syncthreads();
-    if (tid == 0 && (a.K & 63)) sU[Kw - 1] &= (1ull << (a.K & 63)) - 1ull;
-    __syncthreads();
-    const int cnt = tid < Kw ? __popcll(sU[tid]) : 0;
-    int incl = cnt;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
-    }
-    if (lane == kWave - 1) sWave[wave] = incl;
-    __syncthreads();
-    int before = 0, total = 0;
-    for (int i = 0; i < NW; ++i) {
-      if (i < wave) before += sWave[i];
-      total += sWave[i];
-    }
-    if (tid < Kw) sP[tid] = before + incl - cnt;
-    if (tid == 0) sP[Kw] = total;
-    ka = total;
-    if (a.stats && tid == 0 && x == 0 && y == 0 && z == 0) {
-      a.stats->k_total = a.K;
-      a.stats->k_active = total;
-      a.stats->n = a.N;
-      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
-    }
-    __syncthreads();
-  } else {
-    ka = *a.kact;
+template <int NT>
+__device__ __forceinline__ void stage_epilogue(const QbsmArgs& a, EpiStage& ep, int tid, int x, int y) {
+  const int n = x * 64 + tid;
+  if (tid < 64) {
+    ep.bias[tid] = (a.bias && n < a.N) ? a.bias[n] : 0;
+    ep.theta[tid] = a.theta_vec ? (n < a.N ? a.theta_vec[n] : 1) : 0;
   }
-  const int KS = (ka + 63) >> 6;
-  const int ks0 = (int)(((long long)KS * z) / a.P);
-  const int ks1 = (int)(((long long)KS * (z + 1)) / a.P);
-
-  int rowq[RT];
-  bool rowv[RT];
-#pragma unroll
-  for (int q = 0; q < RT; ++q) {
-    const int jr = q * 16 + c;
-    const int t = jr / a.Mb, ml = jr - t * a.Mb, m = y * a.Mb + ml;
-    rowv[q] = t < a.T && m < a.M;
-    rowq[q] = rowv[q] ? t * a.M + m : 0;
-  }
-  const uint32_t colb = (n0 + 4 * c < a.N) ? (uint32_t)(n0 + 4 * c) : (uint32_t)n0;
-  const char* Wb = reinterpret_cast<const char*>(a.W) + colb;
-  const uint32_t* sc32 = reinterpret_cast<const uint32_t*>(a.sc);
-
-  v4i acc[RT][4];
-#pragma unroll
-  for (int q = 0; q < RT; ++q)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
-
-  for (int cs = ks0; cs < ks1; cs += CH) {
-    const int ce = min(cs + CH, ks1);
-    __syncthreads();
-    if constexpr (FUSED) {
-      // active rows [cs*64, ce*64): every union word writes its set bits
-      // that fall in the chunk at their ranks
-      const int e0 = cs * 64, e1 = min(ce * 64, ka);
-      for (int i = tid; i < CH * 64; i += NT) {
-        sIdx[i] = -1;
-        sOff[i] = 0u;
-      }
-      __syncthreads();
-      // one union word per wave, one bit per lane; rank by masked popcount
-      for (int w = wave; w < Kw; w += NW) {
-        const int p0 = sP[w];
-        if (p0 >= e1 || sP[w + 1] <= e0) continue;  // wave-uniform
-        const unsigned long long u = sU[w];
-        const int e = p0 + __popcll(u & ((1ull << lane) - 1ull));
-        if (((u >> lane) & 1ull) && e >= e0 && e < e1) {
-          const int k = w * 64 + lane;
-          sIdx[e - e0] = k;
-          sOff[e - e0] = (uint32_t)k * (uint32_t)a.ldw;
-        }
-      }
-    } else {
-      for (int i = tid; i < CH * 64; i += NT)
-        sOff[i] = (cs * 64 + i < ce * 64) ? a.act_off[(size_t)cs * 64 + i] : 0u;
-    }
-    __syncthreads();
-    const int jb = cs + wave * kGroup;
-    const int nv = min(kGroup, ce - jb);
-    if (nv <= 0) continue;  // wave-uniform
-
-    uint32_t xw[kGroup][16];
-    uint32_t bits[kGroup][RT];
-#pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      const uint4* po = reinterpret_cast<const uint4*>(sOff + (wave * kGroup + i) * 64 + 16 * g);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint4 o = po[u];
-        xw[i][4 * u + 0] = *reinterpret_cast<const uint32_t*>(Wb + o.x);
-        xw[i][4 * u + 1] = *reinterpret_cast<const uint32_t*>(Wb + o.y);
-        xw[i][4 * u + 2] = *reinterpret_cast<const uint32_t*>(Wb + o.z);
-        xw[i][4 * u + 3] = *reinterpret_cast<const uint32_t*>(Wb + o.w);
-      }
-    }
-    if constexpr (!FUSED) {
-#pragma unroll
-      for (int i = 0; i < kGroup; ++i) {
-        const int j = min(jb + i, ce - 1);
-#pragma unroll
-        for (int q = 0; q < RT; ++q) {
-          const uint32_t raw = sc32[((size_t)j * R + rowq[q]) * 2 + (g >> 1)];
-          bits[i][q] = (rowv[q] && i < nv) ? (raw >> ((g & 1) * 16)) & 0xFFFFu : 0u;
-        }
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      if constexpr (FUSED) {
-        // gather the spike bits of this lane's rows at its 16 active rows
-        const int lds_row = 2 * Kw + 1;
-        const int4* pi = reinterpret_cast<const int4*>(sIdx + (wave * kGroup + i) * 64 + 16 * g);
-        int kk[16];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int4 v = pi[u];
-          kk[4 * u + 0] = v.x;
-          kk[4 * u + 1] = v.y;
-          kk[4 * u + 2] = v.z;
-          kk[4 * u + 3] = v.w;
-        }
-#pragma unroll
-        for (int q = 0; q < RT; ++q) {
-          const uint32_t* row = sS + (q * 16 + c) * lds_row;
-          uint32_t b16 = 0;
-#pragma unroll
-          for (int s2 = 0; s2 < 16; ++s2) {
-            const int k = kk[s2];
-            const uint32_t wv = row[max(k, 0) >> 5];
-            b16 |= (k >= 0 ? ((wv >> (k & 31)) & 1u) : 0u) << s2;
-          }
-          bits[i][q] = b16;
-        }
-      }
-      v4i b[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t x0 = xw[i][4 * u], x1 = xw[i][4 * u + 1];
-        const uint32_t x2 = xw[i][4 * u + 2], x3 = xw[i][4 * u + 3];
-        const uint32_t t0 = __builtin_amdgcn_perm(x1, x0, 0x05010400u);  // x0[0] x1[0] x0[1] x1[1]
-        const uint32_t t1 = __builtin_amdgcn_perm(x1, x0, 0x07030602u);  // x0[2] x1[2] x0[3] x1[3]
-        const uint32_t t2 = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
-        const uint32_t t3 = __builtin_amdgcn_perm(x3, x2, 0x07030602u);
-        b[0][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x05040100u);     // column 4c+0, rows 4u..4u+3
-        b[1][u] = (int)__builtin_amdgcn_perm(t2, t0, 0x07060302u);
-        b[2][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x05040100u);
-        b[3][u] = (int)__builtin_amdgcn_perm(t3, t1, 0x07060302u);
-      }
-#pragma unroll
-      for (int q = 0; q < RT; ++q) {
-        const uint32_t bq = bits[i][q];
-        const v4i af = v4i{(int)expand4(bq & 0xFu), (int)expand4((bq >> 4) & 0xFu),
-                           (int)expand4((bq >> 8) & 0xFu), (int)expand4(bq >> 12)};
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
-      }
+  if (a.resid) {
+    for (int i = tid; i < a.T * a.Mb && i < kMaxEpiTokens; i += NT) {
+      const int t = i / a.Mb, m = y * a.Mb + (i - t * a.Mb);
+      ep.resid[i] = m < a.M ? a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x] : 0ull;
     }
   }
+}
 
-  __syncthreads();
+// Sum the waves' accumulators into the LDS tile (physical column order).
+template <int RT>
+__device__ __forceinline__ void reduce_tile(const v4i (&acc)[RT][4], int* sTile, int g, int c) {
 #pragma unroll
   for (int q = 0; q < RT; ++q)
 #pragma unroll
@@ -455,36 +277,44 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
         const int val = acc[q][v][e];
         if (val) atomicAdd(&sTile[(q * 16 + g * 4 + e) * kTileLd + v * 16 + c], val);
       }
+}
+
+// K split across workgroups: every split stores its whole tile (zeros
+// included) into its own slot; the last workgroup to arrive sums the slots in
+// split order.  No slot has to be zero beforehand.  Returns false for the
+// workgroups that are not last.
+template <int ROWS, int NT>
+__device__ bool split_fixup(const QbsmArgs& a, int* sTile, int* sLast, int tid, int x, int y, int z) {
+  const size_t tile_id = (size_t)y * gridDim.x + x;
+  const size_t slot_elems = (size_t)ROWS * 64;
+  const size_t n_tiles = (size_t)gridDim.x * gridDim.y;
+  int* mine = a.part + ((size_t)z * n_tiles + tile_id) * slot_elems;
+  for (int i = tid; i < ROWS * 64; i += NT)
+    __hip_atomic_store(&mine[i], sTile[(i >> 6) * kTileLd + phys_col(i & 63)], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  __threadfence();
   __syncthreads();
-
-  if (a.P > 1) {
-    // K split across workgroups: every split stores its whole tile (zeros
-    // included) into its own slot; the last workgroup to arrive sums the
-    // slots in split order.  No slot has to be zero beforehand.
-    const size_t tile_id = (size_t)y * gridDim.x + x;
-    const size_t slot_elems = (size_t)ROWS * 64;
-    const size_t n_tiles = (size_t)gridDim.x * gridDim.y;
-    int* mine = a.part + ((size_t)z * n_tiles + tile_id) * slot_elems;
-    for (int i = tid; i < ROWS * 64; i += NT)
-      __hip_atomic_store(&mine[i], sTile[(i >> 6) * kTileLd + phys_col(i & 63)], __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) sLast = (atomicAdd(&a.counters[tile_id], 1) == a.P - 1) ? 1 : 0;
-    __syncthreads();
-    if (!sLast) return;
-    __threadfence();
-    for (int i = tid; i < ROWS * 64; i += NT) {
-      int v = 0;
-      for (int q = 0; q < a.P; ++q)
-        v += __hip_atomic_load(a.part + ((size_t)q * n_tiles + tile_id) * slot_elems + i,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      sTile[(i >> 6) * kTileLd + phys_col(i & 63)] = v;
-    }
-    __syncthreads();
+  if (tid == 0) *sLast = (atomicAdd(&a.counters[tile_id], 1) == a.P - 1) ? 1 : 0;
+  __syncthreads();
+  if (!*sLast) return false;
+  __threadfence();
+  for (int i = tid; i < ROWS * 64; i += NT) {
+    int v = 0;
+    for (int q = 0; q < a.P; ++q)
+      v += __hip_atomic_load(a.part + ((size_t)q * n_tiles + tile_id) * slot_elems + i,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sTile[(i >> 6) * kTileLd + phys_col(i & 63)] = v;
   }
+  __syncthreads();
+  return true;
+}
 
-  // ------------------------------------------------------------------ epilogue
+// Epilogue: currents, IF (optionally after the activation table), or head
+// logits, from the reduced tile; emits the partial union of the output.
+template <int NW>
+__device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep,
+                         unsigned long long* sUn, int tid, int lane, int wave, int x, int y) {
+  const int n0 = x * 64;
   const int col = lane, n = n0 + col;
   const bool nv = n < a.N;
   const int pc = phys_col(col);
@@ -499,14 +329,14 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
     }
     return;
   }
-
   const int segi = (a.mode == EPI_CUR) ? 0 : n0 / a.seg_w;
   const SpikeSeg seg = a.seg[segi];
   const int wseg = (n0 - segi * a.seg_w) >> 6;
-  const int bias_n = (a.bias && nv) ? a.bias[n] : 0;
-  const int theta = a.theta_vec ? (nv ? a.theta_vec[n] : 1) : seg.theta;
+  const int bias_n = ep.bias[col];
+  const int theta = a.theta_vec ? ep.theta[col] : seg.theta;
   const bool spikes = a.mode != EPI_CUR;
   const bool tr = spikes && seg.transposed;
+  const bool staged = a.resid && a.T * a.Mb <= kMaxEpiTokens;
   const int wbase = tr ? ((seg.pos0 + y * a.Mb) >> 6) : 0;
   uint64_t tb0[NMDLM_MAX_T], tb1[NMDLM_MAX_T];
 #pragma unroll
@@ -536,7 +366,11 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
             qv = min(127, max(-128, qv));
             I = (int)(int8_t)a.lut[qv & 0xFF];
           }
-          if (a.resid && ((a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x] >> col) & 1ull)) I += theta;
+          if (a.resid) {
+            const unsigned long long rw =
+                staged ? ep.resid[t * a.Mb + ml] : a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x];
+            if ((rw >> col) & 1ull) I += theta;
+          }
           V += I;
           const bool s = nv && V >= theta;
           if (s) V -= theta;
@@ -583,6 +417,281 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm(QbsmArgs a) {
   }
 }
 
+// -------------------------------------------------------------- single kernel
+template <int RT, int NW>
+__global__ __launch_bounds__(NW * 64) void k_qbsm_fused(QbsmArgs a) {
+  constexpr int ROWS = RT * 16;
+  constexpr int NT = NW * 64;
+  constexpr int CH = NW * kGroup;  // k-steps per chunk
+  __shared__ int sTile[ROWS * kTileLd];
+  __shared__ __attribute__((aligned(16))) uint32_t sOff[CH * 64];
+  __shared__ __attribute__((aligned(16))) int sIdx[CH * 64];
+  __shared__ unsigned long long sU[kFusedMaxWords];
+  __shared__ int sP[kFusedMaxWords + 1];
+  __shared__ int sWave[NW];
+  __shared__ unsigned long long sUn[NW];
+  __shared__ unsigned long long sBits[NW * kGroup * ROWS];  // compacted bits per wave/step/row
+  __shared__ EpiStage ep;
+  __shared__ int sLast;
+  // this tile's spike rows as dwords, row stride 2*Kw+1 (odd: the rows a
+  // wave reads at one active row fall in different banks)
+  extern __shared__ uint32_t sS[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  const int R = a.T * a.M;
+  const int Kw = (a.K + 63) >> 6;
+  const int lds_row = 2 * Kw + 1;
+
+  // ---- prologue: every global load here is independent of the others
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  stage_epilogue<NT>(a, ep, tid, x, y);
+  for (int i = tid; i < ROWS * Kw; i += NT) {
+    const int lr = i / Kw, w = i - lr * Kw;
+    const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
+    const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
+    sS[lr * lds_row + 2 * w] = (uint32_t)v;
+    sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
+  }
+  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
+  if (a.dense || a.upart) {
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long u = ~0ull;
+      if (!a.dense) {
+        u = 0ull;
+        for (int q = 0; q < a.nparts; ++q) u |= a.upart[(size_t)q * Kw + w];
+      }
+      sU[w] = (w == Kw - 1) ? (u & last_mask) : u;
+    }
+  } else {
+    // column OR of all R rows (R*Kw is bounded by the host): rg row groups
+    // per word into a scratch table, then one pass over the groups
+    const int rg = max(1, NT / Kw);
+    unsigned long long* sOr = sBits;  // free until the main loop
+    if (tid < rg * Kw) {
+      const int w = tid % Kw, r0 = tid / Kw;
+      unsigned long long u = 0;
+      for (int r = r0; r < R; r += rg) u |= a.S[(size_t)r * Kw + w];
+      sOr[r0 * Kw + w] = u;
+    }
+    __syncthreads();
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long u = 0;
+      for (int q = 0; q < rg; ++q) u |= sOr[q * Kw + w];
+      sU[w] = (w == Kw - 1) ? (u & last_mask) : u;
+    }
+  }
+  __syncthreads();
+  // prefix popcounts (Kw <= NT: one word per thread)
+  const int cnt = tid < Kw ? __popcll(sU[tid]) : 0;
+  int incl = cnt;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == kWave - 1) sWave[wave] = incl;
+  __syncthreads();
+  int before = 0, ka = 0;
+  for (int i = 0; i < NW; ++i) {
+    if (i < wave) before += sWave[i];
+    ka += sWave[i];
+  }
+  if (tid < Kw) sP[tid] = before + incl - cnt;
+  if (tid == 0) sP[Kw] = ka;
+  if (a.stats && tid == 0 && x == 0 && y == 0 && z == 0) {
+    a.stats->k_total = a.K;
+    a.stats->k_active = ka;
+    a.stats->n = a.N;
+    a.stats->weight_bytes = (int64_t)ka * (int64_t)a.N;
+  }
+  __syncthreads();
+
+  const int KS = (ka + 63) >> 6;
+  const int ks0 = (int)(((long long)KS * z) / a.P);
+  const int ks1 = (int)(((long long)KS * (z + 1)) / a.P);
+  const uint32_t colb = (x * 64 + 4 * c < a.N) ? (uint32_t)(x * 64 + 4 * c) : (uint32_t)(x * 64);
+  const char* Wb = reinterpret_cast<const char*>(a.W) + colb;
+
+  v4i acc[RT][4];
+#pragma unroll
+  for (int q = 0; q < RT; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
+
+  for (int cs = ks0; cs < ks1; cs += CH) {
+    const int ce = min(cs + CH, ks1);
+    const int e0 = cs * 64, e1 = min(ce * 64, ka);
+    __syncthreads();  // previous chunk's list and bits are consumed
+    // list entries [e0, e1): one union word per wave, one bit per lane, rank
+    // by masked popcount; entries past e1 in the chunk point at row 0
+    for (int i = (e1 - e0) + tid; i < CH * 64; i += NT) {
+      sIdx[i] = -1;
+      sOff[i] = 0u;
+    }
+    for (int w = wave; w < Kw; w += NW) {
+      const int p0 = sP[w];
+      if (p0 >= e1 || sP[w + 1] <= e0) continue;  // wave-uniform
+      const unsigned long long u = sU[w];
+      const int e = p0 + __popcll(u & ((1ull << lane) - 1ull));
+      if (((u >> lane) & 1ull) && e >= e0 && e < e1) {
+        const int k = w * 64 + lane;
+        sIdx[e - e0] = k;
+        sOff[e - e0] = (uint32_t)k * (uint32_t)a.ldw;
+      }
+    }
+    __syncthreads();
+    const int jb = cs + wave * kGroup;
+    const int nv = min(kGroup, ce - jb);
+    if (nv <= 0) continue;  // wave-uniform
+
+    // weight loads of the whole group first
+    uint32_t xw[kGroup][16];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const uint4* po = reinterpret_cast<const uint4*>(sOff + (wave * kGroup + i) * 64 + 16 * g);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint4 o = po[u];
+        xw[i][4 * u + 0] = *reinterpret_cast<const uint32_t*>(Wb + o.x);
+        xw[i][4 * u + 1] = *reinterpret_cast<const uint32_t*>(Wb + o.y);
+        xw[i][4 * u + 2] = *reinterpret_cast<const uint32_t*>(Wb + o.z);
+        xw[i][4 * u + 3] = *reinterpret_cast<const uint32_t*>(Wb + o.w);
+      }
+    }
+    // while they are in flight: compact the spike bits of the tile rows onto
+    // this wave's active rows (lane = active row, one ballot per tile row)
+    unsigned long long* myBits = sBits + wave * kGroup * ROWS;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const int k = sIdx[(wave * kGroup + i) * 64 + lane];
+      const int kd = max(k, 0) >> 5, kb = k & 31;
+#pragma unroll
+      for (int lr = 0; lr < ROWS; ++lr) {
+        const bool bit = k >= 0 && ((sS[lr * lds_row + kd] >> kb) & 1u);
+        const unsigned long long m = __builtin_amdgcn_ballot_w64(bit);
+        if (lane == 0) myBits[i * ROWS + lr] = m;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      v4i b[4];
+      b_operands(xw[i], b);
+#pragma unroll
+      for (int q = 0; q < RT; ++q) {
+        const uint32_t b16 = (uint32_t)(myBits[i * ROWS + q * 16 + c] >> (16 * g)) & 0xFFFFu;
+        const v4i af = a_operand(b16);
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
+      }
+    }
+  }
+
+  __syncthreads();
+  reduce_tile<RT>(acc, sTile, g, c);
+  __syncthreads();
+  if (a.P > 1 && !split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z)) return;
+  epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
+}
+
+// ------------------------------------------------- list from the prep pass
+template <int RT, int NW>
+__global__ __launch_bounds__(NW * 64) void k_qbsm_list(QbsmArgs a) {
+  constexpr int ROWS = RT * 16;
+  constexpr int NT = NW * 64;
+  constexpr int CH = NW * kGroup;
+  __shared__ int sTile[ROWS * kTileLd];
+  __shared__ __attribute__((aligned(16))) uint32_t sOff[CH * 64];
+  __shared__ unsigned long long sUn[NW];
+  __shared__ EpiStage ep;
+  __shared__ int sLast;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  const int R = a.T * a.M;
+
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  stage_epilogue<NT>(a, ep, tid, x, y);
+  const int ka = *a.kact;
+  const int KS = (ka + 63) >> 6;
+  const int ks0 = (int)(((long long)KS * z) / a.P);
+  const int ks1 = (int)(((long long)KS * (z + 1)) / a.P);
+
+  int rowq[RT];
+  bool rowv[RT];
+#pragma unroll
+  for (int q = 0; q < RT; ++q) {
+    const int jr = q * 16 + c;
+    const int t = jr / a.Mb, ml = jr - t * a.Mb, m = y * a.Mb + ml;
+    rowv[q] = t < a.T && m < a.M;
+    rowq[q] = rowv[q] ? t * a.M + m : 0;
+  }
+  const uint32_t colb = (x * 64 + 4 * c < a.N) ? (uint32_t)(x * 64 + 4 * c) : (uint32_t)(x * 64);
+  const char* Wb = reinterpret_cast<const char*>(a.W) + colb;
+  const uint32_t* sc32 = reinterpret_cast<const uint32_t*>(a.sc);
+
+  v4i acc[RT][4];
+#pragma unroll
+  for (int q = 0; q < RT; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
+
+  for (int cs = ks0; cs < ks1; cs += CH) {
+    const int ce = min(cs + CH, ks1);
+    __syncthreads();
+    for (int i = tid; i < CH * 64; i += NT)
+      sOff[i] = (cs * 64 + i < ce * 64) ? a.act_off[(size_t)cs * 64 + i] : 0u;
+    __syncthreads();
+    const int jb = cs + wave * kGroup;
+    const int nv = min(kGroup, ce - jb);
+    if (nv <= 0) continue;  // wave-uniform
+
+    uint32_t xw[kGroup][16];
+    uint32_t bits[kGroup][RT];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const uint4* po = reinterpret_cast<const uint4*>(sOff + (wave * kGroup + i) * 64 + 16 * g);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint4 o = po[u];
+        xw[i][4 * u + 0] = *reinterpret_cast<const uint32_t*>(Wb + o.x);
+        xw[i][4 * u + 1] = *reinterpret_cast<const uint32_t*>(Wb + o.y);
+        xw[i][4 * u + 2] = *reinterpret_cast<const uint32_t*>(Wb + o.z);
+        xw[i][4 * u + 3] = *reinterpret_cast<const uint32_t*>(Wb + o.w);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const int j = min(jb + i, ce - 1);
+#pragma unroll
+      for (int q = 0; q < RT; ++q) {
+        const uint32_t raw = sc32[((size_t)j * R + rowq[q]) * 2 + (g >> 1)];
+        bits[i][q] = (rowv[q] && i < nv) ? (raw >> ((g & 1) * 16)) & 0xFFFFu : 0u;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      v4i b[4];
+      b_operands(xw[i], b);
+#pragma unroll
+      for (int q = 0; q < RT; ++q) {
+        const v4i af = a_operand(bits[i][q]);
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
+      }
+    }
+  }
+
+  __syncthreads();
+  reduce_tile<RT>(acc, sTile, g, c);
+  __syncthreads();
+  if (a.P > 1 && !split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z)) return;
+  epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -620,16 +729,21 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->counters = cv.take<int32_t>(s->n_counters);
 }
 
-template <int RT, int NW, bool FUSED>
-static void launch_k(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
-  hipLaunchKernelGGL((k_qbsm<RT, NW, FUSED>), grid, dim3(NW * 64), dyn, st, a);
+template <int RT, int NW>
+static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
+  hipLaunchKernelGGL((k_qbsm_fused<RT, NW>), grid, dim3(NW * 64), dyn, st, a);
 }
 
-// Static LDS of k_qbsm<RT, NW, true> (mirrors the declarations above).
+template <int RT, int NW>
+static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0, st, a);
+}
+
+// Static LDS of k_qbsm_fused<RT, NW> (mirrors its declarations).
 static size_t fused_static_lds(int RT, int NW) {
   const size_t ch = (size_t)NW * kGroup * 64;
   return (size_t)RT * 16 * kTileLd * 4 + ch * 4 * 2 + kFusedMaxWords * 8 + (kFusedMaxWords + 1) * 4 +
-         (size_t)NW * 12 + 64;
+         (size_t)NW * 12 + (size_t)NW * kGroup * RT * 16 * 8 + sizeof(EpiStage) + 64;
 }
 
 nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t st, int* gy_out) {
@@ -756,20 +870,20 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   if (c.ev_begin && hipEventRecord(c.ev_begin, st) != hipSuccess) return NMDLM_ERR_HIP;
   if (fused) {
     if (NW == 16) {
-      launch_k<1, 16, true>(grid, a, dyn, st);
+      launch_fused<1, 16>(grid, a, dyn, st);
     } else {
-      if (RT == 1) launch_k<1, 4, true>(grid, a, dyn, st);
-      else launch_k<2, 4, true>(grid, a, dyn, st);
+      if (RT == 1) launch_fused<1, 4>(grid, a, dyn, st);
+      else launch_fused<2, 4>(grid, a, dyn, st);
     }
   } else if (NW == 16) {
-    if (RT == 1) launch_k<1, 16, false>(grid, a, 0, st);
-    else launch_k<2, 16, false>(grid, a, 0, st);
+    if (RT == 1) launch_list<1, 16>(grid, a, st);
+    else launch_list<2, 16>(grid, a, st);
   } else {
     switch (RT) {
-      case 1: launch_k<1, 4, false>(grid, a, 0, st); break;
-      case 2: launch_k<2, 4, false>(grid, a, 0, st); break;
-      case 4: launch_k<4, 4, false>(grid, a, 0, st); break;
-      default: launch_k<8, 4, false>(grid, a, 0, st); break;
+      case 1: launch_list<1, 4>(grid, a, st); break;
+      case 2: launch_list<2, 4>(grid, a, st); break;
+      case 4: launch_list<4, 4>(grid, a, st); break;
+      default: launch_list<8, 4>(grid, a, st); break;
     }
   }
   const nmdlm_status rc = hip_status();
