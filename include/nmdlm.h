@@ -44,15 +44,22 @@ typedef enum nmdlm_status {
 /* flags (bitwise OR) */
 #define NMDLM_FORCE_DENSE 0x1u   /* read every weight row: the un-skipped product */
 #define NMDLM_NO_HEAD     0x2u   /* block step without head/confidence/unmask    */
+#define NMDLM_ATTN_FUSED  0x4u   /* block step: attention and the IF of its output
+                                    in one kernel (one workgroup per head and 16
+                                    queries, all timesteps); default is two
+                                    kernels.  Results do not depend on it.      */
 /* bits 8..15 of the flags of nmdlm_qbsm: force the number of K splits
  * (0 = automatic).  Results do not depend on it. */
 #define NMDLM_SPLIT_SHIFT 8u
 /* bits 16..19: force rows per tile group (0 = automatic; 1,2,4,8 = 16..128
  * rows).  Results do not depend on it. */
 #define NMDLM_ROWTILE_SHIFT 16u
-/* bit 20: build the active-row list in a separate pass instead of inside the
- * product kernel.  Results do not depend on it. */
-#define NMDLM_NO_FUSE 0x100000u
+/* bits 20..21: product kernel (0 = automatic; 1 = separate pass building the
+ * active-row list; 2 = single kernel with an in-kernel list; 3 = single
+ * kernel over 64-channel words, loading only active rows).  Results do not
+ * depend on it. */
+#define NMDLM_PATH_SHIFT 20u
+#define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)
 
 /* Supported envelope (NMDLM_ERR_UNSUPPORTED beyond it). */
 #define NMDLM_MAX_T 8

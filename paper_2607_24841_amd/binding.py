@@ -27,7 +27,11 @@ NMDLM_FORCE_DENSE = 0x1
 NMDLM_NO_HEAD = 0x2
 NMDLM_SPLIT_SHIFT = 8
 NMDLM_ROWTILE_SHIFT = 16
-NMDLM_NO_FUSE = 0x100000
+NMDLM_ATTN_FUSED = 0x4
+NMDLM_PATH_SHIFT = 20
+NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-row list
+NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
+NMDLM_PATH_WORDS = 3 << NMDLM_PATH_SHIFT   # single kernel over 64-channel words
 NMDLM_QNL_S8 = 0
 NMDLM_QNL_U8 = 1
 

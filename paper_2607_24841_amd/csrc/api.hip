@@ -150,6 +150,12 @@ nmdlm_status nmdlm_bbm_attn(const uint64_t* q, const uint64_t* k_cache, const ui
     a = static_cast<int32_t*>(ws);
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!a_out) {
+    // spikes only: one kernel with the IF fused in, when its LDS fits
+    const nmdlm_status rf = launch_attn_if(q, k_cache, vt_cache, cache_cap, T, M, C, H, dh,
+                                           lut_att, theta_a, s_out, nullptr, st);
+    if (rf != NMDLM_ERR_UNSUPPORTED) return rf;
+  }
   nmdlm_status rc = launch_attn(q, k_cache, vt_cache, cache_cap, T, M, C, H, dh, lut_att, a, st);
   if (rc != NMDLM_OK || !s_out) return rc;
   return launch_if(a, T, M, H * dh, theta_a, nullptr, nullptr, nullptr, s_out, st);

@@ -78,7 +78,8 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
 #pragma unroll
       for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & kw[s][w]);
       const bool jv = j0 + s < J;
-      const int p = jv ? sLut[sc] : 0;
+      const int pl = sLut[sc];
+      const int p = jv ? pl : 0;
       den += p;
       pk[s >> 2] |= jv ? (uint32_t)((p - 128) & 0xFF) << ((s & 3) * 8) : 0u;
     }
@@ -130,6 +131,208 @@ nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache, const uint6
     case 2:
       hipLaunchKernelGGL(k_attn<2>, grid, dim3(256), 0, st, q, k_cache, vt_cache, cap, T, M, C, H,
                          lut, a_out);
+      break;
+    default:
+      return NMDLM_ERR_UNSUPPORTED;
+  }
+  return hip_status();
+}
+
+// ---------------------------------------------------------------------------
+// Attention followed by the IF neuron of its output, in one kernel.
+// Workgroup = one head and 16 block queries for every timestep.  Wave =
+// (timestep t, part): the parts of a timestep take 64-key chunks in turn and
+// add their partial sums into LDS.  Per chunk a lane loads one key (row =
+// lane) and the value bits of one channel (= lane), and the wave exchanges
+// them through LDS; chunks go in rounds of kRound whose loads are all issued
+// before the first is scored.  Then one wave per (query, 64-channel word)
+// computes a = floor(256 num / den) and runs the IF recurrence over t,
+// writing the spike words and the token's union over t.
+// ---------------------------------------------------------------------------
+constexpr int kRound = 4;
+
+template <int DHW>
+struct KvChunk {
+  uint64_t kw[DHW];  // key row jc*64 + lane, this head's words
+  uint64_t vw[DHW];  // value bits of channel w*64 + lane over the chunk's keys
+};
+
+template <int DHW>
+__device__ __forceinline__ void load_chunk(KvChunk<DHW>& ch, const uint64_t* __restrict__ kc,
+                                           const uint64_t* __restrict__ vt, int64_t cap, int capw,
+                                           int t, int h, int d, int dw, int J, int jc, int lane) {
+  constexpr int DH = DHW * 64;
+  const int jj = min(jc * 64 + lane, J - 1);  // past C+M: a valid row, masked when scored
+  const uint64_t* kr = kc + ((size_t)t * cap + jj) * dw + h * DHW;
+#pragma unroll
+  for (int w = 0; w < DHW; ++w) {
+    ch.kw[w] = kr[w];
+    ch.vw[w] = vt[((size_t)t * d + h * DH + w * 64 + lane) * capw + jc];
+  }
+}
+
+// sK, sV: this wave's 64 x DHW key words and DH value words in LDS
+// lut_dw: table bytes 4*lane .. 4*lane+3 (entry s is read from lane s/4)
+template <int DHW>
+__device__ __forceinline__ void score_chunk(const KvChunk<DHW>& ch, const uint64_t (&qw)[DHW],
+                                            int lut_dw, uint64_t* sK, uint64_t* sV, int J,
+                                            int jc, int lane, int g, int c, v4i (&acc)[DHW * 4],
+                                            int (&cnt)[DHW * 4], int& den) {
+  const int j0 = jc * 64 + 16 * g;
+#pragma unroll
+  for (int w = 0; w < DHW; ++w) {
+    sK[lane * DHW + w] = ch.kw[w];
+    sV[w * 64 + lane] = ch.vw[w];
+  }
+  __builtin_amdgcn_wave_barrier();
+  uint32_t pk[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    int sc = 0;
+#pragma unroll
+    for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & sK[(16 * g + s) * DHW + w]);
+    const bool jv = j0 + s < J;
+    const int pw = __builtin_amdgcn_ds_bpermute((sc >> 2) << 2, lut_dw);
+    const int p = jv ? (pw >> ((sc & 3) * 8)) & 0xFF : 0;
+    den += p;
+    pk[s >> 2] |= jv ? (uint32_t)((p - 128) & 0xFF) << ((s & 3) * 8) : 0u;
+  }
+  const v4i af = v4i{(int)pk[0], (int)pk[1], (int)pk[2], (int)pk[3]};
+  const int nvalid = J - j0;
+  const uint32_t vmask = nvalid >= 16 ? 0xFFFFu : (nvalid <= 0 ? 0u : ((1u << nvalid) - 1u));
+#pragma unroll
+  for (int nt = 0; nt < DHW * 4; ++nt) {
+    const uint32_t bits = (uint32_t)(sV[nt * 16 + c] >> (16 * g)) & vmask;
+    cnt[nt] += __popc(bits);
+    const v4i bf = v4i{(int)expand4_a(bits & 0xFu), (int)expand4_a((bits >> 4) & 0xFu),
+                       (int)expand4_a((bits >> 8) & 0xFu), (int)expand4_a(bits >> 12)};
+    acc[nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf, acc[nt], 0, 0, 0);
+  }
+  __builtin_amdgcn_wave_barrier();  // sK and sV are rewritten by the next chunk
+}
+
+template <int DHW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_if(const uint64_t* __restrict__ q,
+                                                     const uint64_t* __restrict__ kc,
+                                                     const uint64_t* __restrict__ vt, int64_t cap,
+                                                     int T, int M, int C, int H,
+                                                     const uint8_t* __restrict__ lut,
+                                                     int32_t theta, uint64_t* __restrict__ s_out,
+                                                     uint64_t* __restrict__ u_out) {
+  constexpr int DH = DHW * 64;
+  constexpr int NT = DHW * 4;
+  constexpr int NTH = NW * 64;
+  __shared__ int sDen[NMDLM_MAX_T][16];
+  __shared__ int sCnt[NMDLM_MAX_T][DH];
+  __shared__ uint64_t sKey[NW][64 * DHW];
+  __shared__ uint64_t sVal[NW][DH];
+  extern __shared__ int sNum[];  // [T][16][DH]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int h = blockIdx.x, qb = blockIdx.y;
+  const int d = H * DH, dw = d / 64;
+  const int capw = (int)(cap / 64);
+  const int J = C + M;
+  const int nch = (J + 63) / 64;
+  const int tp = T <= 1 ? 1 : (T <= 2 ? 2 : (T <= 4 ? 4 : 8));
+  const int NP = NW / tp;  // parts per timestep
+  const int t = wave / NP, part = wave - t * NP;
+  const bool active = t < T && part < nch;  // wave-uniform
+  const int tl = min(t, T - 1);             // idle waves load valid rows and discard them
+
+  // table, query words and the first round of chunks: unconditional loads in
+  // one straight run, so each wait covers only what it needs
+  const int lut_dw = (int)reinterpret_cast<const uint32_t*>(lut)[lane];
+  const int iq = qb * 16 + c;
+  uint64_t qw[DHW];
+#pragma unroll
+  for (int w = 0; w < DHW; ++w) qw[w] = q[((size_t)tl * M + min(iq, M - 1)) * dw + h * DHW + w];
+  KvChunk<DHW> ch[kRound];
+#pragma unroll
+  for (int u = 0; u < kRound; ++u)
+    load_chunk<DHW>(ch[u], kc, vt, cap, capw, tl, h, d, dw, J, min(part + u * NP, nch - 1), lane);
+
+  for (int i = tid; i < NMDLM_MAX_T * 16; i += NTH) (&sDen[0][0])[i] = 0;
+  for (int i = tid; i < NMDLM_MAX_T * DH; i += NTH) (&sCnt[0][0])[i] = 0;
+  for (int i = tid; i < T * 16 * DH; i += NTH) sNum[i] = 0;
+  __syncthreads();
+
+  if (active) {
+#pragma unroll
+    for (int w = 0; w < DHW; ++w) qw[w] = iq < M ? qw[w] : 0ull;
+    v4i acc[NT];
+    int cnt[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      acc[i] = v4i{0, 0, 0, 0};
+      cnt[i] = 0;
+    }
+    int den = 0;
+    uint64_t* sK = sKey[wave];
+    uint64_t* sV = sVal[wave];
+    for (int jr = part;;) {
+#pragma unroll
+      for (int u = 0; u < kRound; ++u) {
+        const int jc = jr + u * NP;
+        if (jc < nch) score_chunk<DHW>(ch[u], qw, lut_dw, sK, sV, J, jc, lane, g, c, acc, cnt, den);
+      }
+      jr += kRound * NP;
+      if (jr >= nch) break;
+#pragma unroll
+      for (int u = 0; u < kRound; ++u)
+        load_chunk<DHW>(ch[u], kc, vt, cap, capw, t, h, d, dw, J, min(jr + u * NP, nch - 1), lane);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (acc[nt][e]) atomicAdd(&sNum[(t * 16 + g * 4 + e) * DH + nt * 16 + c], acc[nt][e]);
+    if (den) atomicAdd(&sDen[t][c], den);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      if (cnt[nt]) atomicAdd(&sCnt[t][nt * 16 + c], cnt[nt]);
+  }
+  __syncthreads();
+
+  for (int task = wave; task < 16 * DHW; task += NW) {
+    const int i = task / DHW, w = task - i * DHW;
+    const int iq2 = qb * 16 + i;
+    if (iq2 >= M) break;  // wave-uniform; later tasks have larger i
+    const int chn = w * 64 + lane;
+    long long V = 0;
+    uint64_t uor = 0ull;
+    for (int tt = 0; tt < T; ++tt) {
+      const long long num = (long long)sNum[(tt * 16 + i) * DH + chn] + 128LL * sCnt[tt][chn];
+      const long long dn = sDen[tt][i];
+      V += dn > 0 ? (256LL * num) / dn : 0LL;
+      const bool s = V >= theta;
+      if (s) V -= theta;
+      const uint64_t word = __builtin_amdgcn_ballot_w64(s);
+      uor |= word;
+      if (lane == 0) s_out[((size_t)tt * M + iq2) * dw + h * DHW + w] = word;
+    }
+    if (u_out && lane == 0) u_out[(size_t)iq2 * dw + h * DHW + w] = uor;
+  }
+}
+
+constexpr size_t kAttnIfMaxLds = 49152;  // bytes of [T][16][dh] partial sums
+
+nmdlm_status launch_attn_if(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,
+                            int64_t cap, int T, int M, int C, int H, int dh, const uint8_t* lut,
+                            int32_t theta, uint64_t* s_out, uint64_t* u_out, hipStream_t st) {
+  const size_t dyn = (size_t)T * 16 * dh * sizeof(int);
+  if (dyn > kAttnIfMaxLds || T > NMDLM_MAX_T) return NMDLM_ERR_UNSUPPORTED;
+  if (reinterpret_cast<uintptr_t>(lut) % 4 != 0) return NMDLM_ERR_UNSUPPORTED;  // read as dwords
+  const dim3 grid(H, (M + 15) / 16);
+  switch (dh / 64) {
+    case 1:
+      hipLaunchKernelGGL((k_attn_if<1, 16>), grid, dim3(16 * 64), dyn, st, q, k_cache, vt_cache,
+                         cap, T, M, C, H, lut, theta, s_out, u_out);
+      break;
+    case 2:
+      hipLaunchKernelGGL((k_attn_if<2, 8>), grid, dim3(8 * 64), dyn, st, q, k_cache, vt_cache,
+                         cap, T, M, C, H, lut, theta, s_out, u_out);
       break;
     default:
       return NMDLM_ERR_UNSUPPORTED;

@@ -162,6 +162,11 @@ nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache,
                          const uint64_t* vt_cache, int64_t cap, int T, int M, int C,
                          int H, int dh, const uint8_t* lut, int32_t* a_out,
                          hipStream_t st);
+// attention with the IF of its output fused in (spikes and per-token union
+// over t); NMDLM_ERR_UNSUPPORTED when T*16*dh partial sums exceed its LDS
+nmdlm_status launch_attn_if(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,
+                            int64_t cap, int T, int M, int C, int H, int dh, const uint8_t* lut,
+                            int32_t theta, uint64_t* s_out, uint64_t* u_out, hipStream_t st);
 nmdlm_status launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
 inline nmdlm_status hip_status() {

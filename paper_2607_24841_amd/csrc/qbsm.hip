@@ -208,7 +208,7 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs p) {
 // k_qbsm_fused builds the union, the active-row list and the compacted
 // spike bits in LDS itself; k_qbsm_list reads them from the prep pass.
 // ---------------------------------------------------------------------------
-constexpr int kGroup = 4;
+constexpr int kGroup = 2;
 constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
 constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
@@ -248,6 +248,7 @@ struct EpiStage {
   int bias[64];
   int theta[64];
   unsigned long long resid[kMaxEpiTokens];  // [t * Mb + token]
+  signed char lut[256];                     // activation table (EPI_QNL_IF)
 };
 
 template <int NT>
@@ -263,6 +264,8 @@ __device__ __forceinline__ void stage_epilogue(const QbsmArgs& a, EpiStage& ep, 
       ep.resid[i] = m < a.M ? a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x] : 0ull;
     }
   }
+  if (a.mode == EPI_QNL_IF)
+    for (int i = tid; i < 256; i += NT) ep.lut[i] = (signed char)a.lut[i];
 }
 
 // Sum the waves' accumulators into the LDS tile (physical column order).
@@ -364,7 +367,7 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep
           if (a.mode == EPI_QNL_IF) {
             int qv = I >> a.lut_shift;
             qv = min(127, max(-128, qv));
-            I = (int)(int8_t)a.lut[qv & 0xFF];
+            I = (int)ep.lut[qv & 0xFF];
           }
           if (a.resid) {
             const unsigned long long rw =
@@ -417,6 +420,161 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep
   }
 }
 
+// ------------------------------------------------- word-granular product
+// k-steps are the original 64-channel words.  The A operand comes straight
+// from the staged spike rows (no list, no compaction).  Within a word, a lane
+// loads only the rows active in this tile's rows (its local union): a row
+// absent from the local union has a zero spike in every tile row, so its B
+// slot (left stale) is multiplied by zero.  Across row blocks the rows read
+// are the block union; repeated reads hit the cache.  Words with no active
+// row are skipped.
+template <int RT, int NW>
+__global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
+  constexpr int ROWS = RT * 16;
+  constexpr int NT = NW * 64;
+  __shared__ int sTile[ROWS * kTileLd];
+  __shared__ unsigned long long sUn[NW];
+  __shared__ int sRed[NW];
+  __shared__ EpiStage ep;
+  __shared__ int sLast;
+  // dynamic: local union [Kw] (u64), then the tile's spike rows as dwords
+  // with row stride 2*Kw+1 (odd: the 16 rows a wave reads fall in different banks)
+  extern __shared__ unsigned long long sDyn[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  const int Kw = (a.K + 63) >> 6;
+  const int lds_row = 2 * Kw + 1;
+  unsigned long long* sLU = sDyn;
+  uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + Kw);
+
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  stage_epilogue<NT>(a, ep, tid, x, y);
+  for (int i = tid; i < ROWS * Kw; i += NT) {
+    const int lr = i / Kw, w = i - lr * Kw;
+    const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
+    const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
+    sS[lr * lds_row + 2 * w] = (uint32_t)v;
+    sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
+  }
+  __syncthreads();
+  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
+  for (int w = tid; w < Kw; w += NT) {
+    unsigned long long u = ~0ull;
+    if (!a.dense) {
+      u = 0ull;
+      for (int lr = 0; lr < ROWS; ++lr)
+        u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
+             ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+    }
+    sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
+  }
+  __syncthreads();
+
+  const int w0 = (int)(((long long)Kw * z) / a.P);
+  const int w1 = (int)(((long long)Kw * (z + 1)) / a.P);
+  const uint32_t colb = (x * 64 + 4 * c < a.N) ? (uint32_t)(x * 64 + 4 * c) : (uint32_t)(x * 64);
+  const uint32_t ldw = (uint32_t)a.ldw;
+  const uint32_t lane_base = (uint32_t)(16 * g) * ldw + colb;   // row 16g of word 0
+  const char* Wb = reinterpret_cast<const char*>(a.W);
+
+  v4i acc[RT][4];
+#pragma unroll
+  for (int q = 0; q < RT; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
+  uint32_t xw[kGroup][16];
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i)
+#pragma unroll
+    for (int s2 = 0; s2 < 16; ++s2) xw[i][s2] = 0u;
+
+  for (int jb = w0 + wave * kGroup; jb < w1; jb += NW * kGroup) {
+    unsigned long long uw[kGroup];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) uw[i] = (jb + i < w1) ? sLU[jb + i] : 0ull;
+    // loads of the group's active rows
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      if (uw[i] == 0ull) continue;  // wave-uniform
+      const uint32_t m16 = (uint32_t)(uw[i] >> (16 * g)) & 0xFFFFu;
+      const uint32_t wbase = (uint32_t)(jb + i) * 64u * ldw;
+      if (m16 == 0xFFFFu) {
+#pragma unroll
+        for (int s2 = 0; s2 < 16; ++s2)
+          xw[i][s2] = *reinterpret_cast<const uint32_t*>(Wb + (lane_base + (wbase + (uint32_t)s2 * ldw)));
+      } else {
+#pragma unroll
+        for (int s2 = 0; s2 < 16; ++s2)
+          if ((m16 >> s2) & 1u)
+            xw[i][s2] = *reinterpret_cast<const uint32_t*>(Wb + (lane_base + (wbase + (uint32_t)s2 * ldw)));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      if (uw[i] == 0ull) continue;  // wave-uniform
+      const int w = jb + i;
+      v4i b[4];
+      b_operands(xw[i], b);
+#pragma unroll
+      for (int q = 0; q < RT; ++q) {
+        const uint32_t b16 = (sS[(q * 16 + c) * lds_row + 2 * w + (g >> 1)] >> (16 * (g & 1))) & 0xFFFFu;
+        const v4i af = a_operand(b16);
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
+      }
+    }
+  }
+
+  __syncthreads();
+  reduce_tile<RT>(acc, sTile, g, c);
+  __syncthreads();
+  const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
+  if (last) epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
+
+  // statistics of the whole block (the block union), by one workgroup: each
+  // thread ORs a slice of the sources of one word, then one LDS OR per thread
+  if (a.stats && x == 0 && y == 0 && z == 0) {
+    __syncthreads();
+    for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
+    __syncthreads();
+    const int nsrc = a.dense ? 0 : (a.upart ? a.nparts : a.T * a.M);
+    const int slices = NT >= Kw ? NT / Kw : 1;
+    const int s0 = NT >= Kw ? tid / Kw : 0;
+    if (s0 < slices) {
+      for (int w = NT >= Kw ? tid % Kw : tid; w < Kw; w += (NT >= Kw ? Kw : NT)) {
+        unsigned long long u = 0ull;
+        if (a.upart) {
+          for (int q = s0; q < nsrc; q += slices) u |= a.upart[(size_t)q * Kw + w];
+        } else {
+          for (int r = s0; r < nsrc; r += slices) u |= a.S[(size_t)r * Kw + w];
+        }
+        if (u) atomicOr(&sLU[w], u);
+        if (NT >= Kw) break;
+      }
+    }
+    __syncthreads();
+    int cnt = 0;
+    for (int w = tid; w < Kw; w += NT) {
+      const unsigned long long u = a.dense ? ~0ull : sLU[w];
+      cnt += __popcll((w == Kw - 1) ? (u & last_mask) : u);
+    }
+    for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+    if (lane == 0) sRed[wave] = cnt;
+    __syncthreads();
+    if (tid == 0) {
+      int total = 0;
+      for (int i = 0; i < NW; ++i) total += sRed[i];
+      a.stats->k_total = a.K;
+      a.stats->k_active = total;
+      a.stats->n = a.N;
+      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
+    }
+  }
+}
+
 // -------------------------------------------------------------- single kernel
 template <int RT, int NW>
 __global__ __launch_bounds__(NW * 64) void k_qbsm_fused(QbsmArgs a) {
@@ -430,7 +588,10 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_fused(QbsmArgs a) {
   __shared__ int sP[kFusedMaxWords + 1];
   __shared__ int sWave[NW];
   __shared__ unsigned long long sUn[NW];
-  __shared__ unsigned long long sBits[NW * kGroup * ROWS];  // compacted bits per wave/step/row
+  // compacted bits per wave/step/row; before the main loop also the column-OR
+  // scratch of up to NT words
+  constexpr int kBitsLen = (NW * kGroup * ROWS > NT) ? NW * kGroup * ROWS : NT;
+  __shared__ unsigned long long sBits[kBitsLen];
   __shared__ EpiStage ep;
   __shared__ int sLast;
   // this tile's spike rows as dwords, row stride 2*Kw+1 (odd: the rows a
@@ -735,15 +896,27 @@ static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
 }
 
 template <int RT, int NW>
+static void launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
+  hipLaunchKernelGGL((k_qbsm_words<RT, NW>), grid, dim3(NW * 64), dyn, st, a);
+}
+
+template <int RT, int NW>
 static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0, st, a);
+}
+
+// Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
+static size_t words_lds(int RT, int NW, int Kw) {
+  return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
+         (size_t)Kw * 8 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
 }
 
 // Static LDS of k_qbsm_fused<RT, NW> (mirrors its declarations).
 static size_t fused_static_lds(int RT, int NW) {
   const size_t ch = (size_t)NW * kGroup * 64;
+  const size_t bits = std::max((size_t)NW * kGroup * RT * 16, (size_t)NW * 64);
   return (size_t)RT * 16 * kTileLd * 4 + ch * 4 * 2 + kFusedMaxWords * 8 + (kFusedMaxWords + 1) * 4 +
-         (size_t)NW * 12 + (size_t)NW * kGroup * RT * 16 * 8 + sizeof(EpiStage) + 64;
+         (size_t)NW * 12 + bits * 8 + sizeof(EpiStage) + 64;
 }
 
 nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t st, int* gy_out) {
@@ -755,11 +928,15 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   if (c.mode == EPI_IF || c.mode == EPI_QNL_IF)
     for (int i = 0; i < c.nseg; ++i) has_tr = has_tr || c.seg[i].transposed;
 
-  // rows per tile group: the largest that still gives >= 256 workgroups,
-  // else the smallest (most row blocks; they re-read weights from L2)
+  // product path: 1 = prep pass + list kernel, 2 = single kernel with a
+  // compacted list, 3 = word-granular single kernel, 0 = automatic
+  int path = (int)((c.flags >> NMDLM_PATH_SHIFT) & 0x3u);
   const int rt_full = pick_rt(R);
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
-  if (RT != 1 && RT != 2 && RT != 4 && RT != 8) {
+  const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
+  if (!rt_forced) {
+    // rows per tile group: the largest that still gives >= 256 workgroups,
+    // else the smallest (most row blocks; they re-read weights from L2)
     RT = 1;
     for (int r = rt_full; r >= 1; r >>= 1) {
       const int mb = (16 * r) / c.T;
@@ -771,6 +948,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   }
   while (RT > 1 && 16 * RT / 2 >= R && 16 * RT / 2 >= c.T) RT >>= 1;  // no empty tiles
   while (has_tr && RT > 1 && (16 * RT) / c.T > 64) RT >>= 1;
+  if (path == 0) {
+    path = 3;
+    while (RT > 1 && words_lds(RT, 4, Kw) > kLdsBudget && !rt_forced) RT >>= 1;
+    if (words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
+  }
+  if (path == 3 && words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
   const int Mb = (16 * RT) / c.T;
   const int gy = (c.M + Mb - 1) / Mb;
@@ -790,14 +973,24 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   // waves per workgroup: many when each workgroup has many k-steps
   const int ks_per_wg = (Kw + P - 1) / P;
   int NW = (ks_per_wg >= 8 * kGroup && RT <= 2) ? 16 : 4;
-  // one kernel (union, list and spike gathers in LDS) when the tile's spike
-  // rows fit; else a separate prep pass builds them in global memory
-  const size_t dyn = (size_t)16 * RT * (2 * Kw + 1) * 4;
-  bool fused = !(c.flags & NMDLM_NO_FUSE) && Kw <= kFusedMaxWords && RT <= 2;
-  if (fused && RT == 2) NW = 4;  // the 16-wave variant of RT=2 would spill registers
-  if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) NW = 4;
-  if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) fused = false;
-  if (fused && !c.u_in && !dense && (long long)R * Kw > kUnionDirect) fused = false;
+  size_t dyn = 0;
+  bool fused = false, words = false;
+  if (path == 3) {
+    words = true;
+    // 8 waves, not 16: a 1024-thread bound caps registers at 128 and spills
+    NW = (ks_per_wg >= 8 * kGroup && RT == 1) ? 16 : ((ks_per_wg >= 4 * kGroup && RT <= 2) ? 8 : 4);
+    if (words_lds(RT, NW, Kw) > kLdsBudget) NW = 4;
+    dyn = (size_t)Kw * 8 + (size_t)16 * RT * (2 * Kw + 1) * 4;
+  } else if (path == 2) {
+    // one kernel (union, list and spike compaction in LDS) when the tile's
+    // spike rows fit; else the prep pass builds them in global memory
+    dyn = (size_t)16 * RT * (2 * Kw + 1) * 4;
+    fused = Kw <= kFusedMaxWords && RT <= 2;
+    if (fused && RT == 2) NW = 4;  // the 16-wave variant of RT=2 would spill registers
+    if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) NW = 4;
+    if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) fused = false;
+    if (fused && !c.u_in && !dense && (long long)R * Kw > kUnionDirect) fused = false;
+  }
 
   nmdlm_status rc0 = NMDLM_OK;
   PrepArgs pa;
@@ -817,7 +1010,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   pa.counters = scr.counters;
   pa.n_counters = tiles;
   pa.sc = scr.sc;
-  if (!fused) {
+  if (!fused && !words) {
     if (!dense && !pa.upart && (long long)R * Kw > kUnionDirect) {
       hipLaunchKernelGGL(k_union, dim3(Kw), dim3(256), 0, st, c.s_in, R, Kw, scr.U);
       pa.upart = scr.U;
@@ -825,7 +1018,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     }
     hipLaunchKernelGGL(k_prep, dim3(Kw, (R + kPrepRows - 1) / kPrepRows), dim3(256), 0, st, pa);
   } else if (tiles > 0) {
-    // the fused kernel zeroes no counters: clear them for a split product
+    // the single-kernel paths zero no counters: clear them for a split product
     if (P > 1 && (rc0 = launch_fill_zero(scr.counters, align_up((size_t)tiles * 4, 16), st)) != NMDLM_OK)
       return rc0;
   }
@@ -868,7 +1061,21 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
 
   const dim3 grid(gx, gy, P);
   if (c.ev_begin && hipEventRecord(c.ev_begin, st) != hipSuccess) return NMDLM_ERR_HIP;
-  if (fused) {
+  if (words) {
+    if (NW == 16) {
+      launch_words<1, 16>(grid, a, dyn, st);
+    } else if (NW == 8) {
+      if (RT == 1) launch_words<1, 8>(grid, a, dyn, st);
+      else launch_words<2, 8>(grid, a, dyn, st);
+    } else {
+      switch (RT) {
+        case 1: launch_words<1, 4>(grid, a, dyn, st); break;
+        case 2: launch_words<2, 4>(grid, a, dyn, st); break;
+        case 4: launch_words<4, 4>(grid, a, dyn, st); break;
+        default: launch_words<8, 4>(grid, a, dyn, st); break;
+      }
+    }
+  } else if (fused) {
     if (NW == 16) {
       launch_fused<1, 16>(grid, a, dyn, st);
     } else {

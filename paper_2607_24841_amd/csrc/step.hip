@@ -202,7 +202,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.scale = nullptr;
   c.stats = stats;
   c.flags = flags & (NMDLM_FORCE_DENSE | (0xFFu << NMDLM_SPLIT_SHIFT) | (0xFu << NMDLM_ROWTILE_SHIFT) |
-                     NMDLM_NO_FUSE);
+                     (0x3u << NMDLM_PATH_SHIFT));
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
   c.u_in = nullptr;
@@ -265,12 +265,17 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     attach_events(qkv, io, 4 * l + 0);
     if ((rc = launch_qbsm(qkv, b.qs, st)) != NMDLM_OK) return rc;
 
-    if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att, b.a,
-                          st)) != NMDLM_OK)
-      return rc;
-    if ((rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st, b.uA)) !=
-        NMDLM_OK)
-      return rc;
+    rc = NMDLM_ERR_UNSUPPORTED;
+    if (io->flags & NMDLM_ATTN_FUSED)
+      rc = launch_attn_if(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att,
+                          ly.theta_a, b.A, b.uA, st);
+    if (rc == NMDLM_ERR_UNSUPPORTED) {
+      if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att, b.a,
+                            st)) != NMDLM_OK)
+        return rc;
+      rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st, b.uA);
+    }
+    if (rc != NMDLM_OK) return rc;
 
     QbsmCall o = base_call(b.A, T, M, d, ly.w_o, d, d, EPI_IF, io->flags, stl ? stl + 1 : nullptr);
     o.seg[0] = natural_seg(b.X1, sp_t, dw, ly.theta_o);

@@ -82,7 +82,8 @@ def _chosen_ok(got, want, conf, tol=1e-9):
     return False
 
 
-def test_config4_block_step_matches_stored_oracle():
+@pytest.mark.parametrize("flags", [0, 0x4], ids=["default", "attn-fused"])
+def test_config4_block_step_matches_stored_oracle(flags):
     torch, B = need_gpu()
     ref = _load("cfg4_block_step.json")
     case = synth.config4()
@@ -92,7 +93,7 @@ def test_config4_block_step_matches_stored_oracle():
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
                          B.nmdlm_block_step_workspace_size(dm, M, 0)))
     ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()
-    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, tokens=ctx,
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD | flags, tokens=ctx,
                                      masked=torch.zeros(C, dtype=torch.uint8, device="cuda")), ws)
     tok = torch.zeros(M, dtype=torch.int32, device="cuda")
     msk = torch.ones(M, dtype=torch.uint8, device="cuda")
@@ -102,7 +103,8 @@ def test_config4_block_step_matches_stored_oracle():
     chosen = torch.empty(k, dtype=torch.int32, device="cuda")
     y = torch.empty((m.T, M, m.d // 64), dtype=torch.int64, device="cuda")
     stats = torch.zeros((4 * m.n_layers + 1, 4), dtype=torch.int64, device="cuda")
-    B.nmdlm_block_step(dm, B.step_io(M, C, pos0=C, tokens=tok, masked=msk, k_unmask=k, y_out=y,
+    B.nmdlm_block_step(dm, B.step_io(M, C, pos0=C, flags=flags, tokens=tok, masked=msk,
+                                     k_unmask=k, y_out=y,
                                      logits=logits, pred=pred, conf=conf, unmasked_pos=chosen,
                                      stats=stats), ws)
     torch.cuda.synchronize()

@@ -132,6 +132,40 @@ def test_attention_parity(shape):
     assert_same(s, O.if_neuron(a_ref, 300)[0])
 
 
+def _attn_spikes_gpu(Q, Kc, Vc, lut, cap, C, H, dh, theta):
+    """Spikes only (no currents out): the attention kernel with the IF fused
+    in, or attention + IF when its partial sums do not fit in LDS."""
+    torch, B = need_gpu()
+    T, M, d = Q.shape
+    q = B.to_dev_bits(synth.pack_bits(Q))
+    k = B.to_dev_bits(synth.pack_bits(Kc))
+    vt = B.to_dev_bits(synth.pack_bits(Vc.transpose(0, 2, 1)))
+    s_out = torch.full((T, M, d // 64), -1, dtype=torch.int64, device="cuda")
+    ws = B.workspace(B.nmdlm_bbm_attn_workspace_size(T, M, H, dh))
+    B.nmdlm_bbm_attn(q, k, vt, cap, T, M, C, H, dh, torch.from_numpy(lut).cuda(),
+                     theta_a=theta, s_out=s_out, ws=ws)
+    torch.cuda.synchronize()
+    return synth.unpack_bits(B.from_dev_bits(s_out), d)
+
+
+ATTN_SPIKES = ATTN + [
+    (8, 20, 70, 2, 64, 0.3),       # T = 8, fused
+    (8, 9, 130, 2, 128, 0.3),      # T = 8, dh = 128: partial sums exceed LDS, two kernels
+    (5, 33, 200, 1, 128, 0.2),     # T not a power of two
+]
+
+
+@pytest.mark.parametrize("shape", ATTN_SPIKES,
+                         ids=[f"T{s[0]}M{s[1]}C{s[2]}H{s[3]}dh{s[4]}" for s in ATTN_SPIKES])
+def test_attention_spikes_only_parity(shape):
+    T, M, C, H, dh, p = shape
+    Q, Kc, Vc, lut, cap = _attn_case(sum(shape[:5]) + 1, T, M, C, H, dh, p)
+    for theta in (300, 7):
+        s = _attn_spikes_gpu(Q, Kc, Vc, lut, cap, C, H, dh, theta)
+        a_ref = O.bbm_attention(Q, Kc, Vc, C + M, H, lut)
+        assert_same(s, O.if_neuron(a_ref, theta)[0], f"theta {theta}")
+
+
 def test_attention_closed_forms_on_gpu():
     Q, Kc, Vc, _, cap = _attn_case(3, 2, 8, 50, 2, 64, 0.4, stale=False)
     const = np.full(256, 9, dtype=np.uint8)

@@ -53,21 +53,31 @@ def test_tiny_and_ragged_shapes(shape):
     _check(synth.make_qbsm_case(100 + K + N, T, M, K, N, p))
 
 
-NOFUSE = 0x100000
+NOFUSE = 1 << 20      # prep pass + list kernel
+FUSED = 2 << 20       # single kernel, in-kernel list
+WORDS = 3 << 20       # single kernel over 64-channel words
+
+_FORCED = {
+    "dense": 0x1, "P1": 1 << 8, "P2": 2 << 8, "P7": 7 << 8, "RT1": 1 << 16, "RT2": 2 << 16,
+    "RT4": 4 << 16, "RT8": 8 << 16, "P3RT1": (3 << 8) | (1 << 16),
+    "nofuse": NOFUSE, "nofuse-dense": NOFUSE | 0x1, "nofuse-P2": NOFUSE | (2 << 8),
+    "nofuse-RT1": NOFUSE | (1 << 16), "nofuse-RT8": NOFUSE | (8 << 16),
+    "fused": FUSED, "fused-dense": FUSED | 0x1, "fused-P2": FUSED | (2 << 8),
+    "fused-RT1": FUSED | (1 << 16), "fused-RT2": FUSED | (2 << 16),
+    "words": WORDS, "words-dense": WORDS | 0x1, "words-P3": WORDS | (3 << 8),
+    "words-RT1": WORDS | (1 << 16), "words-RT4": WORDS | (4 << 16), "words-RT8": WORDS | (8 << 16),
+    "words-P2RT2": WORDS | (2 << 8) | (2 << 16),
+}
 
 
-@pytest.mark.parametrize("flags", [0x1, 1 << 8, 2 << 8, 7 << 8, 1 << 16, 2 << 16, 4 << 16, 8 << 16,
-                                   (3 << 8) | (1 << 16), NOFUSE, NOFUSE | 0x1, NOFUSE | (2 << 8),
-                                   NOFUSE | (1 << 16), NOFUSE | (8 << 16)],
-                         ids=["dense", "P1", "P2", "P7", "RT1", "RT2", "RT4", "RT8", "P3RT1", "nofuse",
-                              "nofuse-dense", "nofuse-P2", "nofuse-RT1", "nofuse-RT8"])
+@pytest.mark.parametrize("flags", list(_FORCED.values()), ids=list(_FORCED))
 def test_forced_paths_equal(flags):
     need_gpu()
     case = synth.make_qbsm_case(5, 4, 24, 700, 300, 0.05)
     _check(case, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, NOFUSE], ids=["fused", "nofuse"])
+@pytest.mark.parametrize("flags", [0, NOFUSE, FUSED, WORDS], ids=["auto", "nofuse", "fused", "words"])
 def test_degenerate_inputs(flags):
     need_gpu()
     c = synth.make_qbsm_case(9, 4, 8, 256, 128, 0.1)
@@ -77,11 +87,12 @@ def test_degenerate_inputs(flags):
     _check(c, flags=flags)
 
 
-def test_large_k_shapes():
+@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS], ids=["auto", "nofuse", "words"])
+def test_large_k_shapes(flags):
     need_gpu()
-    # K beyond the single-kernel limit, and a long block (many row blocks)
-    _check(synth.make_qbsm_case(41, 4, 4, 20000, 130, 0.02))
-    _check(synth.make_qbsm_case(42, 4, 300, 700, 200, 0.05))
+    # K beyond the in-kernel-list limit, and a long block (many row blocks)
+    _check(synth.make_qbsm_case(41, 4, 4, 20000, 130, 0.02), flags=flags)
+    _check(synth.make_qbsm_case(42, 4, 300, 700, 200, 0.05), flags=flags)
 
 
 def test_per_neuron_thresholds_and_currents_only():
