@@ -16,6 +16,17 @@ Prints one JSON line with block-denoise tokens/s, the weight-skip fraction,
 the touched-weight bandwidth of the whole step, the roofline of the product
 kernel (timed per launch with HIP events recorded by the library around the
 kernel) and the CPU oracle's rate on a bounded sample.
+
+Other workloads (--config):
+  3  FFN weight-traffic sweep, d=4096 -> 14336 -> 4096, T=4, B in {1,4,16,64},
+     mean input density in {.02,.05,.10,.30}: skipped-row fraction, touched
+     bytes and GB/s of the up and down products at every point (4 rotating
+     weight copies, 470 MB, so that weights stream from HBM).
+  4  12-layer MDLM (d=2048, 16 heads of 128, FFN 8192, vocab 32000, T=4), one
+     block step of 32 masked tokens over 1024 context tokens with head,
+     confidence and top-8 unmasking (640 MB of weights per step).
+  5  24-layer MDLM generation: prompt of 2048 ids, 8 blocks of 32 tokens,
+     8 steps per block, 4 tokens unmasked per step.
 """
 from __future__ import annotations
 
@@ -40,6 +51,9 @@ def parse():
     p.add_argument("--seed", type=int, default=1002)
     p.add_argument("--flags", type=lambda x: int(x, 0), default=0,
                    help="extra block-step flags (path overrides; results do not change)")
+    p.add_argument("--config", type=int, default=2, choices=(2, 3, 4, 5),
+                   help="workload (default 2: one transformer block at one denoising step)")
+    p.add_argument("--reps", type=int, default=20, help="timed repetitions (configs 3 and 4)")
     return p.parse_args()
 
 
@@ -83,7 +97,243 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               f"layout is described in DESIGN.md but not built.", file=sys.stderr)
         sys.exit(2)
+    {2: bench_config2, 3: bench_config3, 4: bench_config4, 5: bench_config5}[args.config](args)
 
+
+def _graph(fn):
+    """Capture fn() (library calls on torch's current stream) into a HIP graph,
+    after one warm run on the capture stream."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def _time_graph(g, reps):
+    """Median over reps of one replay, in ms (torch events on the replay stream)."""
+    import numpy as np
+    import torch
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(reps):
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
+
+
+def bench_config3(args):
+    """FFN weight-traffic sweep: both projections driven by synthetic spikes."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from workloads import synth
+
+    B.load()
+    ffn = synth.config3_weights()
+    d, F = ffn.W_up.shape
+    T = 4
+    n_copies = 4                       # 4 x (58.7 + 58.7) MB > 256 MB last-level cache
+    W_up = [torch.from_numpy(ffn.W_up).cuda() for _ in range(n_copies)]
+    W_dn = [torch.from_numpy(ffn.W_dn).cuda() for _ in range(n_copies)]
+    th_up, th_dn = int(ffn.theta_up), int(ffn.theta_dn)
+    points = []
+    for iB in range(len(synth.CFG3_BLOCKS)):
+        for iR in range(len(synth.CFG3_DENSITIES)):
+            pt = synth.config3_point(iB, iR)
+            Bk = pt.B
+            xu = B.to_dev_bits(synth.pack_bits(pt.X_up))
+            xd = B.to_dev_bits(synth.pack_bits(pt.X_dn))
+            su = torch.empty((T, Bk, (F + 63) // 64), dtype=torch.int64, device="cuda")
+            sd = torch.empty((T, Bk, (d + 63) // 64), dtype=torch.int64, device="cuda")
+            st = torch.zeros((2, 4), dtype=torch.int64, device="cuda")
+            ws = B.workspace(max(B.nmdlm_qbsm_workspace_size(T, Bk, d, F),
+                                 B.nmdlm_qbsm_workspace_size(T, Bk, F, d)))
+
+            def up(c):
+                B.nmdlm_qbsm(xu, T, Bk, d, W_up[c], F, F, theta=th_up, s_out=su, stats=st[0],
+                             flags=args.flags, ws=ws)
+
+            def dn(c):
+                B.nmdlm_qbsm(xd, T, Bk, F, W_dn[c], d, d, theta=th_dn, s_out=sd, stats=st[1],
+                             flags=args.flags, ws=ws)
+
+            g_up = _graph(lambda: [up(c) for c in range(n_copies)])
+            g_dn = _graph(lambda: [dn(c) for c in range(n_copies)])
+            t_up = _time_graph(g_up, args.reps) / n_copies
+            t_dn = _time_graph(g_dn, args.reps) / n_copies
+            k = st.cpu().numpy()
+            rec = {"B": Bk, "density": pt.density}
+            for nm, row, t in (("up", k[0], t_up), ("dn", k[1], t_dn)):
+                touched = int(row[1] * row[2])
+                rec[nm] = {"us": t * 1e3, "k_active": int(row[1]), "k_total": int(row[0]),
+                           "skip": 1.0 - row[1] / row[0], "touched_bytes": touched,
+                           "GBps": touched / (t * 1e-3) / 1e9}
+            rec["tokens_per_s"] = Bk / ((t_up + t_dn) * 1e-3)
+            points.append(rec)
+            del g_up, g_dn
+    head = [p for p in points if p["B"] == 64 and p["density"] == 0.30][0]
+    best = max((p[m]["GBps"], p, m) for p in points for m in ("up", "dn"))
+    out = {
+        "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
+        "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.reps,
+        "warmup": 1, "ms_per_step": (head["up"]["us"] + head["dn"]["us"]) / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "FFN weight-traffic sweep d=4096->14336->4096, T=4, "
+                               "Beta(0.5,8) per-neuron rates; value at B=64, density 0.30",
+                   "weight_copies_rotated": n_copies},
+        "weight_skip_fraction": 1.0 - (head["up"]["touched_bytes"] + head["dn"]["touched_bytes"])
+        / (head["up"]["k_total"] * F + head["dn"]["k_total"] * d),
+        "roofline": {"kernel": "k_qbsm (int8 MFMA spike product with fused IF epilogue)",
+                     "bound": "hbm", "achieved": best[0], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": best[0] / HBM_PEAK_GBPS, "traffic": None,
+                     "at": f"B={best[1]['B']} density={best[1]['density']} {best[2]}"},
+        "sweep": points,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def _mdlm_step_io(B, torch, m, C, M, k, flags, ev=None):
+    tok = torch.zeros(M, dtype=torch.int32, device="cuda")
+    msk = torch.ones(M, dtype=torch.uint8, device="cuda")
+    bufs = dict(
+        tok=tok, msk=msk, tok0=tok.clone(), msk0=msk.clone(),
+        logits=torch.empty((M, m.V), dtype=torch.float32, device="cuda"),
+        pred=torch.empty(M, dtype=torch.int32, device="cuda"),
+        conf=torch.empty(M, dtype=torch.float64, device="cuda"),
+        chosen=torch.empty(k, dtype=torch.int32, device="cuda"),
+        stats=torch.zeros((4 * m.n_layers + 1, 4), dtype=torch.int64, device="cuda"))
+    io = B.step_io(M, C, pos0=C, flags=flags, tokens=tok, masked=msk, k_unmask=k,
+                   logits=bufs["logits"], pred=bufs["pred"], conf=bufs["conf"],
+                   unmasked_pos=bufs["chosen"], stats=bufs["stats"],
+                   prof_events=ev)
+    return io, bufs
+
+
+def bench_config4(args):
+    """12-layer MDLM, one block step with head, confidence and unmasking."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from workloads import synth
+
+    B.load()
+    case = synth.config4()
+    m = case.model
+    C, M, k = case.C, case.B, case.k_unmask
+    dm = B.DeviceModel.from_mdlm(m, C + M)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, 0)))
+    ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, tokens=ctx,
+                                     masked=torch.zeros(C, dtype=torch.uint8, device="cuda")), ws)
+    io, b = _mdlm_step_io(B, torch, m, C, M, k, args.flags)
+
+    def step():
+        # every timed step starts from the fully masked block
+        b["tok"].copy_(b["tok0"])
+        b["msk"].copy_(b["msk0"])
+        B.nmdlm_block_step(dm, io, ws)
+
+    g = _graph(step)
+    t = _time_graph(g, args.reps)
+    st = b["stats"].cpu().numpy()
+    touched = int((st[:, 1] * st[:, 2]).sum())
+    dense = int((st[:, 0] * st[:, 2]).sum())
+    # products timed per launch
+    n_prod = 4 * m.n_layers + 1
+    ev = B.HipEvents(2 * n_prod)
+    pio, pb = _mdlm_step_io(B, torch, m, C, M, k, args.flags, ev=ev.arr)
+    B.nmdlm_block_step(dm, pio, ws)
+    torch.cuda.synchronize()
+    dur = [ev.elapsed_ms(2 * p, 2 * p + 1) for p in range(n_prod)]
+    pst = pb["stats"].cpu().numpy()
+    nbytes = [product_bytes(int(r[0]), int(r[1]), int(r[2]), m.T, M) for r in pst]
+    ev.close()
+    achieved = sum(nbytes) / (sum(dur) * 1e-3) / 1e9
+    out = {
+        "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
+        "value": M / (t * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.reps, "warmup": 2,
+        "ms_per_step": t, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int8", "data": "synthetic",
+        "config": {"workload": "12-layer spiking MDLM, one block step: d=2048, 16 heads x 128, "
+                               "FFN 8192, vocab 32000, T=4, 32 masked tokens over 1024 context "
+                               "tokens, head + confidence + top-8 unmasking"},
+        "unmasked_tokens_per_s": k / (t * 1e-3),
+        "weight_skip_fraction": 1.0 - touched / dense,
+        "touched_weight_bytes_per_step": touched,
+        "touched_weight_GBps": touched / (t * 1e-3) / 1e9,
+        "roofline": {"kernel": "k_qbsm (int8 MFMA spike product with fused epilogue)",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "avg_launch_ms": float(np.mean(dur)), "launches_timed": len(dur)},
+        "per_layer_k_active": st[:-1, 1].reshape(m.n_layers, 4).tolist(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_config5(args):
+    """24-layer MDLM block-diffusion generation (prefill timed apart)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from paper_2607_24841_amd.generate import Generator
+    from workloads import synth
+
+    B.load()
+    case = synth.config5()
+    m = case.model
+    P = len(case.prompt)
+    dm = B.DeviceModel.from_mdlm(m, P + case.n_blocks * case.B)
+    gen = Generator(dm, P, case.B)
+    ids = torch.from_numpy(np.asarray(case.prompt, dtype=np.int32)).cuda()
+    # warm run (fills the caches, loads code), then the timed one
+    gen.run(ids, case.n_blocks, case.steps, case.k_unmask)
+    torch.cuda.synchronize()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    C = gen.prefill(ids)
+    e[1].record()
+    for _ in range(case.n_blocks):
+        gen.run_block(C, case.steps, case.k_unmask)
+        C += case.B
+    e[2].record()
+    torch.cuda.synchronize()
+    t_pre, t_gen = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])
+    n_tok = case.n_blocks * case.B
+    n_steps = case.n_blocks * case.steps
+    out = {
+        "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
+        "value": n_steps * case.B / (t_gen * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": n_steps, "warmup": n_steps, "ms_per_step": t_gen / n_steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "24-layer spiking MDLM generation: prompt 2048 ids, 8 blocks x 32 "
+                               "tokens, 8 denoising steps per block, 4 unmasked per step"},
+        "generated_tokens_per_s": n_tok / (t_gen * 1e-3),
+        "generated_tokens_per_s_with_prefill": n_tok / ((t_pre + t_gen) * 1e-3),
+        "prefill_ms": t_pre, "generation_ms": t_gen, "issue": "eager",
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_config2(args):
     import numpy as np
     import torch
 

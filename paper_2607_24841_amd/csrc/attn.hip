@@ -33,7 +33,11 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int h = blockIdx.x, qb = blockIdx.y, t = blockIdx.z;
+  // neighbouring heads share key lines: consecutive logical ids, head fastest
+  const int nwg = gridDim.x * gridDim.y * gridDim.z;
+  const int lid = xcd_order(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z), nwg);
+  const int h = lid % gridDim.x, qb = (lid / gridDim.x) % gridDim.y,
+            t = lid / (gridDim.x * gridDim.y);
   const int d = H * DH, dw = d / 64;
   const int capw = (int)(cap / 64);
   const int J = C + M;
@@ -230,7 +234,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_if(const uint64_t* __restrict_
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int h = blockIdx.x, qb = blockIdx.y;
+  const int lid = xcd_order(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+  const int h = lid % gridDim.x, qb = lid / gridDim.x;
   const int d = H * DH, dw = d / 64;
   const int capw = (int)(cap / 64);
   const int J = C + M;

@@ -12,6 +12,30 @@ namespace nmdlm {
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+constexpr int kXcds = 8;  // accelerator dies; each has its own L2
+
+// Workgroups are dispatched round-robin over the XCDs (dispatch id d runs on
+// XCD d % 8).  xcd_order maps the dispatch id of a grid of n workgroups to a
+// logical id such that every XCD holds one contiguous range of logical ids;
+// kernels order their tiles so that tiles sharing input lines are
+// consecutive.  A bijection of [0, n) for every n.
+__device__ __forceinline__ int xcd_order(int d, int n) {
+  const int q = n / kXcds, r = n - q * kXcds;
+  const int xcd = d % kXcds, slot = d / kXcds;
+  return xcd < r ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
+}
+
+// Logical (x, y, z) of a workgroup of a 3-D grid, y fastest: the row blocks
+// of one column tile, then the neighbouring column tiles, share an XCD.
+__device__ __forceinline__ void tile_coords(int& x, int& y, int& z) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int n = gx * gy * gridDim.z;
+  const int d = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int l = xcd_order(d, n);
+  y = l % gy;
+  x = (l / gy) % gx;
+  z = l / (gy * gx);
+}
 constexpr int kMaxSeg = 3;
 constexpr int kChunkSteps = 16;   // k-steps (of 64 active rows) staged per LDS chunk
 constexpr int kTileLd = 68;       // LDS row stride (ints) of the 64-column output tile

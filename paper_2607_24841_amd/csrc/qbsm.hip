@@ -443,7 +443,8 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  int x, y, z;
+  tile_coords(x, y, z);
   const int Kw = (a.K + 63) >> 6;
   const int lds_row = 2 * Kw + 1;
   unsigned long long* sLU = sDyn;
@@ -600,7 +601,8 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_fused(QbsmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  int x, y, z;
+  tile_coords(x, y, z);
   const int R = a.T * a.M;
   const int Kw = (a.K + 63) >> 6;
   const int lds_row = 2 * Kw + 1;
@@ -770,7 +772,8 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_list(QbsmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int x = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  int x, y, z;
+  tile_coords(x, y, z);
   const int R = a.T * a.M;
 
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
