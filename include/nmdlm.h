@@ -54,9 +54,10 @@ typedef enum nmdlm_status {
 /* bits 16..19: force rows per tile group (0 = automatic; 1,2,4,8 = 16..128
  * rows).  Results do not depend on it. */
 #define NMDLM_ROWTILE_SHIFT 16u
-/* bits 20..21: product kernel (0 = automatic; 1 = separate pass building the
+/* bits 20..22: product kernel (0 = automatic; 1 = separate pass building the
  * active-row list; 2 = single kernel with an in-kernel list; 3 = single
- * kernel over 64-channel words, loading only active rows).  Results do not
+ * kernel over 64-channel words, loading only active rows into registers;
+ * 4 = as 3, gathering the active rows straight into LDS).  Results do not
  * depend on it. */
 #define NMDLM_PATH_SHIFT 20u
 #define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)

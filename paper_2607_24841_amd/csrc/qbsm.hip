@@ -277,8 +277,7 @@ __device__ __forceinline__ void reduce_tile(const v4i (&acc)[RT][4], int* sTile,
     for (int v = 0; v < 4; ++v)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int val = acc[q][v][e];
-        if (val) atomicAdd(&sTile[(q * 16 + g * 4 + e) * kTileLd + v * 16 + c], val);
+        atomicAdd(&sTile[(q * 16 + g * 4 + e) * kTileLd + v * 16 + c], acc[q][v][e]);
       }
 }
 
@@ -437,6 +436,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   __shared__ int sRed[NW];
   __shared__ EpiStage ep;
   __shared__ int sLast;
+  __shared__ int sFirst;  // first active row of the tile (target of the loads of inactive rows)
   // dynamic: local union [Kw] (u64), then the tile's spike rows as dwords
   // with row stride 2*Kw+1 (odd: the 16 rows a wave reads fall in different banks)
   extern __shared__ unsigned long long sDyn[];
@@ -451,6 +451,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + Kw);
 
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  if (tid == 0) sFirst = 0x7fffffff;
   stage_epilogue<NT>(a, ep, tid, x, y);
   for (int i = tid; i < ROWS * Kw; i += NT) {
     const int lr = i / Kw, w = i - lr * Kw;
@@ -469,7 +470,9 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
         u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
              ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
     }
-    sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
+    u = (w == Kw - 1) ? (u & last_mask) : u;
+    sLU[w] = u;
+    if (u) atomicMin(&sFirst, w * 64 + (int)__builtin_ctzll(u));
   }
   __syncthreads();
 
@@ -485,47 +488,50 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   for (int q = 0; q < RT; ++q)
 #pragma unroll
     for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
-  uint32_t xw[kGroup][16];
+  // Weight loads are unconditional: a lane whose row is not active in this
+  // tile (or a word past the range) loads the tile's first active row, whose
+  // line is read anyway.  Every word then issues the same 16 loads, so the
+  // next word's loads can be in flight while the current one is multiplied.
+  const int first = sFirst;
+  const uint32_t first_off = (uint32_t)first * ldw + colb;
+  const int stride = NW;
+  auto load_word = [&](int w, uint32_t (&xg)[16]) {
+    const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
+    const uint32_t m16 = (uint32_t)(u >> (16 * g)) & 0xFFFFu;
+    const uint32_t wbase = (uint32_t)w * 64u * ldw + lane_base;
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i)
-#pragma unroll
-    for (int s2 = 0; s2 < 16; ++s2) xw[i][s2] = 0u;
-
-  for (int jb = w0 + wave * kGroup; jb < w1; jb += NW * kGroup) {
-    unsigned long long uw[kGroup];
-#pragma unroll
-    for (int i = 0; i < kGroup; ++i) uw[i] = (jb + i < w1) ? sLU[jb + i] : 0ull;
-    // loads of the group's active rows
-#pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      if (uw[i] == 0ull) continue;  // wave-uniform
-      const uint32_t m16 = (uint32_t)(uw[i] >> (16 * g)) & 0xFFFFu;
-      const uint32_t wbase = (uint32_t)(jb + i) * 64u * ldw;
-      if (m16 == 0xFFFFu) {
-#pragma unroll
-        for (int s2 = 0; s2 < 16; ++s2)
-          xw[i][s2] = *reinterpret_cast<const uint32_t*>(Wb + (lane_base + (wbase + (uint32_t)s2 * ldw)));
-      } else {
-#pragma unroll
-        for (int s2 = 0; s2 < 16; ++s2)
-          if ((m16 >> s2) & 1u)
-            xw[i][s2] = *reinterpret_cast<const uint32_t*>(Wb + (lane_base + (wbase + (uint32_t)s2 * ldw)));
-      }
+    for (int s2 = 0; s2 < 16; ++s2) {
+      const uint32_t off = ((m16 >> s2) & 1u) ? wbase + (uint32_t)s2 * ldw : first_off;
+      xg[s2] = *reinterpret_cast<const uint32_t*>(Wb + off);
     }
+  };
+  auto mul_word = [&](int w, const uint32_t (&xg)[16]) {
+    const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
+    if (u == 0ull) return;  // wave-uniform
+    v4i b[4];
+    b_operands(xg, b);
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      if (uw[i] == 0ull) continue;  // wave-uniform
-      const int w = jb + i;
-      v4i b[4];
-      b_operands(xw[i], b);
+    for (int q = 0; q < RT; ++q) {
+      const uint32_t b16 = (sS[(q * 16 + c) * lds_row + 2 * w + (g >> 1)] >> (16 * (g & 1))) & 0xFFFFu;
+      const v4i af = a_operand(b16);
 #pragma unroll
-      for (int q = 0; q < RT; ++q) {
-        const uint32_t b16 = (sS[(q * 16 + c) * lds_row + 2 * w + (g >> 1)] >> (16 * (g & 1))) & 0xFFFFu;
-        const v4i af = a_operand(b16);
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
-      }
+      for (int v = 0; v < 4; ++v)
+        acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
+    }
+  };
+  int jw = w0 + wave;
+  if (first != 0x7fffffff && jw < w1) {  // wave-uniform
+    uint32_t xa[16], xb[16];
+    load_word(jw, xa);
+    while (true) {
+      load_word(jw + stride, xb);
+      mul_word(jw, xa);
+      jw += stride;
+      if (jw >= w1) break;
+      load_word(jw + stride, xa);
+      mul_word(jw, xb);
+      jw += stride;
+      if (jw >= w1) break;
     }
   }
 
@@ -537,6 +543,187 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
 
   // statistics of the whole block (the block union), by one workgroup: each
   // thread ORs a slice of the sources of one word, then one LDS OR per thread
+  if (a.stats && x == 0 && y == 0 && z == 0) {
+    __syncthreads();
+    for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
+    __syncthreads();
+    const int nsrc = a.dense ? 0 : (a.upart ? a.nparts : a.T * a.M);
+    const int slices = NT >= Kw ? NT / Kw : 1;
+    const int s0 = NT >= Kw ? tid / Kw : 0;
+    if (s0 < slices) {
+      for (int w = NT >= Kw ? tid % Kw : tid; w < Kw; w += (NT >= Kw ? Kw : NT)) {
+        unsigned long long u = 0ull;
+        if (a.upart) {
+          for (int q = s0; q < nsrc; q += slices) u |= a.upart[(size_t)q * Kw + w];
+        } else {
+          for (int r = s0; r < nsrc; r += slices) u |= a.S[(size_t)r * Kw + w];
+        }
+        if (u) atomicOr(&sLU[w], u);
+        if (NT >= Kw) break;
+      }
+    }
+    __syncthreads();
+    int cnt = 0;
+    for (int w = tid; w < Kw; w += NT) {
+      const unsigned long long u = a.dense ? ~0ull : sLU[w];
+      cnt += __popcll((w == Kw - 1) ? (u & last_mask) : u);
+    }
+    for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+    if (lane == 0) sRed[wave] = cnt;
+    __syncthreads();
+    if (tid == 0) {
+      int total = 0;
+      for (int i = 0; i < NW; ++i) total += sRed[i];
+      a.stats->k_total = a.K;
+      a.stats->k_active = total;
+      a.stats->n = a.N;
+      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
+    }
+  }
+}
+
+// ------------------------------------------------- LDS-streamed product
+// Same tiles and operands as k_qbsm_words, but the active weight rows are
+// gathered straight into LDS (global_load_lds_dwordx4: 16 bytes per lane,
+// no registers held while in flight).  A word (64 rows x 64 columns) is four
+// such loads, each covering 16 rows: lane l takes row 16q + l/4, bytes
+// 16(l%4)..16(l%4)+15 of the tile's columns.  Each wave keeps D words in
+// flight in a ring of D slots of its own; before using slot i it waits until
+// at most 4(D-1) loads are outstanding.  A lane whose row is inactive (or a
+// word past the range) loads the block's first active row instead, so every
+// word issues exactly four loads and the count stays exact.
+constexpr int kDmaChunk = 1088;         // bytes per 16-row chunk: 16 x 64 + 64 (bank offset)
+constexpr int kDmaSlot = 4 * kDmaChunk;  // bytes per word slot
+
+template <int D>
+__device__ __forceinline__ void dma_wait() {
+  if constexpr (D == 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (D == 2) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if constexpr (D == 3) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+}
+
+template <int RT, int NW, int D>
+__global__ __launch_bounds__(NW * 64) void k_qbsm_dma(QbsmArgs a) {
+  static_assert(D >= 1 && D <= 4, "ring depth");
+  constexpr int ROWS = RT * 16;
+  constexpr int NT = NW * 64;
+  constexpr int kNoRow = 0x7fffffff;
+  __shared__ int sTile[ROWS * kTileLd];
+  __shared__ unsigned long long sUn[NW];
+  __shared__ int sRed[NW];
+  __shared__ EpiStage ep;
+  __shared__ int sLast;
+  __shared__ int sFirst;
+  // dynamic: ring [NW][D][kDmaSlot] bytes, local union [Kw] (u64), the
+  // block's spike rows as dwords with row stride 2*Kw+1
+  extern __shared__ __attribute__((aligned(16))) unsigned char sRaw[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  int x, y, z;
+  tile_coords(x, y, z);
+  const int Kw = (a.K + 63) >> 6;
+  const int lds_row = 2 * Kw + 1;
+  unsigned char* ring = sRaw + (size_t)wave * D * kDmaSlot;
+  unsigned long long* sLU = reinterpret_cast<unsigned long long*>(sRaw + (size_t)NW * D * kDmaSlot);
+  uint32_t* sS = reinterpret_cast<uint32_t*>(sLU + Kw);
+
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  if (tid == 0) sFirst = kNoRow;
+  stage_epilogue<NT>(a, ep, tid, x, y);
+  for (int i = tid; i < ROWS * Kw; i += NT) {
+    const int lr = i / Kw, w = i - lr * Kw;
+    const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
+    const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
+    sS[lr * lds_row + 2 * w] = (uint32_t)v;
+    sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
+  }
+  __syncthreads();
+  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
+  for (int w = tid; w < Kw; w += NT) {
+    unsigned long long u = ~0ull;
+    if (!a.dense) {
+      u = 0ull;
+      for (int lr = 0; lr < ROWS; ++lr)
+        u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
+             ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+    }
+    u = (w == Kw - 1) ? (u & last_mask) : u;
+    sLU[w] = u;
+    if (u) atomicMin(&sFirst, w * 64 + (int)__builtin_ctzll(u));
+  }
+  __syncthreads();
+
+  const int w0 = (int)(((long long)Kw * z) / a.P);
+  const int w1 = (int)(((long long)Kw * (z + 1)) / a.P);
+  const int first = sFirst;
+
+  v4i acc[RT][4];
+#pragma unroll
+  for (int q = 0; q < RT; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[q][v] = v4i{0, 0, 0, 0};
+
+  const int jw0 = w0 + wave;
+  if (first != kNoRow && jw0 < w1) {  // wave-uniform
+    // this lane's part of a 16-row chunk: row rq, 16 bytes at column cbyte
+    const int rq = lane >> 2;
+    const int cbyte = x * 64 + (lane & 3) * 16;
+    const uint32_t ldw = (uint32_t)a.ldw;  // K * ldw < 2^31: 32-bit row offsets
+    // 1 when the lane's 16 bytes lie inside the row (the padded width); the
+    // masks and the row choice are arithmetic, so that the compiler keeps
+    // exactly one load per chunk instead of splitting lanes into branches
+    const uint32_t colmask = (uint32_t)((cbyte + 15 - (int)ldw) >> 31) & 1u;
+    const char* Wcol = reinterpret_cast<const char*>(a.W) + x * 64 + colmask * (cbyte - x * 64);
+    auto issue = [&](int w, int slot) {
+      const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
+      unsigned char* dst = ring + slot * kDmaSlot;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t on = (uint32_t)(u >> (16 * q + rq)) & colmask;
+        const uint32_t row = (uint32_t)first + on * ((uint32_t)(w * 64 + 16 * q + rq) - (uint32_t)first);
+        __builtin_amdgcn_global_load_lds(Wcol + row * ldw, dst + q * kDmaChunk, 16, 0, 0);
+      }
+      asm volatile("" ::: "memory");
+    };
+    const int nw = (w1 - jw0 + NW - 1) / NW;
+#pragma unroll
+    for (int i = 0; i < D; ++i) issue(jw0 + i * NW, i);
+    for (int i = 0; i < nw; ++i) {
+      const int w = jw0 + i * NW;
+      const int slot = i % D;
+      dma_wait<D>();
+      const unsigned long long u = sLU[w];
+      if (u) {  // wave-uniform
+        const unsigned char* src = ring + slot * kDmaSlot + g * kDmaChunk + 4 * c;
+        uint32_t xg[16];
+#pragma unroll
+        for (int s2 = 0; s2 < 16; ++s2) xg[s2] = *reinterpret_cast<const uint32_t*>(src + s2 * 64);
+        v4i b[4];
+        b_operands(xg, b);
+#pragma unroll
+        for (int q = 0; q < RT; ++q) {
+          const uint32_t b16 =
+              (sS[(q * 16 + c) * lds_row + 2 * w + (g >> 1)] >> (16 * (g & 1))) & 0xFFFFu;
+          const v4i af = a_operand(b16);
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
+        }
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // slot reads done before it is refilled
+      issue(w + D * NW, slot);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no LDS write in flight past the loop
+  }
+
+  __syncthreads();
+  reduce_tile<RT>(acc, sTile, g, c);
+  __syncthreads();
+  const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
+  if (last) epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
+
   if (a.stats && x == 0 && y == 0 && z == 0) {
     __syncthreads();
     for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
@@ -903,6 +1090,23 @@ static void launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
   hipLaunchKernelGGL((k_qbsm_words<RT, NW>), grid, dim3(NW * 64), dyn, st, a);
 }
 
+template <int RT, int NW, int D>
+static nmdlm_status launch_dma(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
+  if (dyn > 65536 &&
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_dma<RT, NW, D>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+    return NMDLM_ERR_HIP;
+  hipLaunchKernelGGL((k_qbsm_dma<RT, NW, D>), grid, dim3(NW * 64), dyn, st, a);
+  return NMDLM_OK;
+}
+
+// Static LDS of k_qbsm_dma (mirrors its declarations) and its dynamic part.
+static size_t dma_lds(int RT, int NW, int D, int Kw) {
+  return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
+         (size_t)NW * D * kDmaSlot + (size_t)Kw * 8 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
+}
+constexpr size_t kDmaLdsMax = 163840;  // LDS per workgroup on the device
+
 template <int RT, int NW>
 static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0, st, a);
@@ -933,7 +1137,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
 
   // product path: 1 = prep pass + list kernel, 2 = single kernel with a
   // compacted list, 3 = word-granular single kernel, 0 = automatic
-  int path = (int)((c.flags >> NMDLM_PATH_SHIFT) & 0x3u);
+  int path = (int)((c.flags >> NMDLM_PATH_SHIFT) & 0x7u);
   const int rt_full = pick_rt(R);
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
   const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
@@ -957,6 +1161,8 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     if (words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
   }
   if (path == 3 && words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
+  if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
+  if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
   const int Mb = (16 * RT) / c.T;
   const int gy = (c.M + Mb - 1) / Mb;
@@ -977,11 +1183,19 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   const int ks_per_wg = (Kw + P - 1) / P;
   int NW = (ks_per_wg >= 8 * kGroup && RT <= 2) ? 16 : 4;
   size_t dyn = 0;
-  bool fused = false, words = false;
-  if (path == 3) {
+  bool fused = false, words = false, dma = false;
+  int D = 1;
+  if (path == 4) {
+    // LDS-streamed: 8 waves x 2 words in flight, or 4 waves x 4 words
+    dma = true;
+    NW = (ks_per_wg >= 16 && RT <= 4) ? 8 : 4;
+    D = NW == 8 ? 2 : 4;
+    if (dma_lds(RT, NW, D, Kw) > kDmaLdsMax) { NW = 4; D = 4; }
+    dyn = dma_lds(RT, NW, D, Kw) - ((size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64);
+  } else if (path == 3) {
     words = true;
     // 8 waves, not 16: a 1024-thread bound caps registers at 128 and spills
-    NW = (ks_per_wg >= 8 * kGroup && RT == 1) ? 16 : ((ks_per_wg >= 4 * kGroup && RT <= 2) ? 8 : 4);
+    NW = (ks_per_wg > 32 && RT == 1) ? 16 : ((ks_per_wg >= 4 * kGroup && RT <= 2) ? 8 : 4);
     if (words_lds(RT, NW, Kw) > kLdsBudget) NW = 4;
     dyn = (size_t)Kw * 8 + (size_t)16 * RT * (2 * Kw + 1) * 4;
   } else if (path == 2) {
@@ -1013,7 +1227,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   pa.counters = scr.counters;
   pa.n_counters = tiles;
   pa.sc = scr.sc;
-  if (!fused && !words) {
+  if (!fused && !words && !dma) {
     if (!dense && !pa.upart && (long long)R * Kw > kUnionDirect) {
       hipLaunchKernelGGL(k_union, dim3(Kw), dim3(256), 0, st, c.s_in, R, Kw, scr.U);
       pa.upart = scr.U;
@@ -1064,7 +1278,24 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
 
   const dim3 grid(gx, gy, P);
   if (c.ev_begin && hipEventRecord(c.ev_begin, st) != hipSuccess) return NMDLM_ERR_HIP;
-  if (words) {
+  if (dma) {
+    nmdlm_status rd = NMDLM_OK;
+    if (NW == 8) {
+      switch (RT) {
+        case 1: rd = launch_dma<1, 8, 2>(grid, a, dyn, st); break;
+        case 2: rd = launch_dma<2, 8, 2>(grid, a, dyn, st); break;
+        default: rd = launch_dma<4, 8, 2>(grid, a, dyn, st); break;
+      }
+    } else {
+      switch (RT) {
+        case 1: rd = launch_dma<1, 4, 4>(grid, a, dyn, st); break;
+        case 2: rd = launch_dma<2, 4, 4>(grid, a, dyn, st); break;
+        case 4: rd = launch_dma<4, 4, 4>(grid, a, dyn, st); break;
+        default: rd = launch_dma<8, 4, 4>(grid, a, dyn, st); break;
+      }
+    }
+    if (rd != NMDLM_OK) return rd;
+  } else if (words) {
     if (NW == 16) {
       launch_words<1, 16>(grid, a, dyn, st);
     } else if (NW == 8) {

@@ -202,7 +202,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.scale = nullptr;
   c.stats = stats;
   c.flags = flags & (NMDLM_FORCE_DENSE | (0xFFu << NMDLM_SPLIT_SHIFT) | (0xFu << NMDLM_ROWTILE_SHIFT) |
-                     (0x3u << NMDLM_PATH_SHIFT));
+                     (0x7u << NMDLM_PATH_SHIFT));
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
   c.u_in = nullptr;

@@ -109,8 +109,9 @@ def test_block_step_graph_replays_match_eager():
         assert torch.equal(y, eager), f"replay {r} differs from the eager step"
 
 
-@pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16), 1 << 20, 2 << 20, 3 << 20, 0x4],
-                         ids=["P1", "P3", "P2RT1", "nofuse", "fused", "words", "attn-fused"])
+@pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16), 1 << 20, 2 << 20, 3 << 20,
+                                   4 << 20, 0x4],
+                         ids=["P1", "P3", "P2RT1", "nofuse", "fused", "words", "dma", "attn-fused"])
 def test_config2_forced_paths(flags):
     need_gpu()
     _check_block(synth.config2(), flags=flags)

@@ -82,7 +82,7 @@ def _chosen_ok(got, want, conf, tol=1e-9):
     return False
 
 
-@pytest.mark.parametrize("flags", [0, 0x4], ids=["default", "attn-fused"])
+@pytest.mark.parametrize("flags", [0, 0x4, 4 << 20], ids=["default", "attn-fused", "dma"])
 def test_config4_block_step_matches_stored_oracle(flags):
     torch, B = need_gpu()
     ref = _load("cfg4_block_step.json")

@@ -56,6 +56,7 @@ def test_tiny_and_ragged_shapes(shape):
 NOFUSE = 1 << 20      # prep pass + list kernel
 FUSED = 2 << 20       # single kernel, in-kernel list
 WORDS = 3 << 20       # single kernel over 64-channel words
+DMA = 4 << 20         # as WORDS, active rows gathered into LDS
 
 _FORCED = {
     "dense": 0x1, "P1": 1 << 8, "P2": 2 << 8, "P7": 7 << 8, "RT1": 1 << 16, "RT2": 2 << 16,
@@ -67,6 +68,9 @@ _FORCED = {
     "words": WORDS, "words-dense": WORDS | 0x1, "words-P3": WORDS | (3 << 8),
     "words-RT1": WORDS | (1 << 16), "words-RT4": WORDS | (4 << 16), "words-RT8": WORDS | (8 << 16),
     "words-P2RT2": WORDS | (2 << 8) | (2 << 16),
+    "dma": DMA, "dma-dense": DMA | 0x1, "dma-P3": DMA | (3 << 8), "dma-RT1": DMA | (1 << 16),
+    "dma-RT2": DMA | (2 << 16), "dma-RT4": DMA | (4 << 16), "dma-RT8": DMA | (8 << 16),
+    "dma-P2RT2": DMA | (2 << 8) | (2 << 16),
 }
 
 
@@ -77,7 +81,8 @@ def test_forced_paths_equal(flags):
     _check(case, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, NOFUSE, FUSED, WORDS], ids=["auto", "nofuse", "fused", "words"])
+@pytest.mark.parametrize("flags", [0, NOFUSE, FUSED, WORDS, DMA],
+                         ids=["auto", "nofuse", "fused", "words", "dma"])
 def test_degenerate_inputs(flags):
     need_gpu()
     c = synth.make_qbsm_case(9, 4, 8, 256, 128, 0.1)
@@ -87,7 +92,7 @@ def test_degenerate_inputs(flags):
     _check(c, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS], ids=["auto", "nofuse", "words"])
+@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS, DMA], ids=["auto", "nofuse", "words", "dma"])
 def test_large_k_shapes(flags):
     need_gpu()
     # K beyond the in-kernel-list limit, and a long block (many row blocks)
