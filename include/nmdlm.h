@@ -65,6 +65,7 @@ typedef enum nmdlm_status {
 /* Supported envelope (NMDLM_ERR_UNSUPPORTED beyond it). */
 #define NMDLM_MAX_T 8
 #define NMDLM_MAX_K 65536
+#define NMDLM_MAX_HEAD_M 4096   /* block tokens of a step that runs the head */
 
 /*
  * Statistics of one spike product, written by the device (int64 so the

@@ -203,6 +203,7 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
     if (!weights_ok(md->w_head, md->d, md->V, md->V) || !md->head_scale)
       return NMDLM_ERR_INVALID_ARG;
     if (!io->tokens || !io->masked || io->k_unmask < 0) return NMDLM_ERR_INVALID_ARG;
+    if (io->M > NMDLM_MAX_HEAD_M) return NMDLM_ERR_UNSUPPORTED;
   }
   if (!ws || !aligned(ws, 256) || ws_bytes < block_step_ws_size(md, io->M, io->flags))
     return NMDLM_ERR_WORKSPACE;

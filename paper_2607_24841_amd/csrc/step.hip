@@ -34,66 +34,125 @@ __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ e
 
 // Per token: argmax of the logits (ties -> smallest id) and the largest
 // softmax probability 1 / sum_v exp(l_v - l_max) in fp64.
-__global__ __launch_bounds__(256) void k_conf(const float* __restrict__ logits, int V,
-                                              int32_t* __restrict__ pred,
-                                              double* __restrict__ conf) {
-  __shared__ float sBest[256];
-  __shared__ int sIdx[256];
-  __shared__ double sSum[256];
-  const int m = blockIdx.x, tid = threadIdx.x;
+// Confidence of one token (one workgroup): pred = argmax_v logit (ties ->
+// smallest v), conf = 1 / sum_v exp(logit_v - logit_pred) in float64.
+constexpr int kConfThreads = 1024;
+constexpr int kConfUnroll = 8;
+
+__device__ __forceinline__ bool conf_better(float a, int ia, float b, int ib) {
+  return a > b || (a == b && ia < ib);
+}
+
+__global__ __launch_bounds__(kConfThreads) void k_conf(const float* __restrict__ logits, int V,
+                                                       int32_t* __restrict__ pred,
+                                                       double* __restrict__ conf) {
+  constexpr int NW = kConfThreads / 64;
+  __shared__ float sBest[NW];
+  __shared__ int sIdx[NW];
+  __shared__ double sSum[NW];
+  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* row = logits + (size_t)m * V;
+  // pass 1: arg-max; each batch of loads is unconditional (clamped index)
   float best = -FLT_MAX;
   int bi = 0x7fffffff;
-  for (int v = tid; v < V; v += 256) {
-    const float x = row[v];
-    if (x > best || (x == best && v < bi)) {
-      best = x;
-      bi = v;
-    }
-  }
-  sBest[tid] = best;
-  sIdx[tid] = bi;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) {
-      const float ob = sBest[tid + s];
-      const int oi = sIdx[tid + s];
-      if (ob > sBest[tid] || (ob == sBest[tid] && oi < sIdx[tid])) {
-        sBest[tid] = ob;
-        sIdx[tid] = oi;
+  for (int v0 = tid; v0 < V; v0 += kConfThreads * kConfUnroll) {
+    float xs[kConfUnroll];
+#pragma unroll
+    for (int u = 0; u < kConfUnroll; ++u) xs[u] = row[min(v0 + u * kConfThreads, V - 1)];
+#pragma unroll
+    for (int u = 0; u < kConfUnroll; ++u) {
+      const int v = v0 + u * kConfThreads;
+      if (v < V && conf_better(xs[u], v, best, bi)) {
+        best = xs[u];
+        bi = v;
       }
     }
-    __syncthreads();
   }
-  const double mx = (double)sBest[0];
-  double acc = 0.0;
-  for (int v = tid; v < V; v += 256) acc += exp((double)row[v] - mx);
-  sSum[tid] = acc;
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o);
+    const int oi = __shfl_xor(bi, o);
+    if (conf_better(ob, oi, best, bi)) {
+      best = ob;
+      bi = oi;
+    }
+  }
+  if (lane == 0) {
+    sBest[wave] = best;
+    sIdx[wave] = bi;
+  }
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) sSum[tid] += sSum[tid + s];
-    __syncthreads();
+  best = sBest[0];
+  bi = sIdx[0];
+  for (int w = 1; w < NW; ++w)
+    if (conf_better(sBest[w], sIdx[w], best, bi)) {
+      best = sBest[w];
+      bi = sIdx[w];
+    }
+  // pass 2: sum of exp(logit - max) in float64
+  const double mx = (double)best;
+  double acc = 0.0;
+  for (int v0 = tid; v0 < V; v0 += kConfThreads * kConfUnroll) {
+    float xs[kConfUnroll];
+#pragma unroll
+    for (int u = 0; u < kConfUnroll; ++u) xs[u] = row[min(v0 + u * kConfThreads, V - 1)];
+#pragma unroll
+    for (int u = 0; u < kConfUnroll; ++u)
+      if (v0 + u * kConfThreads < V) acc += exp((double)xs[u] - mx);
   }
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) sSum[wave] = acc;
+  __syncthreads();
   if (tid == 0) {
-    pred[m] = sIdx[0];
-    conf[m] = 1.0 / sSum[0];
+    double sum = 0.0;
+    for (int w = 0; w < NW; ++w) sum += sSum[w];
+    pred[m] = bi;
+    conf[m] = 1.0 / sum;
   }
 }
 
-// Reveal the k most confident masked positions (ties -> lower position).
-__global__ void k_unmask(int32_t* __restrict__ tokens, uint8_t* __restrict__ masked,
-                         const int32_t* __restrict__ pred, const double* __restrict__ conf, int M,
-                         int k, int32_t* __restrict__ chosen) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+// Top-k unmasking by one wave: among the positions still masked, take the
+// highest confidence (ties -> smaller position) k times.  Lane l owns the
+// positions l + 64 j (j < 64, so M <= kUnmaskMaxM) and keeps their masked
+// flags in a register mask.
+constexpr int kUnmaskMaxM = 64 * 64;
+static_assert(kUnmaskMaxM >= NMDLM_MAX_HEAD_M, "unmask register mask covers every head step");
+
+__global__ __launch_bounds__(64) void k_unmask(int32_t* __restrict__ tokens,
+                                               uint8_t* __restrict__ masked,
+                                               const int32_t* __restrict__ pred,
+                                               const double* __restrict__ conf, int M, int k,
+                                               int32_t* __restrict__ chosen) {
+  const int lane = threadIdx.x;
+  uint64_t mine = 0ull;
+  for (int jj = 0, m = lane; m < M; ++jj, m += 64)
+    if (masked[m]) mine |= 1ull << jj;
   for (int r = 0; r < k; ++r) {
-    int best = -1;
-    for (int m = 0; m < M; ++m)
-      if (masked[m] && (best < 0 || conf[m] > conf[best])) best = m;
-    if (best >= 0) {
-      tokens[best] = pred[best];
-      masked[best] = 0;
+    double bc = 0.0;
+    int bm = -1;
+    for (uint64_t rest = mine; rest; rest &= rest - 1) {
+      const int m = lane + 64 * (int)__builtin_ctzll(rest);
+      const double cm = conf[m];
+      if (bm < 0 || cm > bc) {  // ascending m: ties keep the smaller position
+        bc = cm;
+        bm = m;
+      }
     }
-    if (chosen) chosen[r] = best;
+    for (int o = 32; o > 0; o >>= 1) {
+      const double oc = __shfl_xor(bc, o);
+      const int om = __shfl_xor(bm, o);
+      if (om >= 0 && (bm < 0 || oc > bc || (oc == bc && om < bm))) {
+        bc = oc;
+        bm = om;
+      }
+    }
+    if (bm >= 0 && (bm & 63) == lane) mine &= ~(1ull << (bm >> 6));
+    if (lane == 0) {
+      if (bm >= 0) {
+        tokens[bm] = pred[bm];
+        masked[bm] = 0;
+      }
+      if (chosen) chosen[r] = bm;
+    }
   }
 }
 
@@ -336,7 +395,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
   hc.u_nparts = uX_parts;
   attach_events(hc, io, 4 * md->n_layers);
   if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
-  hipLaunchKernelGGL(k_conf, dim3(M), dim3(256), 0, st, logits, md->V, pred, conf);
+  hipLaunchKernelGGL(k_conf, dim3(M), dim3(kConfThreads), 0, st, logits, md->V, pred, conf);
   if ((rc = hip_status()) != NMDLM_OK) return rc;
   hipLaunchKernelGGL(k_unmask, dim3(1), dim3(64), 0, st, io->tokens, io->masked, pred, conf, M,
                      io->k_unmask, io->unmasked_pos);

@@ -118,3 +118,8 @@ def test_block_step_argument_errors(lib):
     assert call(m, head_io) == 1
     no_in = B.step_io(16, 512, flags=B.NMDLM_NO_HEAD)               # no input and no tables
     assert call(m, no_in) == 1
+    # a step with the head takes at most NMDLM_MAX_HEAD_M block tokens
+    mh = B.Model(1, 1024, 16, 4096, 32000, 4, 8192, 0, layers, None, None, FAKE, FAKE)
+    big = B.step_io(4097, 0, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
+    nb = lib.nmdlm_block_step_workspace_size(C.byref(mh), 4097, 0)
+    assert nb > 0 and call(mh, big, nb=nb) == B.NMDLM_ERR_UNSUPPORTED
