@@ -249,6 +249,7 @@ struct EpiStage {
   int theta[64];
   unsigned long long resid[kMaxEpiTokens];  // [t * Mb + token]
   signed char lut[256];                     // activation table (EPI_QNL_IF)
+  uint32_t vbits[NMDLM_MAX_T * 64];         // channel-major output: token bits per (t, column)
 };
 
 template <int NT>
@@ -266,6 +267,7 @@ __device__ __forceinline__ void stage_epilogue(const QbsmArgs& a, EpiStage& ep, 
   }
   if (a.mode == EPI_QNL_IF)
     for (int i = tid; i < 256; i += NT) ep.lut[i] = (signed char)a.lut[i];
+  for (int i = tid; i < NMDLM_MAX_T * 64; i += NT) ep.vbits[i] = 0u;
 }
 
 // Sum the waves' accumulators into the LDS tile (physical column order).
@@ -314,7 +316,7 @@ __device__ bool split_fixup(const QbsmArgs& a, int* sTile, int* sLast, int tid, 
 // Epilogue: currents, IF (optionally after the activation table), or head
 // logits, from the reduced tile; emits the partial union of the output.
 template <int NW>
-__device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep,
+__device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
                          unsigned long long* sUn, int tid, int lane, int wave, int x, int y) {
   const int n0 = x * 64;
   const int col = lane, n = n0 + col;
@@ -338,11 +340,19 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep
   const int theta = a.theta_vec ? ep.theta[col] : seg.theta;
   const bool spikes = a.mode != EPI_CUR;
   const bool tr = spikes && seg.transposed;
+  // channel-major output in whole bytes: the row block's tokens fill whole
+  // bytes of the position words, so this workgroup owns them (plain byte
+  // stores); otherwise bits are cleared and set with atomics
+  const bool tr_bytes = tr && (a.Mb & 7) == 0 && a.Mb <= 32 && (seg.pos0 & 7) == 0;
   const bool staged = a.resid && a.T * a.Mb <= kMaxEpiTokens;
   const int wbase = tr ? ((seg.pos0 + y * a.Mb) >> 6) : 0;
   uint64_t tb0[NMDLM_MAX_T], tb1[NMDLM_MAX_T];
+  uint32_t vb[NMDLM_MAX_T];
 #pragma unroll
-  for (int t = 0; t < NMDLM_MAX_T; ++t) tb0[t] = tb1[t] = 0ull;
+  for (int t = 0; t < NMDLM_MAX_T; ++t) {
+    tb0[t] = tb1[t] = 0ull;
+    vb[t] = 0u;
+  }
   uint64_t tm0 = 0ull, tm1 = 0ull;
   uint64_t uor = 0ull;  // union of this wave's output words (wave-uniform)
 
@@ -381,14 +391,32 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, const EpiStage& ep
             uor |= word;
             if (lane == 0) seg.ptr[t * seg.ld_t + (int64_t)m * seg.ld_m + wseg] = word;
           } else if (s) {
-            if (rel == 0) tb0[t] |= pbit;
+            if (tr_bytes) vb[t] |= 1u << ml;
+            else if (rel == 0) tb0[t] |= pbit;
             else tb1[t] |= pbit;
           }
         }
       }
     }
   }
-  if (tr && nv) {
+  if (tr_bytes) {
+    // the waves' token bits meet in LDS; each column then stores the bytes
+    // that hold at least one token of the block
+#pragma unroll
+    for (int t = 0; t < NMDLM_MAX_T; ++t)
+      if (t < a.T && vb[t]) atomicOr(&ep.vbits[t * 64 + col], vb[t]);
+    __syncthreads();
+    if (wave == 0 && nv) {
+      const int ch = n - segi * a.seg_w;
+      const int p0 = seg.pos0 + y * a.Mb;               // multiple of 8
+      const int nb = (min(a.Mb, a.M - y * a.Mb) + 7) >> 3;  // bytes with a token of the block
+      for (int t = 0; t < a.T; ++t) {
+        uint8_t* rowb = reinterpret_cast<uint8_t*>(seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m) + (p0 >> 3);
+        const uint32_t bits = ep.vbits[t * 64 + col];
+        for (int b = 0; b < nb; ++b) rowb[b] = (uint8_t)(bits >> (8 * b));
+      }
+    }
+  } else if (tr && nv) {
     // channel-major cache: clear this wave's token bits, then set the spikes
     const int ch = n - segi * a.seg_w;
 #pragma unroll
