@@ -57,6 +57,33 @@ def parse():
     return p.parse_args()
 
 
+# HBM bytes per launch of the product kernel in the one-block step (mean of
+# its four products), from two rocprofv3 --pmc passes (FETCH_SIZE, then
+# WRITE_SIZE) over `bench.py --eager`, each scaled by what the counter reads
+# for a 64 MiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0); the summary
+# with the commands is profiles/k_qbsm_words_one_block_step_traffic.md.  Valid
+# only for the product-kernel sources with this digest: any change to them
+# reports null until the counters are taken again.
+TRAFFIC = {"sources_sha256": None, "bytes_per_launch": None}
+PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
+
+
+def product_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for rel in PRODUCT_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def product_traffic():
+    if TRAFFIC["sources_sha256"] and TRAFFIC["sources_sha256"] == product_sources_sha256():
+        return TRAFFIC["bytes_per_launch"]
+    return None
+
+
 def product_bytes(k_total, k_active, n, T, M):
     """Algorithmic bytes of one product launch: active weight rows, packed
     input spikes, packed output spikes."""
@@ -342,22 +369,23 @@ def bench_config2(args):
 
     B.load()
     dev = "cuda"
+    import ctypes as C
     case = synth.config2(seed=args.seed)
     L = case.layer
-    T, C, M, d, H, F = case.T, case.C, case.M, L.d, L.H, L.F
+    T, C_ctx, M, d, H, F = case.T, case.C, case.M, L.d, L.H, L.F
 
     # --- device state (untimed): layer copies, prefilled caches ----------------
-    dms = [B.DeviceModel([L], T, C + M, d, H, F) for _ in range(args.copies)]
-    nb = max(B.nmdlm_block_step_workspace_size(dms[0], C, B.NMDLM_NO_HEAD),
+    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F) for _ in range(args.copies)]
+    nb = max(B.nmdlm_block_step_workspace_size(dms[0], C_ctx, B.NMDLM_NO_HEAD),
              B.nmdlm_block_step_workspace_size(dms[0], M, B.NMDLM_NO_HEAD))
     ws = B.workspace(nb)
     xc = B.to_dev_bits(synth.pack_bits(case.X_ctx))
     for dm in dms:
-        B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, x_in=xc), ws)
+        B.nmdlm_block_step(dm, B.step_io(C_ctx, 0, flags=B.NMDLM_NO_HEAD, x_in=xc), ws)
     xb = B.to_dev_bits(synth.pack_bits(case.X_blk))
     y = torch.zeros((T, M, d // 64), dtype=torch.int64, device=dev)
     stats = torch.zeros((4, 4), dtype=torch.int64, device=dev)
-    io = B.step_io(M, C, flags=B.NMDLM_NO_HEAD | args.flags, x_in=xb, y_out=y, stats=stats)
+    io = B.step_io(M, C_ctx, flags=B.NMDLM_NO_HEAD | args.flags, x_in=xb, y_out=y, stats=stats)
     torch.cuda.synchronize()
 
     def eager_steps(i0, n):
@@ -408,21 +436,36 @@ def bench_config2(args):
     w_dense = int((k_total * n_col).sum())
     skip = 1.0 - w_touched / w_dense
 
-    # --- product kernel timed per launch (events recorded around it) ------------
-    ev = B.HipEvents(2 * 4)
-    pio = B.step_io(M, C, flags=B.NMDLM_NO_HEAD | args.flags, x_in=xb, y_out=y, stats=stats,
-                    prof_events=ev.arr)
+    # --- product kernel timed per launch: the library stamps a HIP event
+    #     pair with the start and end of every product kernel (from its
+    #     dispatch).  Events cannot be graph nodes here, so the same steps are
+    #     issued directly behind a spin kernel: the queue fills while it spins
+    #     and the kernels then run back to back, as in the timed region
+    n_ev = 2 * 4
+    ev = B.HipEvents(n_ev * args.copies)
+    ptr_size = C.sizeof(C.c_void_p)
+    sub = [(C.c_void_p * n_ev).from_address(C.addressof(ev.arr) + i * n_ev * ptr_size)
+           for i in range(args.copies)]
+    pios = [B.step_io(M, C_ctx, flags=B.NMDLM_NO_HEAD | args.flags, x_in=xb, y_out=y,
+                      stats=stats, prof_events=sub[i]) for i in range(args.copies)]
+    for i in range(args.copies):                 # warm the event path
+        B.nmdlm_block_step(dms[i], pios[i], ws)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(50_000_000)
+    for i in range(args.copies):
+        B.nmdlm_block_step(dms[i], pios[i], ws)
+    torch.cuda.synchronize()
+    timing_issue = "direct issue behind a spin kernel (queue full)"
     dur = []
     nbytes = []
     for i in range(args.copies):
-        B.nmdlm_block_step(dms[i % args.copies], pio, ws)
-        torch.cuda.synchronize()
         for p in range(4):
-            dur.append(ev.elapsed_ms(2 * p, 2 * p + 1))
+            dur.append(ev.elapsed_ms(i * n_ev + 2 * p, i * n_ev + 2 * p + 1))
             nbytes.append(product_bytes(int(k_total[p]), int(k_active[p]), int(n_col[p]), T, M))
     ev.close()
     avg_ms = float(np.mean(dur))
     achieved = sum(nbytes) / (sum(dur) * 1e-3) / 1e9
+    traffic = product_traffic()
 
     out = {
         "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
@@ -441,7 +484,7 @@ def bench_config2(args):
             "workload": "one spiking transformer block at a single denoising step: d=1024, "
                         "16 heads x 64, FFN 4096, T=4, block of 16 masked tokens over 512 "
                         "context tokens, input spike rate 0.10, int8 weights",
-            "block_tokens": M, "context_tokens": C, "timesteps": T,
+            "block_tokens": M, "context_tokens": C_ctx, "timesteps": T,
             "layer_copies_rotated": args.copies, "issue": "eager" if args.eager else "hip_graph",
         },
         "weight_skip_fraction": skip,
@@ -454,9 +497,10 @@ def bench_config2(args):
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": traffic,
             "avg_launch_ms": avg_ms,
             "launches_timed": len(dur),
+            "timing_issue": timing_issue,
         },
     }
     if not args.no_cpu_baseline:

@@ -247,9 +247,10 @@ typedef struct nmdlm_step_io {
   nmdlm_qbsm_stats* stats; /* device [4*n_layers + 1] or NULL: per product
                               (QKV, O, up, down per layer, then the head)  */
   void** prof_events;      /* HOST array of hipEvent_t or NULL: when given,
-                              events 2i and 2i+1 are recorded on the stream
-                              just before and after the main kernel of
-                              product i (same order as stats), for timing  */
+                              events 2i and 2i+1 take the start and end
+                              times of the main kernel of product i (same
+                              order as stats), stamped by its dispatch;
+                              NMDLM_ERR_UNSUPPORTED inside stream capture  */
   int n_prof_events;       /* length of prof_events                         */
 } nmdlm_step_io;
 

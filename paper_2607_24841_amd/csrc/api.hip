@@ -207,6 +207,12 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   }
   if (!ws || !aligned(ws, 256) || ws_bytes < block_step_ws_size(md, io->M, io->flags))
     return NMDLM_ERR_WORKSPACE;
+  if (io->prof_events && io->n_prof_events > 0) {
+    // timing events are plain records: not available inside stream capture
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(static_cast<hipStream_t>(stream), &cs) != hipSuccess) return NMDLM_ERR_HIP;
+    if (cs != hipStreamCaptureStatusNone) return NMDLM_ERR_UNSUPPORTED;
+  }
   return block_step_impl(md, io, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 

@@ -8,6 +8,8 @@
 // (currents, integrate-and-fire, table + IF, or head logits) that also emits
 // the partial union of its output spikes.  Blocks too large for LDS (long
 // prefills) take a prep pass (k_union, k_prep) and k_qbsm_list.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 
 namespace nmdlm {
@@ -1108,23 +1110,28 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->counters = cv.take<int32_t>(s->n_counters);
 }
 
+// Product launches: hipExtLaunchKernelGGL stamps the optional start/stop
+// events from the kernel's own dispatch (no marker packets around it).
 template <int RT, int NW>
-static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
-  hipLaunchKernelGGL((k_qbsm_fused<RT, NW>), grid, dim3(NW * 64), dyn, st, a);
+static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
+                         hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((k_qbsm_fused<RT, NW>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0, e1, 0, a);
 }
 
 template <int RT, int NW>
-static void launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
-  hipLaunchKernelGGL((k_qbsm_words<RT, NW>), grid, dim3(NW * 64), dyn, st, a);
+static void launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
+                         hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((k_qbsm_words<RT, NW>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0, e1, 0, a);
 }
 
 template <int RT, int NW, int D>
-static nmdlm_status launch_dma(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st) {
+static nmdlm_status launch_dma(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
+                               hipEvent_t e0, hipEvent_t e1) {
   if (dyn > 65536 &&
       hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_dma<RT, NW, D>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
     return NMDLM_ERR_HIP;
-  hipLaunchKernelGGL((k_qbsm_dma<RT, NW, D>), grid, dim3(NW * 64), dyn, st, a);
+  hipExtLaunchKernelGGL((k_qbsm_dma<RT, NW, D>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0, e1, 0, a);
   return NMDLM_OK;
 }
 
@@ -1136,8 +1143,9 @@ static size_t dma_lds(int RT, int NW, int D, int Kw) {
 constexpr size_t kDmaLdsMax = 163840;  // LDS per workgroup on the device
 
 template <int RT, int NW>
-static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0, st, a);
+static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st, hipEvent_t e0,
+                        hipEvent_t e1) {
+  hipExtLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0u, st, e0, e1, 0, a);
 }
 
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
@@ -1170,14 +1178,31 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
   const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
   if (!rt_forced) {
-    // rows per tile group: the largest that still gives >= 256 workgroups,
-    // else the smallest (most row blocks; they re-read weights from L2)
+    // rows per tile group: the largest that still gives >= 2 workgroups per
+    // compute unit, else the smallest (most row blocks; they re-read weights
+    // from L2)
     RT = 1;
     for (int r = rt_full; r >= 1; r >>= 1) {
       const int mb = (16 * r) / c.T;
-      if (mb >= 1 && (long long)gx * ((c.M + mb - 1) / mb) >= 256) {
+      if (mb >= 1 && (long long)gx * ((c.M + mb - 1) / mb) >= 512) {
         RT = r;
         break;
+      }
+    }
+    // a channel-major output segment is written in whole bytes when a row
+    // block's tokens fill them: take the fewest rows that do, if the grid
+    // keeps >= 256 workgroups
+    bool pos_ok = true;
+    for (int i = 0; i < c.nseg; ++i)
+      if (c.seg[i].transposed && (c.seg[i].pos0 & 7)) pos_ok = false;
+    if (has_tr && pos_ok) {
+      for (int r = RT; r <= 8; r <<= 1) {
+        const int mb = (16 * r) / c.T;
+        if (mb > 32) break;
+        if (mb % 8 == 0) {
+          if (r == RT || (long long)gx * ((c.M + mb - 1) / mb) >= 256) RT = r;
+          break;
+        }
       }
     }
   }
@@ -1305,58 +1330,58 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.stats = c.stats;
 
   const dim3 grid(gx, gy, P);
-  if (c.ev_begin && hipEventRecord(c.ev_begin, st) != hipSuccess) return NMDLM_ERR_HIP;
+  hipEvent_t e0 = c.ev_begin, e1 = c.ev_end;
   if (dma) {
     nmdlm_status rd = NMDLM_OK;
     if (NW == 8) {
       switch (RT) {
-        case 1: rd = launch_dma<1, 8, 2>(grid, a, dyn, st); break;
-        case 2: rd = launch_dma<2, 8, 2>(grid, a, dyn, st); break;
-        default: rd = launch_dma<4, 8, 2>(grid, a, dyn, st); break;
+        case 1: rd = launch_dma<1, 8, 2>(grid, a, dyn, st, e0, e1); break;
+        case 2: rd = launch_dma<2, 8, 2>(grid, a, dyn, st, e0, e1); break;
+        default: rd = launch_dma<4, 8, 2>(grid, a, dyn, st, e0, e1); break;
       }
     } else {
       switch (RT) {
-        case 1: rd = launch_dma<1, 4, 4>(grid, a, dyn, st); break;
-        case 2: rd = launch_dma<2, 4, 4>(grid, a, dyn, st); break;
-        case 4: rd = launch_dma<4, 4, 4>(grid, a, dyn, st); break;
-        default: rd = launch_dma<8, 4, 4>(grid, a, dyn, st); break;
+        case 1: rd = launch_dma<1, 4, 4>(grid, a, dyn, st, e0, e1); break;
+        case 2: rd = launch_dma<2, 4, 4>(grid, a, dyn, st, e0, e1); break;
+        case 4: rd = launch_dma<4, 4, 4>(grid, a, dyn, st, e0, e1); break;
+        default: rd = launch_dma<8, 4, 4>(grid, a, dyn, st, e0, e1); break;
       }
     }
     if (rd != NMDLM_OK) return rd;
   } else if (words) {
     if (NW == 16) {
-      launch_words<1, 16>(grid, a, dyn, st);
+      launch_words<1, 16>(grid, a, dyn, st, e0, e1);
     } else if (NW == 8) {
-      if (RT == 1) launch_words<1, 8>(grid, a, dyn, st);
-      else launch_words<2, 8>(grid, a, dyn, st);
+      if (RT == 1) launch_words<1, 8>(grid, a, dyn, st, e0, e1);
+      else launch_words<2, 8>(grid, a, dyn, st, e0, e1);
     } else {
       switch (RT) {
-        case 1: launch_words<1, 4>(grid, a, dyn, st); break;
-        case 2: launch_words<2, 4>(grid, a, dyn, st); break;
-        case 4: launch_words<4, 4>(grid, a, dyn, st); break;
-        default: launch_words<8, 4>(grid, a, dyn, st); break;
+        case 1: launch_words<1, 4>(grid, a, dyn, st, e0, e1); break;
+        case 2: launch_words<2, 4>(grid, a, dyn, st, e0, e1); break;
+        case 4: launch_words<4, 4>(grid, a, dyn, st, e0, e1); break;
+        default: launch_words<8, 4>(grid, a, dyn, st, e0, e1); break;
       }
     }
   } else if (fused) {
     if (NW == 16) {
-      launch_fused<1, 16>(grid, a, dyn, st);
+      launch_fused<1, 16>(grid, a, dyn, st, e0, e1);
     } else {
-      if (RT == 1) launch_fused<1, 4>(grid, a, dyn, st);
-      else launch_fused<2, 4>(grid, a, dyn, st);
+      if (RT == 1) launch_fused<1, 4>(grid, a, dyn, st, e0, e1);
+      else launch_fused<2, 4>(grid, a, dyn, st, e0, e1);
     }
   } else if (NW == 16) {
-    if (RT == 1) launch_list<1, 16>(grid, a, st);
-    else launch_list<2, 16>(grid, a, st);
+    if (RT == 1) launch_list<1, 16>(grid, a, st, e0, e1);
+    else launch_list<2, 16>(grid, a, st, e0, e1);
   } else {
     switch (RT) {
-      case 1: launch_list<1, 4>(grid, a, st); break;
-      case 2: launch_list<2, 4>(grid, a, st); break;
-      case 4: launch_list<4, 4>(grid, a, st); break;
-      default: launch_list<8, 4>(grid, a, st); break;
+      case 1: launch_list<1, 4>(grid, a, st, e0, e1); break;
+      case 2: launch_list<2, 4>(grid, a, st, e0, e1); break;
+      case 4: launch_list<4, 4>(grid, a, st, e0, e1); break;
+      default: launch_list<8, 4>(grid, a, st, e0, e1); break;
     }
   }
   const nmdlm_status rc = hip_status();
-  if (rc == NMDLM_OK && c.ev_end && hipEventRecord(c.ev_end, st) != hipSuccess) return NMDLM_ERR_HIP;
+
   return rc;
 }
 
