@@ -17,15 +17,15 @@ the touched-weight bandwidth of the whole step, the roofline of the product
 kernel (timed per launch with HIP events recorded by the library around the
 kernel) and the CPU oracle's rate on a bounded sample.
 
-Other workloads (--config):
-  3  FFN weight-traffic sweep, d=4096 -> 14336 -> 4096, T=4, B in {1,4,16,64},
+Other workloads (--workload):
+  ffn-sweep        FFN weight-traffic sweep, d=4096 -> 14336 -> 4096, T=4, B in {1,4,16,64},
      mean input density in {.02,.05,.10,.30}: skipped-row fraction, touched
      bytes and GB/s of the up and down products at every point (4 rotating
      weight copies, 470 MB, so that weights stream from HBM).
-  4  12-layer MDLM (d=2048, 16 heads of 128, FFN 8192, vocab 32000, T=4), one
+  mdlm12-step      12-layer MDLM (d=2048, 16 heads of 128, FFN 8192, vocab 32000, T=4), one
      block step of 32 masked tokens over 1024 context tokens with head,
      confidence and top-8 unmasking (640 MB of weights per step).
-  5  24-layer MDLM generation: prompt of 2048 ids, 8 blocks of 32 tokens,
+  mdlm24-generate  24-layer MDLM generation: prompt of 2048 ids, 8 blocks of 32 tokens,
      8 steps per block, 4 tokens unmasked per step.
 """
 from __future__ import annotations
@@ -51,9 +51,11 @@ def parse():
     p.add_argument("--seed", type=int, default=1002)
     p.add_argument("--flags", type=lambda x: int(x, 0), default=0,
                    help="extra block-step flags (path overrides; results do not change)")
-    p.add_argument("--config", type=int, default=2, choices=(2, 3, 4, 5),
-                   help="workload (default 2: one transformer block at one denoising step)")
-    p.add_argument("--reps", type=int, default=20, help="timed repetitions (configs 3 and 4)")
+    p.add_argument("--workload", default="block",
+                   choices=("block", "ffn-sweep", "mdlm12-step", "mdlm24-generate"),
+                   help="block: one transformer block at one denoising step (default)")
+    p.add_argument("--reps", type=int, default=20,
+                   help="timed repetitions (ffn-sweep, mdlm12-step)")
     return p.parse_args()
 
 
@@ -125,7 +127,8 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               f"layout is described in DESIGN.md but not built.", file=sys.stderr)
         sys.exit(2)
-    {2: bench_config2, 3: bench_config3, 4: bench_config4, 5: bench_config5}[args.config](args)
+    {"block": bench_block, "ffn-sweep": bench_ffn_sweep, "mdlm12-step": bench_mdlm12_step,
+     "mdlm24-generate": bench_mdlm24_generate}[args.workload](args)
 
 
 def _graph(fn):
@@ -162,7 +165,7 @@ def _time_graph(g, reps):
     return float(np.median(ts))
 
 
-def bench_config3(args):
+def bench_ffn_sweep(args):
     """FFN weight-traffic sweep: both projections driven by synthetic spikes."""
     import numpy as np
     import torch
@@ -171,7 +174,7 @@ def bench_config3(args):
     from workloads import synth
 
     B.load()
-    ffn = synth.config3_weights()
+    ffn = synth.ffn_sweep_weights()
     d, F = ffn.W_up.shape
     T = 4
     n_copies = 4                       # 4 x (58.7 + 58.7) MB > 256 MB last-level cache
@@ -179,9 +182,9 @@ def bench_config3(args):
     W_dn = [torch.from_numpy(ffn.W_dn).cuda() for _ in range(n_copies)]
     th_up, th_dn = int(ffn.theta_up), int(ffn.theta_dn)
     points = []
-    for iB in range(len(synth.CFG3_BLOCKS)):
-        for iR in range(len(synth.CFG3_DENSITIES)):
-            pt = synth.config3_point(iB, iR)
+    for iB in range(len(synth.FFN_SWEEP_BLOCKS)):
+        for iR in range(len(synth.FFN_SWEEP_DENSITIES)):
+            pt = synth.ffn_sweep_point(iB, iR)
             Bk = pt.B
             xu = B.to_dev_bits(synth.pack_bits(pt.X_up))
             xd = B.to_dev_bits(synth.pack_bits(pt.X_dn))
@@ -252,7 +255,7 @@ def _mdlm_step_io(B, torch, m, C, M, k, flags, ev=None):
     return io, bufs
 
 
-def bench_config4(args):
+def bench_mdlm12_step(args):
     """12-layer MDLM, one block step with head, confidence and unmasking."""
     import numpy as np
     import torch
@@ -261,7 +264,7 @@ def bench_config4(args):
     from workloads import synth
 
     B.load()
-    case = synth.config4()
+    case = synth.mdlm12_step_case()
     m = case.model
     C, M, k = case.C, case.B, case.k_unmask
     dm = B.DeviceModel.from_mdlm(m, C + M)
@@ -315,7 +318,7 @@ def bench_config4(args):
     print(json.dumps(out), flush=True)
 
 
-def bench_config5(args):
+def bench_mdlm24_generate(args):
     """24-layer MDLM block-diffusion generation (prefill timed apart)."""
     import numpy as np
     import torch
@@ -325,7 +328,7 @@ def bench_config5(args):
     from workloads import synth
 
     B.load()
-    case = synth.config5()
+    case = synth.mdlm24_generation_case()
     m = case.model
     P = len(case.prompt)
     dm = B.DeviceModel.from_mdlm(m, P + case.n_blocks * case.B)
@@ -361,7 +364,7 @@ def bench_config5(args):
     print(json.dumps(out), flush=True)
 
 
-def bench_config2(args):
+def bench_block(args):
     import numpy as np
     import torch
 
@@ -371,7 +374,7 @@ def bench_config2(args):
     B.load()
     dev = "cuda"
     import ctypes as C
-    case = synth.config2(seed=args.seed)
+    case = synth.block_case(seed=args.seed)
     L = case.layer
     T, C_ctx, M, d, H, F = case.T, case.C, case.M, L.d, L.H, L.F
 

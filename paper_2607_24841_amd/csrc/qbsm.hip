@@ -1076,6 +1076,16 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_list(QbsmArgs a) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+constexpr size_t kWordsLdsBudget = 81920;  // word product: two workgroups per CU fit in LDS
+constexpr int kCus = 256;            // compute units of the device
+constexpr int kThreadsPerCu = 2048;  // resident threads per compute unit
+
+// Waves per workgroup of the word product: 16 for one row group with more
+// than 32 words of K, 8 for up to two row groups with 8 or more, else 4.
+static int words_waves(int RT, int kwords) {
+  return (kwords > 32 && RT == 1) ? 16 : ((kwords >= 4 * kGroup && RT <= 2) ? 8 : 4);
+}
+
 static int pick_rt(int R) {
   if (R <= 16) return 1;
   if (R <= 32) return 2;
@@ -1119,9 +1129,14 @@ static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
 }
 
 template <int RT, int NW>
-static void launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
-                         hipEvent_t e0, hipEvent_t e1) {
+static nmdlm_status launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
+                                 hipEvent_t e0, hipEvent_t e1) {
+  if (dyn > 65536 &&
+      hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_words<RT, NW>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+    return NMDLM_ERR_HIP;
   hipExtLaunchKernelGGL((k_qbsm_words<RT, NW>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0, e1, 0, a);
+  return NMDLM_OK;
 }
 
 template <int RT, int NW, int D>
@@ -1178,15 +1193,22 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
   const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
   if (!rt_forced) {
-    // rows per tile group: the largest that still gives >= 2 workgroups per
-    // compute unit, else the smallest (most row blocks; they re-read weights
-    // from L2)
+    // rows per tile group (at most 4): the largest that gives >= 512
+    // workgroups all resident at once (256 CUs x 2048 threads), else >= 256
+    // resident, else 1 (the most row blocks; they re-read weights from L2)
     RT = 1;
-    for (int r = rt_full; r >= 1; r >>= 1) {
-      const int mb = (16 * r) / c.T;
-      if (mb >= 1 && (long long)gx * ((c.M + mb - 1) / mb) >= 512) {
-        RT = r;
-        break;
+    bool found = false;
+    for (int want = 512; want >= 256 && !found; want /= 2) {
+      for (int r = std::min(rt_full, 4); r >= 1; r >>= 1) {
+        const int mb = (16 * r) / c.T;
+        if (mb < 1) continue;
+        const long long wgs = (long long)gx * ((c.M + mb - 1) / mb);
+        const int nw = words_waves(r, Kw);
+        if (wgs >= want && wgs * nw * 64 <= (long long)kCus * kThreadsPerCu) {
+          RT = r;
+          found = true;
+          break;
+        }
       }
     }
     // a channel-major output segment is written in whole bytes when a row
@@ -1210,10 +1232,10 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   while (has_tr && RT > 1 && (16 * RT) / c.T > 64) RT >>= 1;
   if (path == 0) {
     path = 3;
-    while (RT > 1 && words_lds(RT, 4, Kw) > kLdsBudget && !rt_forced) RT >>= 1;
-    if (words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
+    while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
+    if (words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
   }
-  if (path == 3 && words_lds(RT, 4, Kw) > kLdsBudget) path = 1;
+  if (path == 3 && words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
@@ -1248,8 +1270,8 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   } else if (path == 3) {
     words = true;
     // 8 waves, not 16: a 1024-thread bound caps registers at 128 and spills
-    NW = (ks_per_wg > 32 && RT == 1) ? 16 : ((ks_per_wg >= 4 * kGroup && RT <= 2) ? 8 : 4);
-    if (words_lds(RT, NW, Kw) > kLdsBudget) NW = 4;
+    NW = words_waves(RT, ks_per_wg);
+    if (words_lds(RT, NW, Kw) > kWordsLdsBudget) NW = 4;
     dyn = (size_t)Kw * 8 + (size_t)16 * RT * (2 * Kw + 1) * 4;
   } else if (path == 2) {
     // one kernel (union, list and spike compaction in LDS) when the tile's
@@ -1349,19 +1371,21 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     }
     if (rd != NMDLM_OK) return rd;
   } else if (words) {
+    nmdlm_status rw = NMDLM_OK;
     if (NW == 16) {
-      launch_words<1, 16>(grid, a, dyn, st, e0, e1);
+      rw = launch_words<1, 16>(grid, a, dyn, st, e0, e1);
     } else if (NW == 8) {
-      if (RT == 1) launch_words<1, 8>(grid, a, dyn, st, e0, e1);
-      else launch_words<2, 8>(grid, a, dyn, st, e0, e1);
+      if (RT == 1) rw = launch_words<1, 8>(grid, a, dyn, st, e0, e1);
+      else rw = launch_words<2, 8>(grid, a, dyn, st, e0, e1);
     } else {
       switch (RT) {
-        case 1: launch_words<1, 4>(grid, a, dyn, st, e0, e1); break;
-        case 2: launch_words<2, 4>(grid, a, dyn, st, e0, e1); break;
-        case 4: launch_words<4, 4>(grid, a, dyn, st, e0, e1); break;
-        default: launch_words<8, 4>(grid, a, dyn, st, e0, e1); break;
+        case 1: rw = launch_words<1, 4>(grid, a, dyn, st, e0, e1); break;
+        case 2: rw = launch_words<2, 4>(grid, a, dyn, st, e0, e1); break;
+        case 4: rw = launch_words<4, 4>(grid, a, dyn, st, e0, e1); break;
+        default: rw = launch_words<8, 4>(grid, a, dyn, st, e0, e1); break;
       }
     }
+    if (rw != NMDLM_OK) return rw;
   } else if (fused) {
     if (NW == 16) {
       launch_fused<1, 16>(grid, a, dyn, st, e0, e1);

@@ -1,6 +1,6 @@
 """Write the stored expected values of the full-size MDLM cases.
 
-Usage:  python tests/golden/make_golden.py cfg4|cfg5
+Usage:  python tests/golden/make_golden.py mdlm12|mdlm24
 
 Calls only the oracle (oracle/) and the seeded generator (workloads/); the
 HIP library is never imported here.  Outputs are JSON files next to this
@@ -36,9 +36,9 @@ def cache_digests(kc, vc, J):
             [sha(synth.pack_bits(v[:, :J])) for v in vc])
 
 
-def cfg4():
+def mdlm12():
     t0 = time.time()
-    case = synth.config4()
+    case = synth.mdlm12_step_case()
     m = case.model
     emb = O.unpack_model_emb(m)
     C, M = case.C, case.B
@@ -54,7 +54,7 @@ def cfg4():
     out = {
         "case": "12-layer MDLM, one block step: d=2048, 16 heads x 128, FFN 8192, V=32000, T=4, "
                 "1024 context tokens (prefill), block of 32 masked tokens, top-8 unmasking",
-        "seed": synth.MASTER_SEEDS[4],
+        "seed": synth.SEEDS["mdlm12"],
         "layout": "logits: float32 [M][V]; y: packed last-layer spikes uint64 [T][M][d/64]; "
                   "caches: packed spike rows uint64 [T][C+M][d/64] per layer",
         "tokens": r.tokens.tolist(),
@@ -71,27 +71,27 @@ def cfg4():
         "head_k_active": int(O.block_union(r.Y).sum()),
         "seconds": round(time.time() - t0, 1),
     }
-    with open(os.path.join(HERE, "cfg4_block_step.json"), "w") as f:
+    with open(os.path.join(HERE, "mdlm12_block_step.json"), "w") as f:
         json.dump(out, f, indent=1)
 
 
-def cfg5():
+def mdlm24():
     t0 = time.time()
-    case = synth.config5()
+    case = synth.mdlm24_generation_case()
     m = case.model
     ids, log = O.generate(m, case.prompt, case.n_blocks, case.B, case.steps, case.k_unmask)
     out = {
         "case": "24-layer MDLM generation: d=2048, 16 heads x 128, FFN 8192, V=32000, T=4, "
                 "2048-token prompt, 8 blocks of 32 tokens, 8 steps per block, 4 tokens per step",
-        "seed": synth.MASTER_SEEDS[5],
+        "seed": synth.SEEDS["mdlm24"],
         "ids": ids.tolist(),
         "chosen": [c.tolist() for c in log],
         "seconds": round(time.time() - t0, 1),
     }
-    with open(os.path.join(HERE, "cfg5_generation.json"), "w") as f:
+    with open(os.path.join(HERE, "mdlm24_generation.json"), "w") as f:
         json.dump(out, f, indent=1)
 
 
 if __name__ == "__main__":
-    which = sys.argv[1] if len(sys.argv) > 1 else "cfg4"
-    {"cfg4": cfg4, "cfg5": cfg5}[which]()
+    which = sys.argv[1] if len(sys.argv) > 1 else "mdlm12"
+    {"mdlm12": mdlm12, "mdlm24": mdlm24}[which]()

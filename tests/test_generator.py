@@ -19,15 +19,15 @@ def test_pack_unpack_roundtrip_and_layout():
 
 
 def test_seeds_reproduce_and_differ():
-    a = synth.config1()
-    b = synth.config1()
+    a = synth.linear_layer_case()
+    b = synth.linear_layer_case()
     assert np.array_equal(a.S, b.S) and np.array_equal(a.W, b.W) and np.array_equal(a.bias, b.bias)
-    c = synth.config1(seed=7)
+    c = synth.linear_layer_case(seed=7)
     assert not np.array_equal(a.W, c.W)
 
 
-def test_config1_distributions():
-    c = synth.config1()
+def test_linear_layer_distributions():
+    c = synth.linear_layer_case()
     assert c.S.shape == (4, 8, 512) and c.W.shape == (512, 512) and c.theta == 256
     n = c.S.size
     assert abs(c.S.mean() - 0.15) < 5 * np.sqrt(0.15 * 0.85 / n)

@@ -1,5 +1,6 @@
 """GPU parity of nmdlm_block_step: a spiking transformer block at one
-denoising step (configuration 2, full size, with its context prefill), and a
+denoising step (d=1024, 16 tokens over 512 of context, full size, with its
+context prefill), and a
 small MDLM with head, confidence, unmasking and block-diffusion generation."""
 import numpy as np
 import pytest
@@ -65,19 +66,19 @@ def _check_block(case, flags=0):
 
 def test_block_small_shapes():
     need_gpu()
-    case = synth.config2(seed=7, C=70, M=5, d=128, H=2, F=256)
+    case = synth.block_case(seed=7, C=70, M=5, d=128, H=2, F=256)
     _check_block(case)
     _check_block(case, flags=1)
 
 
-def test_config2_full_size():
+def test_block_full_size():
     need_gpu()
-    _check_block(synth.config2())
+    _check_block(synth.block_case())
 
 
 def test_block_step_graph_replays_match_eager():
     torch, B = need_gpu()
-    case = synth.config2()
+    case = synth.block_case()
     L = case.layer
     T, C, M, d = case.T, case.C, case.M, L.d
     dm = B.DeviceModel([L], T, C + M, d, L.H, L.F)
@@ -113,9 +114,9 @@ def test_block_step_graph_replays_match_eager():
                                    4 << 20, 0x4, 2 << 16, 8 << 16],
                          ids=["P1", "P3", "P2RT1", "nofuse", "fused", "words", "dma", "attn-fused",
                               "RT2-bytes", "RT8"])
-def test_config2_forced_paths(flags):
+def test_block_forced_paths(flags):
     need_gpu()
-    _check_block(synth.config2(), flags=flags)
+    _check_block(synth.block_case(), flags=flags)
 
 
 # ----------------------------------------------------------------------------

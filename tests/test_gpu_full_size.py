@@ -1,7 +1,7 @@
-"""GPU parity at the full sizes of configurations 3, 4 and 5.
+"""GPU parity at full size: the FFN sweep, the 12-layer block step and the 24-layer generation.
 
-Configuration 3 (FFN sweep) is checked element by element against the oracle
-computed in the test.  Configurations 4 and 5 compare against stored values
+The FFN sweep is checked element by element against the oracle
+computed in the test.  The 12- and 24-layer models compare against stored values
 written by tests/golden/make_golden.py (oracle only): exact digests of the
 logits, last-layer spikes and every cache, and the unmasking decisions."""
 import hashlib
@@ -25,18 +25,18 @@ def _sha(a):
 
 
 # ----------------------------------------------------------------------------
-# configuration 3: FFN weight-traffic sweep (16 points x 2 products)
+# FFN weight-traffic sweep (16 points x 2 products)
 # ----------------------------------------------------------------------------
 @pytest.fixture(scope="module")
 def ffn():
     need_gpu()
-    return synth.config3_weights()
+    return synth.ffn_sweep_weights()
 
 
-@pytest.mark.parametrize("iB", range(4), ids=[f"B{b}" for b in synth.CFG3_BLOCKS])
-def test_config3_sweep_points(ffn, iB):
+@pytest.mark.parametrize("iB", range(4), ids=[f"B{b}" for b in synth.FFN_SWEEP_BLOCKS])
+def test_ffn_sweep_points(ffn, iB):
     for iR in range(4):
-        pt = synth.config3_point(iB, iR)
+        pt = synth.ffn_sweep_point(iB, iR)
         for name, X, W, th in (("up", pt.X_up, ffn.W_up, ffn.theta_up),
                                ("dn", pt.X_dn, ffn.W_dn, ffn.theta_dn)):
             I_ref = O.qbsm(X, W)
@@ -48,10 +48,10 @@ def test_config3_sweep_points(ffn, iB):
             assert st["k_active"] == act and st["weight_bytes"] == act * W.shape[1], tag
 
 
-def test_config3_chained_ffn(ffn):
+def test_ffn_chained(ffn):
     # X_dn = IF output of the up product, as in a real FFN
     for iB, iR in ((1, 0), (3, 3)):
-        pt = synth.config3_point(iB, iR)
+        pt = synth.ffn_sweep_point(iB, iR)
         _, h, _, _, _ = run_qbsm(pt.X_up, ffn.W_up, None, theta=ffn.theta_up, want_cur=False)
         h_ref = O.if_neuron(O.qbsm(pt.X_up, ffn.W_up), ffn.theta_up)[0]
         assert_same(h, h_ref, "hidden spikes")
@@ -61,7 +61,7 @@ def test_config3_chained_ffn(ffn):
 
 
 # ----------------------------------------------------------------------------
-# configurations 4 and 5: multi-layer MDLM against stored oracle values
+# 12- and 24-layer MDLM against stored oracle values
 # ----------------------------------------------------------------------------
 def _load(name):
     path = os.path.join(GOLDEN, name)
@@ -83,10 +83,10 @@ def _chosen_ok(got, want, conf, tol=1e-9):
 
 
 @pytest.mark.parametrize("flags", [0, 0x4, 4 << 20], ids=["default", "attn-fused", "dma"])
-def test_config4_block_step_matches_stored_oracle(flags):
+def test_mdlm12_step_matches_stored_oracle(flags):
     torch, B = need_gpu()
-    ref = _load("cfg4_block_step.json")
-    case = synth.config4()
+    ref = _load("mdlm12_block_step.json")
+    case = synth.mdlm12_step_case()
     m = case.model
     C, M, k = case.C, case.B, case.k_unmask
     dm = B.DeviceModel.from_mdlm(m, C + M)
@@ -131,12 +131,12 @@ def test_config4_block_step_matches_stored_oracle(flags):
         assert vd == ref["v_cache_sha256"][l], f"V cache layer {l}"
 
 
-def test_config5_generation_matches_stored_oracle():
+def test_mdlm24_generation_matches_stored_oracle():
     need_gpu()
     from paper_2607_24841_amd import binding as B
     from paper_2607_24841_amd.generate import generate
-    ref = _load("cfg5_generation.json")
-    case = synth.config5()
+    ref = _load("mdlm24_generation.json")
+    case = synth.mdlm24_generation_case()
     m = case.model
     dm = B.DeviceModel.from_mdlm(m, len(case.prompt) + case.n_blocks * case.B)
     ids, log = generate(dm, case.prompt, case.n_blocks, case.B, case.steps, case.k_unmask)

@@ -116,8 +116,8 @@ ATTN = [  # T, M, C, H, dh, p
     (2, 5, 37, 2, 64, 0.5),
     (1, 1, 0, 1, 128, 0.5),
     (4, 40, 100, 3, 64, 0.2),
-    (4, 16, 512, 16, 64, 0.3),     # one block step of configuration 2
-    (4, 32, 1024, 16, 128, 0.4),   # one block step of configuration 4
+    (4, 16, 512, 16, 64, 0.3),     # the one-block step (d=1024, 16 heads of 64)
+    (4, 32, 1024, 16, 128, 0.4),   # the 12-layer model step (16 heads of 128)
     (3, 17, 63, 2, 128, 0.05),
 ]
 

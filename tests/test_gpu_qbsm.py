@@ -41,9 +41,9 @@ def _check(case, flags=0, theta_vec=None):
     assert st["weight_bytes"] == k_act * case.N
 
 
-def test_config1_bit_exact():
+def test_linear_layer_bit_exact():
     need_gpu()
-    _check(synth.config1())
+    _check(synth.linear_layer_case())
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=[f"T{s[0]}M{s[1]}K{s[2]}N{s[3]}" for s in SHAPES])
@@ -98,6 +98,15 @@ def test_large_k_shapes(flags):
     # K beyond the in-kernel-list limit, and a long block (many row blocks)
     _check(synth.make_qbsm_case(41, 4, 4, 20000, 130, 0.02), flags=flags)
     _check(synth.make_qbsm_case(42, 4, 300, 700, 200, 0.05), flags=flags)
+
+
+def test_words_with_more_than_64k_lds():
+    need_gpu()
+    # K = 14336 with two row groups: the staged spike rows need more than
+    # 64 KB of LDS (the launch raises the dynamic LDS limit)
+    c = synth.make_qbsm_case(44, 4, 16, 14336, 320, 0.01)
+    _check(c, flags=WORDS | (2 << 16))
+    _check(c)
 
 
 def test_per_neuron_thresholds_and_currents_only():

@@ -8,7 +8,7 @@ attention, no unmasking).
 Random streams
 --------------
 Every array comes from its own PCG64 stream addressed by a spawn key under
-the configuration's seed: ``np.random.SeedSequence(seed, spawn_key=path)``.
+the workload's seed: ``np.random.SeedSequence(seed, spawn_key=path)``.
 An array therefore never depends on how many other arrays were drawn before
 it, and a large model can be generated layer by layer.
 
@@ -35,7 +35,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-MASTER_SEEDS = {1: 1001, 2: 1002, 3: 1003, 4: 1004, 5: 1005}
+SEEDS = {"linear": 1001, "block": 1002, "ffn_sweep": 1003, "mdlm12": 1004, "mdlm24": 1005}
 
 
 # ----------------------------------------------------------------------------
@@ -117,7 +117,7 @@ def sorted_lut_s8(rng: np.random.Generator) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
-# single QBSM + IF (configuration 1 and the tiny shapes used by the tests)
+# single QBSM + IF (the 4x8x512 -> 512 spiking linear layer and the tiny shapes of the tests)
 # ----------------------------------------------------------------------------
 @dataclass
 class QbsmCase:
@@ -146,7 +146,7 @@ def make_qbsm_case(seed: int, T: int, M: int, K: int, N: int, density: float,
     return QbsmCase(T, M, K, N, S, W, bias, int(theta))
 
 
-def config1(seed: int = MASTER_SEEDS[1]) -> QbsmCase:
+def linear_layer_case(seed: int = SEEDS["linear"]) -> QbsmCase:
     """Single spiking linear layer: T=4, B=8, K=N=512, Bernoulli(0.15) input,
     int8 weights on [-127,127], int32 bias on [-64,64], threshold 256."""
     return make_qbsm_case(seed, T=4, M=8, K=512, N=512, density=0.15, theta=256)
@@ -193,7 +193,7 @@ def make_layer(seed: int, layer: int, d: int, F: int, H: int) -> LayerParams:
 
 
 # ----------------------------------------------------------------------------
-# configuration 2: one spiking transformer block, one denoising step
+# one spiking transformer block (d=1024, 16 heads, FFN 4096), one denoising step
 # ----------------------------------------------------------------------------
 @dataclass
 class BlockCase:
@@ -205,7 +205,7 @@ class BlockCase:
     X_blk: np.ndarray     # bool [T][M][d] block inputs
 
 
-def config2(seed: int = MASTER_SEEDS[2], C: int = 512, M: int = 16, d: int = 1024,
+def block_case(seed: int = SEEDS["block"], C: int = 512, M: int = 16, d: int = 1024,
             H: int = 16, F: int = 4096, T: int = 4, density: float = 0.10) -> BlockCase:
     X_ctx = bernoulli(stream(seed, 0), density, (T, C, d))
     X_blk = bernoulli(stream(seed, 1), density, (T, M, d))
@@ -214,10 +214,10 @@ def config2(seed: int = MASTER_SEEDS[2], C: int = 512, M: int = 16, d: int = 102
 
 
 # ----------------------------------------------------------------------------
-# configuration 3: FFN weight-traffic sweep
+# FFN weight-traffic sweep (4096 -> 14336 -> 4096)
 # ----------------------------------------------------------------------------
-CFG3_BLOCKS = (1, 4, 16, 64)
-CFG3_DENSITIES = (0.02, 0.05, 0.10, 0.30)
+FFN_SWEEP_BLOCKS = (1, 4, 16, 64)
+FFN_SWEEP_DENSITIES = (0.02, 0.05, 0.10, 0.30)
 
 
 @dataclass
@@ -239,7 +239,7 @@ class FfnPoint:
     X_dn: np.ndarray      # bool [T][B][F]
 
 
-def config3_weights(seed: int = MASTER_SEEDS[3], d: int = 4096, F: int = 14336) -> FfnWeights:
+def ffn_sweep_weights(seed: int = SEEDS["ffn_sweep"], d: int = 4096, F: int = 14336) -> FfnWeights:
     W_up = int8_uniform(stream(seed, 0), (d, F))
     W_dn = int8_uniform(stream(seed, 1), (F, d))
     th = int_uniform(stream(seed, 2), 128, 512, (2,))
@@ -254,17 +254,17 @@ def correlated_spikes(rng: np.random.Generator, T: int, B: int, K: int,
     return rng.random((T, B, K)) < r[None, None, :]
 
 
-def config3_point(iB: int, iR: int, seed: int = MASTER_SEEDS[3], d: int = 4096,
+def ffn_sweep_point(iB: int, iR: int, seed: int = SEEDS["ffn_sweep"], d: int = 4096,
                   F: int = 14336, T: int = 4) -> FfnPoint:
-    B = CFG3_BLOCKS[iB]
-    rho = CFG3_DENSITIES[iR]
+    B = FFN_SWEEP_BLOCKS[iB]
+    rho = FFN_SWEEP_DENSITIES[iR]
     X_up = correlated_spikes(stream(seed, 10 + 4 * iB + iR, 0), T, B, d, rho)
     X_dn = correlated_spikes(stream(seed, 10 + 4 * iB + iR, 1), T, B, F, rho)
     return FfnPoint(B, rho, T, X_up, X_dn)
 
 
 # ----------------------------------------------------------------------------
-# configurations 4 and 5: multi-layer spiking MDLM
+# multi-layer spiking MDLM (12-layer block step, 24-layer generation)
 # ----------------------------------------------------------------------------
 @dataclass
 class MdlmModel:
@@ -318,7 +318,7 @@ class MdlmStepCase:
     k_unmask: int
 
 
-def config4(seed: int = MASTER_SEEDS[4], n_layers: int = 12, C: int = 1024, B: int = 32,
+def mdlm12_step_case(seed: int = SEEDS["mdlm12"], n_layers: int = 12, C: int = 1024, B: int = 32,
             k_unmask: int = 8, **kw) -> MdlmStepCase:
     model = make_mdlm(seed, n_layers, max_pos=max(C + B, kw.pop("max_pos", 0)), **kw)
     ctx = random_tokens(seed, C, model.V)
@@ -335,7 +335,7 @@ class GenerationCase:
     k_unmask: int
 
 
-def config5(seed: int = MASTER_SEEDS[5], n_layers: int = 24, prompt_len: int = 2048,
+def mdlm24_generation_case(seed: int = SEEDS["mdlm24"], n_layers: int = 24, prompt_len: int = 2048,
             n_blocks: int = 8, B: int = 32, steps: int = 8, k_unmask: int = 4,
             **kw) -> GenerationCase:
     model = make_mdlm(seed, n_layers, max_pos=prompt_len + n_blocks * B, **kw)
