@@ -466,7 +466,6 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   __shared__ int sRed[NW];
   __shared__ EpiStage ep;
   __shared__ int sLast;
-  __shared__ int sFirst;  // first active row of the tile (target of the loads of inactive rows)
   // dynamic: local union [Kw] (u64), then the tile's spike rows as dwords
   // with row stride 2*Kw+1 (odd: the 16 rows a wave reads fall in different banks)
   extern __shared__ unsigned long long sDyn[];
@@ -480,8 +479,13 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   unsigned long long* sLU = sDyn;
   uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + Kw);
 
+  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
+  // With the producer's partial unions, the union is their OR over the whole
+  // block (a superset of this row block's own union: the extra rows meet zero
+  // spikes), and its loads go out with the staging loads; otherwise it is the
+  // OR of the staged rows.
+  const bool from_parts = a.upart && !a.dense;
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
-  if (tid == 0) sFirst = 0x7fffffff;
   stage_epilogue<NT>(a, ep, tid, x, y);
   for (int i = tid; i < ROWS * Kw; i += NT) {
     const int lr = i / Kw, w = i - lr * Kw;
@@ -490,21 +494,41 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     sS[lr * lds_row + 2 * w] = (uint32_t)v;
     sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
   }
-  __syncthreads();
-  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
-  for (int w = tid; w < Kw; w += NT) {
-    unsigned long long u = ~0ull;
-    if (!a.dense) {
-      u = 0ull;
-      for (int lr = 0; lr < ROWS; ++lr)
-        u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
-             ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+  if (from_parts) {
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long u = 0ull;
+      int q = 0;
+      for (; q + 4 <= a.nparts; q += 4)
+        u |= a.upart[(size_t)q * Kw + w] | a.upart[(size_t)(q + 1) * Kw + w] |
+             a.upart[(size_t)(q + 2) * Kw + w] | a.upart[(size_t)(q + 3) * Kw + w];
+      for (; q < a.nparts; ++q) u |= a.upart[(size_t)q * Kw + w];
+      sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
     }
-    u = (w == Kw - 1) ? (u & last_mask) : u;
-    sLU[w] = u;
-    if (u) atomicMin(&sFirst, w * 64 + (int)__builtin_ctzll(u));
   }
   __syncthreads();
+  if (!from_parts) {
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long u = ~0ull;
+      if (!a.dense) {
+        u = 0ull;
+        for (int lr = 0; lr < ROWS; ++lr)
+          u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
+               ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+      }
+      sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
+    }
+    __syncthreads();
+  }
+  // first active row (the target of the loads of inactive rows), per wave
+  int first = 0x7fffffff;
+  for (int w = lane; w < Kw; w += kWave) {
+    const unsigned long long u = sLU[w];
+    if (u) {
+      first = w * 64 + (int)__builtin_ctzll(u);
+      break;
+    }
+  }
+  for (int o = kWave / 2; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o));
 
   const int w0 = (int)(((long long)Kw * z) / a.P);
   const int w1 = (int)(((long long)Kw * (z + 1)) / a.P);
@@ -522,7 +546,6 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   // tile (or a word past the range) loads the tile's first active row, whose
   // line is read anyway.  Every word then issues the same 16 loads, so the
   // next word's loads can be in flight while the current one is multiplied.
-  const int first = sFirst;
   const uint32_t first_off = (uint32_t)first * ldw + colb;
   const int stride = NW;
   auto load_word = [&](int w, uint32_t (&xg)[16]) {
