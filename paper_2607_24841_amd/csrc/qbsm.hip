@@ -214,6 +214,7 @@ constexpr int kGroup = 2;
 constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
 constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
+static_assert(kMaxEpiTokens >= 8 * 16, "every tile's residual words are staged (RT <= 8)");
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
   // 4 bits -> 4 bytes of 0/1 (bit i -> byte i); the shifted copies of the
@@ -259,7 +260,11 @@ __device__ __forceinline__ void stage_epilogue(const QbsmArgs& a, EpiStage& ep, 
   const int n = x * 64 + tid;
   if (tid < 64) {
     ep.bias[tid] = (a.bias && n < a.N) ? a.bias[n] : 0;
-    ep.theta[tid] = a.theta_vec ? (n < a.N ? a.theta_vec[n] : 1) : 0;
+    // firing threshold of each column: per channel, else the segment's
+    int th = 0;
+    if (a.theta_vec) th = n < a.N ? a.theta_vec[n] : 1;
+    else if (a.mode == EPI_IF || a.mode == EPI_QNL_IF) th = a.seg[(x * 64) / a.seg_w].theta;
+    ep.theta[tid] = th;
   }
   if (a.resid) {
     for (int i = tid; i < a.T * a.Mb && i < kMaxEpiTokens; i += NT) {
@@ -339,14 +344,13 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   const SpikeSeg seg = a.seg[segi];
   const int wseg = (n0 - segi * a.seg_w) >> 6;
   const int bias_n = ep.bias[col];
-  const int theta = a.theta_vec ? ep.theta[col] : seg.theta;
+  const int theta = ep.theta[col];
   const bool spikes = a.mode != EPI_CUR;
   const bool tr = spikes && seg.transposed;
   // channel-major output in whole bytes: the row block's tokens fill whole
   // bytes of the position words, so this workgroup owns them (plain byte
   // stores); otherwise bits are cleared and set with atomics
   const bool tr_bytes = tr && (a.Mb & 7) == 0 && a.Mb <= 32 && (seg.pos0 & 7) == 0;
-  const bool staged = a.resid && a.T * a.Mb <= kMaxEpiTokens;
   const int wbase = tr ? ((seg.pos0 + y * a.Mb) >> 6) : 0;
   uint64_t tb0[NMDLM_MAX_T], tb1[NMDLM_MAX_T];
   uint32_t vb[NMDLM_MAX_T];
@@ -381,8 +385,8 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
             I = (int)ep.lut[qv & 0xFF];
           }
           if (a.resid) {
-            const unsigned long long rw =
-                staged ? ep.resid[t * a.Mb + ml] : a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x];
+            // staged at entry: T * Mb <= 16 * RT <= kMaxEpiTokens rows
+            const unsigned long long rw = ep.resid[t * a.Mb + ml];
             if ((rw >> col) & 1ull) I += theta;
           }
           V += I;
