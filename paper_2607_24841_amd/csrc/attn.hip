@@ -16,18 +16,37 @@ __device__ __forceinline__ uint32_t expand4_a(uint32_t nib) {
   return (nib * 0x00204081u) & 0x01010101u;
 }
 
-// grid (H, ceil(M/16), T); 4 waves take 64-key chunks in turn.
-template <int DHW>
-__global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
-                                              const uint64_t* __restrict__ kc,
-                                              const uint64_t* __restrict__ vt, int64_t cap, int T,
-                                              int M, int C, int H,
-                                              const uint8_t* __restrict__ lut,
-                                              int32_t* __restrict__ a_out) {
+// Table bytes 4*lane .. 4*lane+3 as one dword (byte loads: any alignment).
+__device__ __forceinline__ int lut_dword(const uint8_t* __restrict__ lut, int lane) {
+  const uint8_t* b = lut + 4 * lane;
+  return (int)((uint32_t)b[0] | ((uint32_t)b[1] << 8) | ((uint32_t)b[2] << 16) |
+               ((uint32_t)b[3] << 24));
+}
+
+// floor(256 * num / den) for num >= 0, den > 0 (0 when den = 0).  For fewer
+// than 65536 keys, 256 * num < 2^32 and the division is done in 32 bits.
+__device__ __forceinline__ int32_t attn_norm(long long num, long long den, bool small) {
+  if (den <= 0) return 0;
+  if (small) return (int32_t)((256u * (uint32_t)num) / (uint32_t)den);
+  return (int32_t)((256LL * num) / den);
+}
+
+// grid (H, ceil(M/16), T); wave i takes 64-key chunks i, i+NW, ...  Every
+// load of a chunk (16 keys per lane, NT value words) is issued before it is
+// scored; with up to 64*NW keys each wave has one chunk, so all the key and
+// value loads of the workgroup are in flight together.  The table is read
+// with ds_bpermute from lut_dw (entry s sits in byte s%4 of lane s/4).
+template <int DHW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q,
+                                                  const uint64_t* __restrict__ kc,
+                                                  const uint64_t* __restrict__ vt, int64_t cap,
+                                                  int T, int M, int C, int H,
+                                                  const uint8_t* __restrict__ lut,
+                                                  int32_t* __restrict__ a_out) {
   constexpr int DH = DHW * 64;
   constexpr int NT = DH / 16;
-  __shared__ int sLut[256];
-  __shared__ int sNum[4][16][DH];
+  constexpr int NTH = NW * 64;
+  __shared__ int sNum[16][DH];
   __shared__ int sDen[16];
   __shared__ int sCnt[DH];
 
@@ -43,16 +62,14 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
   const int J = C + M;
   const int nch = (J + 63) / 64;
 
-  sLut[tid] = lut[tid];
-  if (tid < 16) sDen[tid] = 0;
-  for (int i = tid; i < DH; i += 256) sCnt[i] = 0;
-
+  const int lut_dw = lut_dword(lut, lane);
   const int iq = qb * 16 + c;
-  const bool qv = iq < M;
   uint64_t qw[DHW];
 #pragma unroll
-  for (int w = 0; w < DHW; ++w) qw[w] = qv ? q[((size_t)t * M + iq) * dw + h * DHW + w] : 0ull;
-  __syncthreads();
+  for (int w = 0; w < DHW; ++w) qw[w] = q[((size_t)t * M + min(iq, M - 1)) * dw + h * DHW + w];
+  for (int i = tid; i < 16 * DH; i += NTH) (&sNum[0][0])[i] = 0;
+  if (tid < 16) sDen[tid] = 0;
+  for (int i = tid; i < DH; i += NTH) sCnt[i] = 0;
 
   v4i acc[NT];
   int cnt[NT];
@@ -62,12 +79,11 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
     cnt[i] = 0;
   }
   int den = 0;
+  // rows of queries past M (clamped loads) are scored too; they are never read
 
-  for (int jc = wave; jc < nch; jc += 4) {
+  for (int jc = wave; jc < nch; jc += NW) {  // wave-uniform
     const int j0 = jc * 64 + 16 * g;
-    uint32_t pk[4] = {0u, 0u, 0u, 0u};
-    // keys past C+M read a valid row (clamped) and are masked, so that all
-    // sixteen key loads are issued back to back
+    // keys past C+M read a valid row (clamped) and are masked when scored
     uint64_t kw[16][DHW];
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
@@ -76,14 +92,19 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
 #pragma unroll
       for (int w = 0; w < DHW; ++w) kw[s][w] = kr[w];
     }
+    uint64_t vw[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) vw[nt] = vt[((size_t)t * d + h * DH + nt * 16 + c) * capw + jc];
+    __builtin_amdgcn_sched_barrier(0);  // every load above is issued before the first use
+    uint32_t pk[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
       int sc = 0;
 #pragma unroll
       for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & kw[s][w]);
       const bool jv = j0 + s < J;
-      const int pl = sLut[sc];
-      const int p = jv ? pl : 0;
+      const int pw = __builtin_amdgcn_ds_bpermute((sc >> 2) << 2, lut_dw);
+      const int p = jv ? (pw >> ((sc & 3) * 8)) & 0xFF : 0;
       den += p;
       pk[s >> 2] |= jv ? (uint32_t)((p - 128) & 0xFF) << ((s & 3) * 8) : 0u;
     }
@@ -92,36 +113,39 @@ __global__ __launch_bounds__(256) void k_attn(const uint64_t* __restrict__ q,
     const uint32_t vmask = nvalid >= 16 ? 0xFFFFu : (nvalid <= 0 ? 0u : ((1u << nvalid) - 1u));
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int ch = h * DH + nt * 16 + c;
-      const uint64_t wv = vt[((size_t)t * d + ch) * capw + jc];
-      const uint32_t bits = (uint32_t)(wv >> (16 * g)) & vmask;
+      const uint32_t bits = (uint32_t)(vw[nt] >> (16 * g)) & vmask;
       cnt[nt] += __popc(bits);
       const v4i bf = v4i{(int)expand4_a(bits & 0xFu), (int)expand4_a((bits >> 4) & 0xFu),
                          (int)expand4_a((bits >> 8) & 0xFu), (int)expand4_a(bits >> 12)};
       acc[nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf, acc[nt], 0, 0, 0);
     }
   }
-
+  __syncthreads();  // the partial sums are cleared
+  if (wave < nch) {  // wave-uniform
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sNum[wave][g * 4 + e][nt * 16 + c] = acc[nt][e];
-  atomicAdd(&sDen[c], den);
+      for (int e = 0; e < 4; ++e) atomicAdd(&sNum[g * 4 + e][nt * 16 + c], acc[nt][e]);
+    atomicAdd(&sDen[c], den);
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) atomicAdd(&sCnt[nt * 16 + c], cnt[nt]);
+    for (int nt = 0; nt < NT; ++nt) atomicAdd(&sCnt[nt * 16 + c], cnt[nt]);
+  }
   __syncthreads();
 
-  for (int i = tid; i < 16 * DH; i += 256) {
+  const bool small = J < 65536;
+  for (int i = tid; i < 16 * DH; i += NTH) {
     const int qi = i / DH, ch = i - qi * DH;
     const int iq2 = qb * 16 + qi;
     if (iq2 < M) {
-      const long long num = (long long)sNum[0][qi][ch] + sNum[1][qi][ch] + sNum[2][qi][ch] +
-                            sNum[3][qi][ch] + 128LL * sCnt[ch];
-      const long long dn = sDen[qi];
-      a_out[((size_t)t * M + iq2) * d + h * DH + ch] = dn > 0 ? (int32_t)((256LL * num) / dn) : 0;
+      const long long num = (long long)sNum[qi][ch] + 128LL * sCnt[ch];
+      a_out[((size_t)t * M + iq2) * d + h * DH + ch] = attn_norm(num, sDen[qi], small);
     }
   }
 }
+
+// waves per workgroup: 16 for dh = 64; 8 for dh = 128 (its 16 keys of two
+// words per lane need more than the 128 registers of a 1024-thread group)
+constexpr int kAttnWaves64 = 16, kAttnWaves128 = 8;
 
 nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,
                          int64_t cap, int T, int M, int C, int H, int dh, const uint8_t* lut,
@@ -129,12 +153,12 @@ nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache, const uint6
   const dim3 grid(H, (M + 15) / 16, T);
   switch (dh / 64) {
     case 1:
-      hipLaunchKernelGGL(k_attn<1>, grid, dim3(256), 0, st, q, k_cache, vt_cache, cap, T, M, C, H,
-                         lut, a_out);
+      hipLaunchKernelGGL((k_attn<1, kAttnWaves64>), grid, dim3(kAttnWaves64 * 64), 0, st, q, k_cache,
+                         vt_cache, cap, T, M, C, H, lut, a_out);
       break;
     case 2:
-      hipLaunchKernelGGL(k_attn<2>, grid, dim3(256), 0, st, q, k_cache, vt_cache, cap, T, M, C, H,
-                         lut, a_out);
+      hipLaunchKernelGGL((k_attn<2, kAttnWaves128>), grid, dim3(kAttnWaves128 * 64), 0, st, q, k_cache,
+                         vt_cache, cap, T, M, C, H, lut, a_out);
       break;
     default:
       return NMDLM_ERR_UNSUPPORTED;
@@ -248,7 +272,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_if(const uint64_t* __restrict_
 
   // table, query words and the first round of chunks: unconditional loads in
   // one straight run, so each wait covers only what it needs
-  const int lut_dw = (int)reinterpret_cast<const uint32_t*>(lut)[lane];
+  const int lut_dw = lut_dword(lut, lane);
   const int iq = qb * 16 + c;
   uint64_t qw[DHW];
 #pragma unroll
@@ -309,8 +333,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_if(const uint64_t* __restrict_
     uint64_t uor = 0ull;
     for (int tt = 0; tt < T; ++tt) {
       const long long num = (long long)sNum[(tt * 16 + i) * DH + chn] + 128LL * sCnt[tt][chn];
-      const long long dn = sDen[tt][i];
-      V += dn > 0 ? (256LL * num) / dn : 0LL;
+      V += attn_norm(num, sDen[tt][i], J < 65536);
       const bool s = V >= theta;
       if (s) V -= theta;
       const uint64_t word = __builtin_amdgcn_ballot_w64(s);
@@ -328,7 +351,6 @@ nmdlm_status launch_attn_if(const uint64_t* q, const uint64_t* k_cache, const ui
                             int32_t theta, uint64_t* s_out, uint64_t* u_out, hipStream_t st) {
   const size_t dyn = (size_t)T * 16 * dh * sizeof(int);
   if (dyn > kAttnIfMaxLds || T > NMDLM_MAX_T) return NMDLM_ERR_UNSUPPORTED;
-  if (reinterpret_cast<uintptr_t>(lut) % 4 != 0) return NMDLM_ERR_UNSUPPORTED;  // read as dwords
   const dim3 grid(H, (M + 15) / 16);
   switch (dh / 64) {
     case 1:

@@ -6,6 +6,10 @@ namespace nmdlm {
 
 // One wave per (token, 64-neuron word); lane = neuron.  Integrate-then-fire
 // with soft reset; the membrane is int64 so any int32 currents are exact.
+// Timesteps go in rounds of kIfRound whose current (and residual) loads are
+// all issued before the recurrence uses the first of them.
+constexpr int kIfRound = 8;
+
 __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int T, int M, int N,
                                             int32_t theta, const int32_t* __restrict__ theta_vec,
                                             const uint64_t* __restrict__ resid,
@@ -19,18 +23,32 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
   const int m = (int)(unit / Nw), w = (int)(unit % Nw);
   const int n = w * 64 + lane;
   const bool nv = n < N;
-  const long long th = theta_vec ? (nv ? theta_vec[n] : 1) : theta;
+  const int nc = nv ? n : N - 1;  // lanes past N read a valid current and drop it
+  const long long th = theta_vec ? theta_vec[nc] : theta;
   long long V = (v_inout && nv) ? v_inout[(size_t)m * N + n] : 0;
   uint64_t uor = 0;
-  for (int t = 0; t < T; ++t) {
-    long long I = nv ? cur[((size_t)t * M + m) * N + n] : 0;
-    if (resid && ((resid[((size_t)t * M + m) * Nw + w] >> lane) & 1ull)) I += th;
-    V += I;
-    const bool s = nv && V >= th;
-    if (s) V -= th;
-    const uint64_t word = __builtin_amdgcn_ballot_w64(s);
-    uor |= word;
-    if (lane == 0) s_out[((size_t)t * M + m) * Nw + w] = word;
+  for (int t0 = 0; t0 < T; t0 += kIfRound) {
+    int32_t cu[kIfRound];
+    uint64_t rw[kIfRound];
+#pragma unroll
+    for (int u = 0; u < kIfRound; ++u) {
+      const int t = min(t0 + u, T - 1);
+      cu[u] = cur[((size_t)t * M + m) * N + nc];
+      rw[u] = resid ? resid[((size_t)t * M + m) * Nw + w] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kIfRound; ++u) {
+      const int t = t0 + u;
+      if (t >= T) break;  // wave-uniform
+      long long I = nv ? cu[u] : 0;
+      if ((rw[u] >> lane) & 1ull) I += th;
+      V += I;
+      const bool s = nv && V >= th;
+      if (s) V -= th;
+      const uint64_t word = __builtin_amdgcn_ballot_w64(s);
+      uor |= word;
+      if (lane == 0) s_out[((size_t)t * M + m) * Nw + w] = word;
+    }
   }
   if (v_inout && nv) v_inout[(size_t)m * N + n] = (int32_t)V;
   // partial union over t of this token's word, for a following product

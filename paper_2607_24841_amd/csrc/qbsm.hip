@@ -347,32 +347,21 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   const int theta = ep.theta[col];
   const bool spikes = a.mode != EPI_CUR;
   const bool tr = spikes && seg.transposed;
-  // channel-major output in whole bytes: the row block's tokens fill whole
-  // bytes of the position words, so this workgroup owns them (plain byte
-  // stores); otherwise bits are cleared and set with atomics
-  const bool tr_bytes = tr && (a.Mb & 7) == 0 && a.Mb <= 32 && (seg.pos0 & 7) == 0;
-  const int wbase = tr ? ((seg.pos0 + y * a.Mb) >> 6) : 0;
-  uint64_t tb0[NMDLM_MAX_T], tb1[NMDLM_MAX_T];
+  // channel-major output (row blocks of at most 32 tokens): the waves' token
+  // bits meet in LDS and one wave writes them, in plain byte stores when the
+  // row block's tokens fill whole bytes of the position words (this workgroup
+  // owns them), else by clearing and setting its bits with one pair of
+  // atomics per word
+  const bool tr_bytes = tr && (a.Mb & 7) == 0 && (seg.pos0 & 7) == 0;
   uint32_t vb[NMDLM_MAX_T];
 #pragma unroll
-  for (int t = 0; t < NMDLM_MAX_T; ++t) {
-    tb0[t] = tb1[t] = 0ull;
-    vb[t] = 0u;
-  }
-  uint64_t tm0 = 0ull, tm1 = 0ull;
+  for (int t = 0; t < NMDLM_MAX_T; ++t) vb[t] = 0u;
   uint64_t uor = 0ull;  // union of this wave's output words (wave-uniform)
 
   for (int ml = wave; ml < a.Mb; ml += NW) {
     const int m = y * a.Mb + ml;
     if (m >= a.M) break;
     int V = 0;
-    const int pos = seg.pos0 + m;
-    const int rel = (pos >> 6) - wbase;
-    const uint64_t pbit = 1ull << (pos & 63);
-    if (tr) {
-      if (rel == 0) tm0 |= pbit;
-      else tm1 |= pbit;
-    }
 #pragma unroll
     for (int t = 0; t < NMDLM_MAX_T; ++t) {
       if (t < a.T) {
@@ -397,46 +386,50 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
             uor |= word;
             if (lane == 0) seg.ptr[t * seg.ld_t + (int64_t)m * seg.ld_m + wseg] = word;
           } else if (s) {
-            if (tr_bytes) vb[t] |= 1u << ml;
-            else if (rel == 0) tb0[t] |= pbit;
-            else tb1[t] |= pbit;
+            vb[t] |= 1u << ml;
           }
         }
       }
     }
   }
-  if (tr_bytes) {
-    // the waves' token bits meet in LDS; each column then stores the bytes
-    // that hold at least one token of the block
+  if (tr) {
+    // the waves' token bits meet in LDS; wave 0 then writes each column's
+    // bits of the row block's tokens
 #pragma unroll
     for (int t = 0; t < NMDLM_MAX_T; ++t)
       if (t < a.T && vb[t]) atomicOr(&ep.vbits[t * 64 + col], vb[t]);
     __syncthreads();
     if (wave == 0 && nv) {
       const int ch = n - segi * a.seg_w;
-      const int p0 = seg.pos0 + y * a.Mb;               // multiple of 8
-      const int nb = (min(a.Mb, a.M - y * a.Mb) + 7) >> 3;  // bytes with a token of the block
-      for (int t = 0; t < a.T; ++t) {
-        uint8_t* rowb = reinterpret_cast<uint8_t*>(seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m) + (p0 >> 3);
-        const uint32_t bits = ep.vbits[t * 64 + col];
-        for (int b = 0; b < nb; ++b) rowb[b] = (uint8_t)(bits >> (8 * b));
-      }
-    }
-  } else if (tr && nv) {
-    // channel-major cache: clear this wave's token bits, then set the spikes
-    const int ch = n - segi * a.seg_w;
-#pragma unroll
-    for (int t = 0; t < NMDLM_MAX_T; ++t) {
-      if (t < a.T) {
-        unsigned long long* row = reinterpret_cast<unsigned long long*>(
-            seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + wbase);
-        if (tm0) {
-          atomicAnd(row, ~tm0);
-          if (tb0[t]) atomicOr(row, tb0[t]);
+      const int p0 = seg.pos0 + y * a.Mb;
+      const int nvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the block, <= 32
+      if (tr_bytes) {
+        // p0 is a multiple of 8: store the bytes holding a token of the block
+        const int nb = (nvalid + 7) >> 3;
+        for (int t = 0; t < a.T; ++t) {
+          uint8_t* rowb = reinterpret_cast<uint8_t*>(seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m) + (p0 >> 3);
+          const uint32_t bits = ep.vbits[t * 64 + col];
+          for (int b = 0; b < nb; ++b) rowb[b] = (uint8_t)(bits >> (8 * b));
         }
-        if (tm1) {
-          atomicAnd(row + 1, ~tm1);
-          if (tb1[t]) atomicOr(row + 1, tb1[t]);
+      } else {
+        // the block's bits start at bit off of word p0/64 and may run into
+        // the next word
+        const int off = p0 & 63;
+        const uint64_t full = (nvalid >= 32) ? 0xFFFFFFFFull : ((1ull << nvalid) - 1ull);
+        const uint64_t m0 = full << off;
+        const uint64_t m1 = off ? (full >> (64 - off)) : 0ull;
+        for (int t = 0; t < a.T; ++t) {
+          unsigned long long* row = reinterpret_cast<unsigned long long*>(
+              seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + (p0 >> 6));
+          const uint64_t bits = ep.vbits[t * 64 + col];
+          const uint64_t b0 = bits << off;
+          const uint64_t b1 = off ? (bits >> (64 - off)) : 0ull;
+          atomicAnd(row, ~m0);
+          if (b0) atomicOr(row, b0);
+          if (m1) {
+            atomicAnd(row + 1, ~m1);
+            if (b1) atomicOr(row + 1, b1);
+          }
         }
       }
     }
@@ -453,6 +446,76 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   }
 }
 
+// ------------------------------------------------- weight-skip statistics
+// The statistics of a product are those of the whole block: the number of
+// input rows (channels) active in the union of all its spike rows.  Workgroup
+// (0,0,0) computes them between the barriers the product already has, so they
+// add no round trip at the end of the kernel:
+//   stats_slice  (with the staging loads) this thread's OR over a slice of
+//                the union sources: the producer's partial unions when given,
+//                else the spike rows
+//   stats_merge  (after the first barrier) ORs the slices into sStat
+//   stats_count  (after a later barrier) adds the popcounts into sCnt
+//   stats_write  (after a later barrier) thread 0 stores the record
+template <int NT>
+__device__ __forceinline__ unsigned long long stats_slice(const QbsmArgs& a, int Kw, int tid) {
+  unsigned long long u = 0ull;
+  if (a.dense || NT < Kw) return u;
+  const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
+  if (s0 >= slices) return u;
+  const uint64_t* src = a.upart ? a.upart : a.S;
+  const int nsrc = a.upart ? a.nparts : a.T * a.M;
+  int r = s0;
+  for (; r + 3 * slices < nsrc; r += 4 * slices)
+    u |= src[(size_t)r * Kw + w] | src[(size_t)(r + slices) * Kw + w] |
+         src[(size_t)(r + 2 * slices) * Kw + w] | src[(size_t)(r + 3 * slices) * Kw + w];
+  for (; r < nsrc; r += slices) u |= src[(size_t)r * Kw + w];
+  return u;
+}
+
+template <int NT>
+__device__ __forceinline__ void stats_merge(const QbsmArgs& a, unsigned long long* sStat, int Kw,
+                                            int tid, unsigned long long u) {
+  if (a.dense) return;
+  if (NT >= Kw) {
+    const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
+    if (s0 < slices && u) atomicOr(&sStat[w], u);
+  } else {
+    // more words than threads: each thread ORs every source of its words
+    const uint64_t* src = a.upart ? a.upart : a.S;
+    const int nsrc = a.upart ? a.nparts : a.T * a.M;
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long v = 0ull;
+      for (int r = 0; r < nsrc; ++r) v |= src[(size_t)r * Kw + w];
+      sStat[w] = v;  // the only writer of word w
+    }
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void stats_count(const QbsmArgs& a, const unsigned long long* sStat,
+                                            int* sCnt, int Kw, int tid, int lane) {
+  const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
+  int cnt = 0;
+  if (a.dense) {
+    cnt = tid == 0 ? a.K : 0;
+  } else {
+    for (int w = tid; w < Kw; w += NT) {
+      const unsigned long long u = sStat[w];
+      cnt += __popcll((w == Kw - 1) ? (u & last_mask) : u);
+    }
+  }
+  for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
+  if (lane == 0 && cnt) atomicAdd(sCnt, cnt);
+}
+
+__device__ __forceinline__ void stats_write(const QbsmArgs& a, int total) {
+  a.stats->k_total = a.K;
+  a.stats->k_active = total;
+  a.stats->n = a.N;
+  a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
+}
+
 // ------------------------------------------------- word-granular product
 // k-steps are the original 64-channel words.  The A operand comes straight
 // from the staged spike rows (no list, no compaction).  Within a word, a lane
@@ -467,11 +530,12 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   constexpr int NT = NW * 64;
   __shared__ int sTile[ROWS * kTileLd];
   __shared__ unsigned long long sUn[NW];
-  __shared__ int sRed[NW];
   __shared__ EpiStage ep;
   __shared__ int sLast;
-  // dynamic: local union [Kw] (u64), then the tile's spike rows as dwords
-  // with row stride 2*Kw+1 (odd: the 16 rows a wave reads fall in different banks)
+  __shared__ int sStatCnt;
+  // dynamic: local union [Kw] (u64), the block union of the statistics [Kw]
+  // (u64), then the tile's spike rows as dwords with row stride 2*Kw+1 (odd:
+  // the 16 rows a wave reads fall in different banks)
   extern __shared__ unsigned long long sDyn[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -481,7 +545,9 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   const int Kw = (a.K + 63) >> 6;
   const int lds_row = 2 * Kw + 1;
   unsigned long long* sLU = sDyn;
-  uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + Kw);
+  unsigned long long* sStat = sDyn + Kw;
+  uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + 2 * Kw);
+  const bool stats_wg = a.stats && x == 0 && y == 0 && z == 0;  // workgroup-uniform
 
   const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
   // With the producer's partial unions, the union is their OR over the whole
@@ -491,6 +557,12 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   const bool from_parts = a.upart && !a.dense;
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
   stage_epilogue<NT>(a, ep, tid, x, y);
+  unsigned long long spart = 0ull;
+  if (stats_wg) {
+    for (int w = tid; w < Kw; w += NT) sStat[w] = 0ull;
+    if (tid == 0) sStatCnt = 0;
+    spart = stats_slice<NT>(a, Kw, tid);
+  }
   for (int i = tid; i < ROWS * Kw; i += NT) {
     const int lr = i / Kw, w = i - lr * Kw;
     const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
@@ -510,6 +582,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     }
   }
   __syncthreads();
+  if (stats_wg) stats_merge<NT>(a, sStat, Kw, tid, spart);
   if (!from_parts) {
     for (int w = tid; w < Kw; w += NT) {
       unsigned long long u = ~0ull;
@@ -594,49 +667,11 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
 
   __syncthreads();
   reduce_tile<RT>(acc, sTile, g, c);
+  if (stats_wg) stats_count<NT>(a, sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
+  if (stats_wg && tid == 0) stats_write(a, sStatCnt);
   const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
   if (last) epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
-
-  // statistics of the whole block (the block union), by one workgroup: each
-  // thread ORs a slice of the sources of one word, then one LDS OR per thread
-  if (a.stats && x == 0 && y == 0 && z == 0) {
-    __syncthreads();
-    for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
-    __syncthreads();
-    const int nsrc = a.dense ? 0 : (a.upart ? a.nparts : a.T * a.M);
-    const int slices = NT >= Kw ? NT / Kw : 1;
-    const int s0 = NT >= Kw ? tid / Kw : 0;
-    if (s0 < slices) {
-      for (int w = NT >= Kw ? tid % Kw : tid; w < Kw; w += (NT >= Kw ? Kw : NT)) {
-        unsigned long long u = 0ull;
-        if (a.upart) {
-          for (int q = s0; q < nsrc; q += slices) u |= a.upart[(size_t)q * Kw + w];
-        } else {
-          for (int r = s0; r < nsrc; r += slices) u |= a.S[(size_t)r * Kw + w];
-        }
-        if (u) atomicOr(&sLU[w], u);
-        if (NT >= Kw) break;
-      }
-    }
-    __syncthreads();
-    int cnt = 0;
-    for (int w = tid; w < Kw; w += NT) {
-      const unsigned long long u = a.dense ? ~0ull : sLU[w];
-      cnt += __popcll((w == Kw - 1) ? (u & last_mask) : u);
-    }
-    for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
-    if (lane == 0) sRed[wave] = cnt;
-    __syncthreads();
-    if (tid == 0) {
-      int total = 0;
-      for (int i = 0; i < NW; ++i) total += sRed[i];
-      a.stats->k_total = a.K;
-      a.stats->k_active = total;
-      a.stats->n = a.N;
-      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
-    }
-  }
 }
 
 // ------------------------------------------------- LDS-streamed product
@@ -668,12 +703,13 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_dma(QbsmArgs a) {
   constexpr int kNoRow = 0x7fffffff;
   __shared__ int sTile[ROWS * kTileLd];
   __shared__ unsigned long long sUn[NW];
-  __shared__ int sRed[NW];
   __shared__ EpiStage ep;
   __shared__ int sLast;
   __shared__ int sFirst;
-  // dynamic: ring [NW][D][kDmaSlot] bytes, local union [Kw] (u64), the
-  // block's spike rows as dwords with row stride 2*Kw+1
+  __shared__ int sStatCnt;
+  // dynamic: ring [NW][D][kDmaSlot] bytes, local union [Kw] (u64), the block
+  // union of the statistics [Kw] (u64), the block's spike rows as dwords with
+  // row stride 2*Kw+1
   extern __shared__ __attribute__((aligned(16))) unsigned char sRaw[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -684,11 +720,19 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_dma(QbsmArgs a) {
   const int lds_row = 2 * Kw + 1;
   unsigned char* ring = sRaw + (size_t)wave * D * kDmaSlot;
   unsigned long long* sLU = reinterpret_cast<unsigned long long*>(sRaw + (size_t)NW * D * kDmaSlot);
-  uint32_t* sS = reinterpret_cast<uint32_t*>(sLU + Kw);
+  unsigned long long* sStat = sLU + Kw;
+  uint32_t* sS = reinterpret_cast<uint32_t*>(sStat + Kw);
+  const bool stats_wg = a.stats && x == 0 && y == 0 && z == 0;  // workgroup-uniform
 
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
   if (tid == 0) sFirst = kNoRow;
   stage_epilogue<NT>(a, ep, tid, x, y);
+  unsigned long long spart = 0ull;
+  if (stats_wg) {
+    for (int w = tid; w < Kw; w += NT) sStat[w] = 0ull;
+    if (tid == 0) sStatCnt = 0;
+    spart = stats_slice<NT>(a, Kw, tid);
+  }
   for (int i = tid; i < ROWS * Kw; i += NT) {
     const int lr = i / Kw, w = i - lr * Kw;
     const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
@@ -697,6 +741,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_dma(QbsmArgs a) {
     sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
   }
   __syncthreads();
+  if (stats_wg) stats_merge<NT>(a, sStat, Kw, tid, spart);
   const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
   for (int w = tid; w < Kw; w += NT) {
     unsigned long long u = ~0ull;
@@ -777,47 +822,11 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_dma(QbsmArgs a) {
 
   __syncthreads();
   reduce_tile<RT>(acc, sTile, g, c);
+  if (stats_wg) stats_count<NT>(a, sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
+  if (stats_wg && tid == 0) stats_write(a, sStatCnt);
   const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
   if (last) epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
-
-  if (a.stats && x == 0 && y == 0 && z == 0) {
-    __syncthreads();
-    for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
-    __syncthreads();
-    const int nsrc = a.dense ? 0 : (a.upart ? a.nparts : a.T * a.M);
-    const int slices = NT >= Kw ? NT / Kw : 1;
-    const int s0 = NT >= Kw ? tid / Kw : 0;
-    if (s0 < slices) {
-      for (int w = NT >= Kw ? tid % Kw : tid; w < Kw; w += (NT >= Kw ? Kw : NT)) {
-        unsigned long long u = 0ull;
-        if (a.upart) {
-          for (int q = s0; q < nsrc; q += slices) u |= a.upart[(size_t)q * Kw + w];
-        } else {
-          for (int r = s0; r < nsrc; r += slices) u |= a.S[(size_t)r * Kw + w];
-        }
-        if (u) atomicOr(&sLU[w], u);
-        if (NT >= Kw) break;
-      }
-    }
-    __syncthreads();
-    int cnt = 0;
-    for (int w = tid; w < Kw; w += NT) {
-      const unsigned long long u = a.dense ? ~0ull : sLU[w];
-      cnt += __popcll((w == Kw - 1) ? (u & last_mask) : u);
-    }
-    for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
-    if (lane == 0) sRed[wave] = cnt;
-    __syncthreads();
-    if (tid == 0) {
-      int total = 0;
-      for (int i = 0; i < NW; ++i) total += sRed[i];
-      a.stats->k_total = a.K;
-      a.stats->k_active = total;
-      a.stats->n = a.N;
-      a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
-    }
-  }
 }
 
 // -------------------------------------------------------------- single kernel
@@ -1180,7 +1189,7 @@ static nmdlm_status launch_dma(const dim3& grid, const QbsmArgs& a, size_t dyn, 
 // Static LDS of k_qbsm_dma (mirrors its declarations) and its dynamic part.
 static size_t dma_lds(int RT, int NW, int D, int Kw) {
   return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
-         (size_t)NW * D * kDmaSlot + (size_t)Kw * 8 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
+         (size_t)NW * D * kDmaSlot + (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
 }
 constexpr size_t kDmaLdsMax = 163840;  // LDS per workgroup on the device
 
@@ -1193,7 +1202,7 @@ static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st, hip
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
 static size_t words_lds(int RT, int NW, int Kw) {
   return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
-         (size_t)Kw * 8 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
+         (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
 }
 
 // Static LDS of k_qbsm_fused<RT, NW> (mirrors its declarations).
@@ -1256,7 +1265,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     }
   }
   while (RT > 1 && 16 * RT / 2 >= R && 16 * RT / 2 >= c.T) RT >>= 1;  // no empty tiles
-  while (has_tr && RT > 1 && (16 * RT) / c.T > 64) RT >>= 1;
+  while (has_tr && RT > 1 && (16 * RT) / c.T > 32) RT >>= 1;  // channel-major: <= 32 tokens
   if (path == 0) {
     path = 3;
     while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
@@ -1299,7 +1308,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     // 8 waves, not 16: a 1024-thread bound caps registers at 128 and spills
     NW = words_waves(RT, ks_per_wg);
     if (words_lds(RT, NW, Kw) > kWordsLdsBudget) NW = 4;
-    dyn = (size_t)Kw * 8 + (size_t)16 * RT * (2 * Kw + 1) * 4;
+    dyn = (size_t)Kw * 16 + (size_t)16 * RT * (2 * Kw + 1) * 4;
   } else if (path == 2) {
     // one kernel (union, list and spike compaction in LDS) when the tile's
     // spike rows fit; else the prep pass builds them in global memory

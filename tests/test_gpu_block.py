@@ -71,6 +71,15 @@ def test_block_small_shapes():
     _check_block(case, flags=1)
 
 
+@pytest.mark.parametrize("C,M,flags", [(62, 7, 0), (62, 7, 2 << 16), (50, 20, 8 << 16)])
+def test_block_cache_word_straddle(C, M, flags):
+    # row blocks of 4 (default), 8 and 32 tokens (T = 4) whose positions cross
+    # the boundary between two words of the channel-major value cache and do
+    # not fill whole bytes of it
+    need_gpu()
+    _check_block(synth.block_case(seed=11, C=C, M=M, d=128, H=2, F=256), flags)
+
+
 def test_block_full_size():
     need_gpu()
     _check_block(synth.block_case())
