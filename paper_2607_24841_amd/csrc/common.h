@@ -12,6 +12,31 @@ namespace nmdlm {
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+// floor(i / d) for 0 <= i, 1 <= d and i + d < 2^22, from inv_d = 1.0f / d.
+// The quotient of i + 0.5 lies at least 0.5 / d from any integer, and the
+// float rounding errors stay below that in this range, so the truncation is
+// exact; it costs a conversion and a multiply instead of an integer division.
+__device__ __forceinline__ int div_small(int i, float inv_d) {
+  return (int)(((float)i + 0.5f) * inv_d);
+}
+
+// Kernel arguments are read through the scalar cache, and the compiler
+// fetches each field just before its first use, so an argument block that
+// spans several 64-byte lines costs one dependent round trip per line.
+// Reading one dword of every line at entry (all loads issued, then one
+// wait) brings the lines in together; later field reads hit the cache.
+template <size_t Bytes>
+__device__ __forceinline__ void touch_kernargs() {
+  typedef const __attribute__((address_space(4))) uint32_t KargWord;
+  KargWord* k = (KargWord*)__builtin_amdgcn_kernarg_segment_ptr();
+  constexpr int kLines = (int)((Bytes + 63) / 64);
+  uint32_t v[kLines];
+#pragma unroll
+  for (int i = 0; i < kLines; ++i) v[i] = k[i * 16];
+#pragma unroll
+  for (int i = 0; i < kLines; ++i) asm volatile("" ::"s"(v[i]));
+}
+
 constexpr int kXcds = 8;  // accelerator dies; each has its own L2
 
 // Workgroups are dispatched round-robin over the XCDs (dispatch id d runs on

@@ -214,6 +214,8 @@ constexpr int kGroup = 2;
 constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
 constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
+constexpr int kUpLoads = 4;             // partial-union loads per thread staged in registers
+constexpr int kRowLoads = 4;            // spike-row words per thread staged in registers
 static_assert(kMaxEpiTokens >= 8 * 16, "every tile's residual words are staged (RT <= 8)");
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
@@ -255,26 +257,60 @@ struct EpiStage {
   uint32_t vbits[NMDLM_MAX_T * 64];         // channel-major output: token bits per (t, column)
 };
 
+// The epilogue operands one thread stages (at most one of each kind per
+// thread: 64 columns, T * Mb <= kMaxEpiTokens residual words, 256 table
+// bytes), loaded into registers first so that the staging loads of a kernel
+// are all in flight together.  The loads take clamped (valid) addresses and
+// no per-lane condition; the conditions are applied when the values are
+// stored, so that no load is waited for before the last one is issued.
+struct EpiRegs {
+  int bias, theta_ch, theta_seg;
+  unsigned long long resid;
+  int lut;
+};
+
+template <int NT>
+__device__ __forceinline__ EpiRegs epi_load(const QbsmArgs& a, int tid, int x, int y) {
+  static_assert(NT >= 256 && NT >= kMaxEpiTokens, "one staged item of each kind per thread");
+  EpiRegs r{0, 0, 0, 0ull, 0};
+  // each kind is loaded by the waves that hold one of its items (a
+  // wave-uniform test), every lane of such a wave at a valid address
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nc = min(x * 64 + (tid & 63), a.N - 1);
+  if (wv == 0) {
+    if (a.bias) r.bias = a.bias[nc];
+    if (a.theta_vec) r.theta_ch = a.theta_vec[nc];
+  }
+  if (a.mode == EPI_IF || a.mode == EPI_QNL_IF) r.theta_seg = a.seg[(x * 64) / a.seg_w].theta;
+  if (a.resid && wv * 64 < a.T * a.Mb) {  // T * Mb <= 16 * RT <= kMaxEpiTokens
+    const int i = min(tid, a.T * a.Mb - 1);
+    const int t = div_small(i, 1.0f / (float)a.Mb), m = min(y * a.Mb + (i - t * a.Mb), a.M - 1);
+    r.resid = a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x];
+  }
+  if (a.mode == EPI_QNL_IF && wv < 4) r.lut = (int)(signed char)a.lut[tid & 255];
+  return r;
+}
+
+template <int NT>
+__device__ __forceinline__ void epi_store(const QbsmArgs& a, EpiStage& ep, const EpiRegs& r, int tid,
+                                          int x, int y) {
+  if (tid < 64) {
+    const bool nv = x * 64 + tid < a.N;
+    ep.bias[tid] = nv ? r.bias : 0;
+    // firing threshold of each column: per channel, else the segment's
+    ep.theta[tid] = a.theta_vec ? (nv ? r.theta_ch : 1) : r.theta_seg;
+  }
+  if (a.resid && tid < a.T * a.Mb) {
+    const int t = div_small(tid, 1.0f / (float)a.Mb), m = y * a.Mb + (tid - t * a.Mb);
+    ep.resid[tid] = m < a.M ? r.resid : 0ull;
+  }
+  if (a.mode == EPI_QNL_IF && tid < 256) ep.lut[tid] = (signed char)r.lut;
+  for (int i = tid; i < NMDLM_MAX_T * 64; i += NT) ep.vbits[i] = 0u;
+}
+
 template <int NT>
 __device__ __forceinline__ void stage_epilogue(const QbsmArgs& a, EpiStage& ep, int tid, int x, int y) {
-  const int n = x * 64 + tid;
-  if (tid < 64) {
-    ep.bias[tid] = (a.bias && n < a.N) ? a.bias[n] : 0;
-    // firing threshold of each column: per channel, else the segment's
-    int th = 0;
-    if (a.theta_vec) th = n < a.N ? a.theta_vec[n] : 1;
-    else if (a.mode == EPI_IF || a.mode == EPI_QNL_IF) th = a.seg[(x * 64) / a.seg_w].theta;
-    ep.theta[tid] = th;
-  }
-  if (a.resid) {
-    for (int i = tid; i < a.T * a.Mb && i < kMaxEpiTokens; i += NT) {
-      const int t = i / a.Mb, m = y * a.Mb + (i - t * a.Mb);
-      ep.resid[i] = m < a.M ? a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x] : 0ull;
-    }
-  }
-  if (a.mode == EPI_QNL_IF)
-    for (int i = tid; i < 256; i += NT) ep.lut[i] = (signed char)a.lut[i];
-  for (int i = tid; i < NMDLM_MAX_T * 64; i += NT) ep.vbits[i] = 0u;
+  epi_store<NT>(a, ep, epi_load<NT>(a, tid, x, y), tid, x, y);
 }
 
 // Sum the waves' accumulators into the LDS tile (physical column order).
@@ -453,18 +489,21 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
 // add no round trip at the end of the kernel:
 //   stats_slice  (with the staging loads) this thread's OR over a slice of
 //                the union sources: the producer's partial unions when given,
-//                else the spike rows
+//                else the spike rows (a product whose own union already is
+//                the block union counts that instead)
 //   stats_merge  (after the first barrier) ORs the slices into sStat
 //   stats_count  (after a later barrier) adds the popcounts into sCnt
 //   stats_write  (after a later barrier) thread 0 stores the record
+// OR of src[r][w] (r < nsrc, row stride Kw) over a slice of the rows: with
+// NT >= Kw, thread tid takes word tid % Kw and rows tid / Kw, + NT / Kw, ...,
+// so that few loads per thread are all in flight together.
 template <int NT>
-__device__ __forceinline__ unsigned long long stats_slice(const QbsmArgs& a, int Kw, int tid) {
+__device__ __forceinline__ unsigned long long or_slice(const uint64_t* src, int nsrc, int Kw,
+                                                       int tid) {
   unsigned long long u = 0ull;
-  if (a.dense || NT < Kw) return u;
+  if (NT < Kw) return u;
   const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
   if (s0 >= slices) return u;
-  const uint64_t* src = a.upart ? a.upart : a.S;
-  const int nsrc = a.upart ? a.nparts : a.T * a.M;
   int r = s0;
   for (; r + 3 * slices < nsrc; r += 4 * slices)
     u |= src[(size_t)r * Kw + w] | src[(size_t)(r + slices) * Kw + w] |
@@ -473,23 +512,38 @@ __device__ __forceinline__ unsigned long long stats_slice(const QbsmArgs& a, int
   return u;
 }
 
+// dst[w] = OR of the slices (dst cleared before the barrier that precedes
+// this call); bits of the last word past K are dropped with last_mask.
+template <int NT>
+__device__ __forceinline__ void or_merge(unsigned long long* dst, const uint64_t* src, int nsrc,
+                                         int Kw, int tid, unsigned long long u,
+                                         unsigned long long last_mask) {
+  if (NT >= Kw) {
+    const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
+    if (w == Kw - 1) u &= last_mask;
+    if (s0 < slices && u) atomicOr(&dst[w], u);
+  } else {
+    // more words than threads: each thread ORs every source of its words
+    for (int w = tid; w < Kw; w += NT) {
+      unsigned long long v = 0ull;
+      for (int r = 0; r < nsrc; ++r) v |= src[(size_t)r * Kw + w];
+      dst[w] = (w == Kw - 1) ? (v & last_mask) : v;  // the only writer of word w
+    }
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ unsigned long long stats_slice(const QbsmArgs& a, int Kw, int tid) {
+  if (a.dense) return 0ull;
+  return a.upart ? or_slice<NT>(a.upart, a.nparts, Kw, tid) : or_slice<NT>(a.S, a.T * a.M, Kw, tid);
+}
+
 template <int NT>
 __device__ __forceinline__ void stats_merge(const QbsmArgs& a, unsigned long long* sStat, int Kw,
                                             int tid, unsigned long long u) {
   if (a.dense) return;
-  if (NT >= Kw) {
-    const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
-    if (s0 < slices && u) atomicOr(&sStat[w], u);
-  } else {
-    // more words than threads: each thread ORs every source of its words
-    const uint64_t* src = a.upart ? a.upart : a.S;
-    const int nsrc = a.upart ? a.nparts : a.T * a.M;
-    for (int w = tid; w < Kw; w += NT) {
-      unsigned long long v = 0ull;
-      for (int r = 0; r < nsrc; ++r) v |= src[(size_t)r * Kw + w];
-      sStat[w] = v;  // the only writer of word w
-    }
-  }
+  if (a.upart) or_merge<NT>(sStat, a.upart, a.nparts, Kw, tid, u, ~0ull);
+  else or_merge<NT>(sStat, a.S, a.T * a.M, Kw, tid, u, ~0ull);
 }
 
 template <int NT>
@@ -538,6 +592,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   // the 16 rows a wave reads fall in different banks)
   extern __shared__ unsigned long long sDyn[];
 
+  touch_kernargs<sizeof(QbsmArgs)>();
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   int x, y, z;
@@ -552,38 +607,90 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
   // With the producer's partial unions, the union is their OR over the whole
   // block (a superset of this row block's own union: the extra rows meet zero
-  // spikes), and its loads go out with the staging loads; otherwise it is the
-  // OR of the staged rows.
+  // spikes): each thread ORs a slice of them with the staging loads, and the
+  // slices meet in LDS after the first barrier.  Otherwise it is the OR of
+  // the staged rows.  Either way a second barrier publishes it.
   const bool from_parts = a.upart && !a.dense;
-  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
-  stage_epilogue<NT>(a, ep, tid, x, y);
-  unsigned long long spart = 0ull;
-  if (stats_wg) {
-    for (int w = tid; w < Kw; w += NT) sStat[w] = 0ull;
-    if (tid == 0) sStatCnt = 0;
-    spart = stats_slice<NT>(a, Kw, tid);
+  const bool stats_rows = stats_wg && !from_parts && !a.dense;  // block union from the rows
+
+  // ---- staging, load phase: every load goes out before the first is used
+  const EpiRegs er = epi_load<NT>(a, tid, x, y);
+  // thread tid takes word wq = tid % Kw and rows r0 = tid / Kw, + rpp, ...
+  // (rpp = NT / Kw rows per pass; none when the words outnumber the threads)
+  const float inv_kw = 1.0f / (float)Kw, inv_mb = 1.0f / (float)a.Mb;
+  const int r0 = div_small(tid, inv_kw), wq = tid - r0 * Kw;
+  const int rpp = div_small(NT, inv_kw);
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr0 = __builtin_amdgcn_readfirstlane(r0);  // first row of this wave's lanes
+  // partial unions: part s = r0 + k * rpp of word wq
+  const int slices = rpp;
+  const int s0 = r0;
+  const bool up_regs = from_parts && slices > 0 && a.nparts > 0 && a.nparts <= kUpLoads * slices;
+  unsigned long long upv[kUpLoads];
+#pragma unroll
+  for (int k = 0; k < kUpLoads; ++k) {
+    upv[k] = 0ull;
+    // waves with a part to load (uniform); other lanes load a valid word
+    if (up_regs && wr0 + k * slices < a.nparts)
+      upv[k] = a.upart[(size_t)min(s0 + k * slices, a.nparts - 1) * Kw + wq];
   }
-  for (int i = tid; i < ROWS * Kw; i += NT) {
+  // this row block's spike rows: tile row lr = r0 + k * rpp, word wq; rows
+  // past the tile or the block load a valid word and drop it
+  unsigned long long rv[kRowLoads];
+  int rdst[kRowLoads];  // dword offset of the item in sS, or -1
+  uint32_t keep = 0u;   // bit k: item k lies in the block (else it is stored as zero)
+#pragma unroll
+  for (int k = 0; k < kRowLoads; ++k) {
+    const int lr = r0 + k * rpp;
+    rdst[k] = -1;
+    rv[k] = 0ull;
+    if (wr0 < rpp && wr0 + k * rpp < ROWS) {  // wave-uniform
+      const int lc = min(lr, ROWS - 1);
+      const int t = div_small(lc, inv_mb), m = y * a.Mb + (lc - t * a.Mb);
+      rv[k] = a.S[(size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + wq];
+      rdst[k] = (r0 < rpp && lr < ROWS) ? lr * lds_row + 2 * wq : -1;
+      keep |= (uint32_t)(t < a.T && m < a.M) << k;
+    }
+  }
+  // many partial unions (or more words than threads): OR loops
+  unsigned long long upart_or = 0ull;
+  if (from_parts && !up_regs) upart_or = or_slice<NT>(a.upart, a.nparts, Kw, tid);
+  unsigned long long spart = 0ull;
+  if (stats_rows) spart = or_slice<NT>(a.S, a.T * a.M, Kw, tid);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- staging, store phase
+  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  epi_store<NT>(a, ep, er, tid, x, y);
+  if (from_parts)
+    for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
+  if (stats_wg && tid == 0) sStatCnt = 0;
+  if (stats_rows)
+    for (int w = tid; w < Kw; w += NT) sStat[w] = 0ull;
+#pragma unroll
+  for (int k = 0; k < kRowLoads; ++k)
+    if (rdst[k] >= 0) {
+      const unsigned long long v = ((keep >> k) & 1u) ? rv[k] : 0ull;
+      sS[rdst[k]] = (uint32_t)v;
+      sS[rdst[k] + 1] = (uint32_t)(v >> 32);
+    }
+  // rows past kRowLoads passes (all rows when the words outnumber the threads)
+  for (int i = tid + kRowLoads * rpp * Kw; i < ROWS * Kw; i += NT) {
     const int lr = i / Kw, w = i - lr * Kw;
     const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
     const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
     sS[lr * lds_row + 2 * w] = (uint32_t)v;
     sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
   }
-  if (from_parts) {
-    for (int w = tid; w < Kw; w += NT) {
-      unsigned long long u = 0ull;
-      int q = 0;
-      for (; q + 4 <= a.nparts; q += 4)
-        u |= a.upart[(size_t)q * Kw + w] | a.upart[(size_t)(q + 1) * Kw + w] |
-             a.upart[(size_t)(q + 2) * Kw + w] | a.upart[(size_t)(q + 3) * Kw + w];
-      for (; q < a.nparts; ++q) u |= a.upart[(size_t)q * Kw + w];
-      sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
-    }
+  if (up_regs && s0 < slices) {
+#pragma unroll
+    for (int k = 0; k < kUpLoads; ++k)
+      if (s0 + k * slices < a.nparts) upart_or |= upv[k];
   }
   __syncthreads();
-  if (stats_wg) stats_merge<NT>(a, sStat, Kw, tid, spart);
-  if (!from_parts) {
+  if (from_parts) {
+    or_merge<NT>(sLU, a.upart, a.nparts, Kw, tid, upart_or, last_mask);
+  } else {
     for (int w = tid; w < Kw; w += NT) {
       unsigned long long u = ~0ull;
       if (!a.dense) {
@@ -594,8 +701,9 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       }
       sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
     }
-    __syncthreads();
   }
+  if (stats_rows) or_merge<NT>(sStat, a.S, a.T * a.M, Kw, tid, spart, ~0ull);
+  __syncthreads();
   // first active row (the target of the loads of inactive rows), per wave
   int first = 0x7fffffff;
   for (int w = lane; w < Kw; w += kWave) {
@@ -667,7 +775,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
 
   __syncthreads();
   reduce_tile<RT>(acc, sTile, g, c);
-  if (stats_wg) stats_count<NT>(a, sStat, &sStatCnt, Kw, tid, lane);
+  if (stats_wg) stats_count<NT>(a, from_parts ? sLU : sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
   if (stats_wg && tid == 0) stats_write(a, sStatCnt);
   const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
