@@ -214,8 +214,8 @@ constexpr int kGroup = 2;
 constexpr int kFusedMaxWords = 256;     // K <= 16384 for the single-kernel product
 constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product kernel
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
-constexpr int kUpLoads = 4;             // partial-union loads per thread staged in registers
-constexpr int kRowLoads = 4;            // spike-row words per thread staged in registers
+constexpr int kUpLoads = 2;             // partial-union loads per thread staged in registers
+constexpr int kRowLoads = 2;            // spike-row words per thread staged in registers
 static_assert(kMaxEpiTokens >= 8 * 16, "every tile's residual words are staged (RT <= 8)");
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
