@@ -162,8 +162,9 @@ nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode,
  *
  *   q         device spikes [T][M][d/64], d = H*dh
  *   k_cache   device spikes [T][cache_cap][d/64]  (token-major)
- *   vt_cache  device spikes, channel-major: [T][d][cache_cap/64], bit j%64
- *             of word j/64 of row (t, c) is V[t,j,c]
+ *   vt_cache  device spikes, word-major: [T][cache_cap/64][d]; bit j%64 of
+ *             word (t, j/64, c) is V[t,j,c] (the 64 positions of one word
+ *             for every channel lie side by side)
  *   cache_cap multiple of 64, >= C+M
  *   dh        64 or 128 (else NMDLM_ERR_UNSUPPORTED): scores stay within
  *             the 256-entry table
@@ -212,7 +213,8 @@ typedef struct nmdlm_layer {
   const uint8_t* lut_att;/* device [256] attention score table */
   const uint8_t* lut_act;/* device [256] activation table (int8 bytes) */
   uint64_t* k_cache;     /* device [T][cache_cap][d/64]      */
-  uint64_t* vt_cache;    /* device [T][d][cache_cap/64]      */
+  uint64_t* vt_cache;    /* device [T][cache_cap/64][d]: bit j%64 of word
+                            (t, j/64, c) is value channel c of position j */
 } nmdlm_layer;
 
 typedef struct nmdlm_model {

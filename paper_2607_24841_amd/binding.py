@@ -249,7 +249,7 @@ class DeviceLayer:
         self.lut_att = _dev(L.lut_att, device)
         self.lut_act = _dev(L.lut_act, device)
         self.k_cache = torch.zeros((T, cache_cap, d // 64), dtype=torch.int64, device=device)
-        self.vt_cache = torch.zeros((T, d, cache_cap // 64), dtype=torch.int64, device=device)
+        self.vt_cache = torch.zeros((T, cache_cap // 64, d), dtype=torch.int64, device=device)  # word-major
         th = L.theta
         self.c = Layer(ptr(self.w_qkv), ptr(self.w_o), ptr(self.w_up), ptr(self.w_dn),
                        th["q"], th["k"], th["v"], th["a"], th["o"], th["up"], th["dn"], L.s_up,

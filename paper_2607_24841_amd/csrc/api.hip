@@ -86,7 +86,7 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
     c.seg[i].theta = theta;
     c.seg[i].transposed = 0;
     c.seg[i].pos0 = 0;
-    c.seg[i].pad_ = 0;
+    c.seg[i].ld_p = 0;
   }
   c.resid = nullptr;
   c.rld_t = c.rld_m = 0;

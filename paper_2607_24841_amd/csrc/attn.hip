@@ -94,7 +94,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
     }
     uint64_t vw[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) vw[nt] = vt[((size_t)t * d + h * DH + nt * 16 + c) * capw + jc];
+    for (int nt = 0; nt < NT; ++nt) vw[nt] = vt[((size_t)t * capw + jc) * d + h * DH + nt * 16 + c];
     __builtin_amdgcn_sched_barrier(0);  // every load above is issued before the first use
     uint32_t pk[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -195,7 +195,7 @@ __device__ __forceinline__ void load_chunk(KvChunk<DHW>& ch, const uint64_t* __r
 #pragma unroll
   for (int w = 0; w < DHW; ++w) {
     ch.kw[w] = kr[w];
-    ch.vw[w] = vt[((size_t)t * d + h * DH + w * 64 + lane) * capw + jc];
+    ch.vw[w] = vt[((size_t)t * capw + jc) * d + h * DH + w * 64 + lane];
   }
 }
 

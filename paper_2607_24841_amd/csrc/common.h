@@ -76,8 +76,9 @@ enum EpiMode : int {
 
 // Destination of the spikes of one column segment of a product.
 //   natural    : word (t, m, w) at ptr[t*ld_t + m*ld_m + w]
-//   transposed : channel-major cache, bit (pos0+m)%64 of word (pos0+m)/64 of
-//                row ptr + t*ld_t + ch*ld_m  (ld_m = words per channel row)
+//   transposed : position-packed cache: bit (pos0+m)%64 of the word
+//                ptr[t*ld_t + ch*ld_m + ((pos0+m)/64)*ld_p] holds channel ch
+//                of token m (word-major caches: ld_m = 1, ld_p = channels)
 struct SpikeSeg {
   uint64_t* ptr;
   int64_t ld_t;
@@ -85,7 +86,7 @@ struct SpikeSeg {
   int32_t theta;
   int32_t transposed;
   int32_t pos0;
-  int32_t pad_;
+  int32_t ld_p;
 };
 
 struct QbsmArgs {

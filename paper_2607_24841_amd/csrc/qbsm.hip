@@ -440,12 +440,17 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
       const int p0 = seg.pos0 + y * a.Mb;
       const int nvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the block, <= 32
       if (tr_bytes) {
-        // p0 is a multiple of 8: store the bytes holding a token of the block
+        // p0 is a multiple of 8: store the (up to 4) bytes holding a token of
+        // the block; they may straddle two position words
         const int nb = (nvalid + 7) >> 3;
         for (int t = 0; t < a.T; ++t) {
-          uint8_t* rowb = reinterpret_cast<uint8_t*>(seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m) + (p0 >> 3);
           const uint32_t bits = ep.vbits[t * 64 + col];
-          for (int b = 0; b < nb; ++b) rowb[b] = (uint8_t)(bits >> (8 * b));
+          uint64_t* base = seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m;
+          for (int b = 0; b < nb; ++b) {
+            const int pb = (p0 >> 3) + b;  // byte index along the positions
+            uint8_t* wb = reinterpret_cast<uint8_t*>(base + (int64_t)(pb >> 3) * seg.ld_p);
+            wb[pb & 7] = (uint8_t)(bits >> (8 * b));
+          }
         }
       } else {
         // the block's bits start at bit off of word p0/64 and may run into
@@ -456,15 +461,15 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
         const uint64_t m1 = off ? (full >> (64 - off)) : 0ull;
         for (int t = 0; t < a.T; ++t) {
           unsigned long long* row = reinterpret_cast<unsigned long long*>(
-              seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + (p0 >> 6));
+              seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + (int64_t)(p0 >> 6) * seg.ld_p);
           const uint64_t bits = ep.vbits[t * 64 + col];
           const uint64_t b0 = bits << off;
           const uint64_t b1 = off ? (bits >> (64 - off)) : 0ull;
           atomicAnd(row, ~m0);
           if (b0) atomicOr(row, b0);
           if (m1) {
-            atomicAnd(row + 1, ~m1);
-            if (b1) atomicOr(row + 1, b1);
+            atomicAnd(row + seg.ld_p, ~m1);
+            if (b1) atomicOr(row + seg.ld_p, b1);
           }
         }
       }

@@ -231,7 +231,7 @@ static SpikeSeg natural_seg(uint64_t* p, int64_t ld_t, int64_t ld_m, int32_t the
   s.theta = theta;
   s.transposed = 0;
   s.pos0 = 0;
-  s.pad_ = 0;
+  s.ld_p = 0;
   return s;
 }
 
@@ -316,8 +316,11 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     qkv.seg_w = d;
     qkv.seg[0] = natural_seg(b.Q, sp_t, dw, ly.theta_q);
     qkv.seg[1] = natural_seg(ly.k_cache + (int64_t)C * dw, cap * dw, dw, ly.theta_k);
-    qkv.seg[2] = natural_seg(ly.vt_cache, (int64_t)d * capw, capw, ly.theta_v);
+    // value cache word-major [T][cap/64][d]: position word p of channel ch
+    // at (t * capw + p) * d + ch
+    qkv.seg[2] = natural_seg(ly.vt_cache, (int64_t)d * capw, 1, ly.theta_v);
     qkv.seg[2].transposed = 1;
+    qkv.seg[2].ld_p = d;
     qkv.seg[2].pos0 = C;
     qkv.u_in = uX;
     qkv.u_nparts = uX_parts;

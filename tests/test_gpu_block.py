@@ -18,8 +18,8 @@ def _caches_to_host(dm, T, d, J):
     ks, vs = [], []
     for l in dm.layers:
         ks.append(synth.unpack_bits(B.from_dev_bits(l.k_cache), d)[:, :J])
-        vt = synth.unpack_bits(B.from_dev_bits(l.vt_cache), dm.cache_cap)   # [T][d][cap]
-        vs.append(vt.transpose(0, 2, 1)[:, :J])
+        words = np.ascontiguousarray(B.from_dev_bits(l.vt_cache).transpose(0, 2, 1))  # [T][d][cap/64]
+        vs.append(synth.unpack_bits(words, dm.cache_cap).transpose(0, 2, 1)[:, :J])
     return ks, vs
 
 
@@ -71,11 +71,13 @@ def test_block_small_shapes():
     _check_block(case, flags=1)
 
 
-@pytest.mark.parametrize("C,M,flags", [(62, 7, 0), (62, 7, 2 << 16), (50, 20, 8 << 16)])
+@pytest.mark.parametrize("C,M,flags", [(62, 7, 0), (62, 7, 2 << 16), (50, 20, 8 << 16),
+                                        (56, 16, 4 << 16)])
 def test_block_cache_word_straddle(C, M, flags):
     # row blocks of 4 (default), 8 and 32 tokens (T = 4) whose positions cross
-    # the boundary between two words of the channel-major value cache and do
-    # not fill whole bytes of it
+    # the boundary between two position words of the value cache and do not
+    # fill whole bytes of it; and 16-token row blocks at position 56, written
+    # in whole bytes that straddle two position words
     need_gpu()
     _check_block(synth.block_case(seed=11, C=C, M=M, d=128, H=2, F=256), flags)
 

@@ -125,7 +125,8 @@ def test_mdlm12_step_matches_stored_oracle(flags):
     J = C + M
     for l, layer in enumerate(dm.layers):
         kd = _sha(B.from_dev_bits(layer.k_cache)[:, :J])
-        vt = synth.unpack_bits(B.from_dev_bits(layer.vt_cache), dm.cache_cap)
+        words = np.ascontiguousarray(B.from_dev_bits(layer.vt_cache).transpose(0, 2, 1))  # [T][d][cap/64]
+        vt = synth.unpack_bits(words, dm.cache_cap)
         vd = _sha(synth.pack_bits(vt.transpose(0, 2, 1)[:, :J]))
         assert kd == ref["k_cache_sha256"][l], f"K cache layer {l}"
         assert vd == ref["v_cache_sha256"][l], f"V cache layer {l}"

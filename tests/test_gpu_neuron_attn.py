@@ -97,12 +97,19 @@ def _attn_case(seed, T, M, C, H, dh, p, stale=True):
     return Q, Kc, Vc, lut, cap
 
 
+def _vt_words(Vc):
+    """Value cache [T][cap][d] bits -> device words [T][cap/64][d] (word-major)."""
+    _, B = need_gpu()
+    words = synth.pack_bits(Vc.transpose(0, 2, 1))            # [T][d][cap/64]
+    return B.to_dev_bits(np.ascontiguousarray(words.transpose(0, 2, 1)))
+
+
 def _attn_gpu(Q, Kc, Vc, lut, cap, C, H, dh, theta=None):
     torch, B = need_gpu()
     T, M, d = Q.shape
     q = B.to_dev_bits(synth.pack_bits(Q))
     k = B.to_dev_bits(synth.pack_bits(Kc))
-    vt = B.to_dev_bits(synth.pack_bits(Vc.transpose(0, 2, 1)))    # [T][d][cap/64]
+    vt = _vt_words(Vc)
     a = torch.full((T, M, d), -5, dtype=torch.int32, device="cuda")
     s_out = torch.full((T, M, d // 64), -1, dtype=torch.int64, device="cuda") if theta else None
     B.nmdlm_bbm_attn(q, k, vt, cap, T, M, C, H, dh, torch.from_numpy(lut).cuda(), a_out=a,
@@ -139,7 +146,7 @@ def _attn_spikes_gpu(Q, Kc, Vc, lut, cap, C, H, dh, theta):
     T, M, d = Q.shape
     q = B.to_dev_bits(synth.pack_bits(Q))
     k = B.to_dev_bits(synth.pack_bits(Kc))
-    vt = B.to_dev_bits(synth.pack_bits(Vc.transpose(0, 2, 1)))
+    vt = _vt_words(Vc)
     s_out = torch.full((T, M, d // 64), -1, dtype=torch.int64, device="cuda")
     ws = B.workspace(B.nmdlm_bbm_attn_workspace_size(T, M, H, dh))
     B.nmdlm_bbm_attn(q, k, vt, cap, T, M, C, H, dh, torch.from_numpy(lut).cuda(),
