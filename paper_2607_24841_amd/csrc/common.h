@@ -65,7 +65,6 @@ constexpr int kMaxSeg = 3;
 constexpr int kChunkSteps = 16;   // k-steps (of 64 active rows) staged per LDS chunk
 constexpr int kTileLd = 68;       // LDS row stride (ints) of the 64-column output tile
 constexpr int kSplitMaxRows = 256;  // K splits only for blocks of at most this many rows
-constexpr int kSplitSlots = 8;      // split slots reserved per (rows x columns) of output
 
 enum EpiMode : int {
   EPI_CUR = 0,     // write int32 currents only
@@ -113,8 +112,8 @@ struct QbsmArgs {
   int lut_shift;
   float* logits;             // EPI_HEAD: [M][N]
   const float* scale;        // EPI_HEAD: [N]
-  int32_t* part;             // split slots [P][gy*gx][16*RT*64]
-  int32_t* counters;         // [gx*gy] arrival counters (zeroed by the prep kernel)
+  int32_t* part;             // K-split accumulators [gy*gx][16*RT*64], zero between products
+  int32_t* counters;         // [gx*gy] arrival counters, zero between products
   uint64_t* u_out;           // partial unions of the output spikes [gy][u_ld] or null
   int u_ld;
   // single-kernel product: union sources and statistics
@@ -132,11 +131,19 @@ struct QbsmScratch {
   int32_t* kact;       // [1]
   uint64_t* sc;        // [ceil(K/64)][R]
   uint64_t* U;         // [ceil(K/64)] union of a large block
-  int32_t* part;       // split slots (split products only)
-  int32_t* counters;   // [tiles]
+  int32_t* part;       // K-split accumulators (split products only), then
+  int32_t* counters;   // [tiles] arrival counters: together the split region
   size_t part_elems;
   size_t n_counters;
 };
+
+// The split region [part, counters + n_counters) rounded to whole 16-byte
+// units (the carver aligns every region to 256 bytes).
+inline int64_t split_region_elems(const QbsmScratch& s) {
+  const char* b = s.part ? reinterpret_cast<const char*>(s.part) : reinterpret_cast<const char*>(s.counters);
+  const char* e = reinterpret_cast<const char*>(s.counters + s.n_counters);
+  return (int64_t)(((size_t)(e - b) + 15) / 16 * 4);
+}
 
 // One product request (host side).
 struct QbsmCall {

@@ -216,6 +216,7 @@ constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
 constexpr int kUpLoads = 2;             // partial-union loads per thread staged in registers
 constexpr int kRowLoads = 2;            // spike-row words per thread staged in registers
+constexpr int kStageBatch = 8;          // further spike-row words per thread per staging batch
 static_assert(kMaxEpiTokens >= 8 * 16, "every tile's residual words are staged (RT <= 8)");
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
@@ -326,32 +327,38 @@ __device__ __forceinline__ void reduce_tile(const v4i (&acc)[RT][4], int* sTile,
       }
 }
 
-// K split across workgroups: every split stores its whole tile (zeros
-// included) into its own slot; the last workgroup to arrive sums the slots in
-// split order.  No slot has to be zero beforehand.  Returns false for the
-// workgroups that are not last.
+// K split across workgroups: every split adds its tile into the tile's
+// accumulator (int32, zero between products) with device-scope atomic adds
+// whose returned values are waited for, so that each add has been performed
+// at the device's point of coherence before the barrier after them; one
+// thread then counts the arrival.  The split that arrives last (it sees P - 1
+// earlier arrivals, each counted after that split's adds were performed)
+// takes the sums with atomic exchanges that leave the accumulator zero, and
+// resets the counter.  Every access to the accumulator and the counter is a
+// device-scope atomic, so no cache has to be written back or invalidated.
+// Integer addition makes the sums independent of the order of arrival.
+// Returns false for the workgroups that are not last.
 template <int ROWS, int NT>
 __device__ bool split_fixup(const QbsmArgs& a, int* sTile, int* sLast, int tid, int x, int y, int z) {
+  (void)z;
   const size_t tile_id = (size_t)y * gridDim.x + x;
-  const size_t slot_elems = (size_t)ROWS * 64;
-  const size_t n_tiles = (size_t)gridDim.x * gridDim.y;
-  int* mine = a.part + ((size_t)z * n_tiles + tile_id) * slot_elems;
-  for (int i = tid; i < ROWS * 64; i += NT)
-    __hip_atomic_store(&mine[i], sTile[(i >> 6) * kTileLd + phys_col(i & 63)], __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-  __threadfence();
+  int* acc = a.part + tile_id * (size_t)(ROWS * 64);
+  int sink = 0;
+  for (int i = tid; i < ROWS * 64; i += NT) {
+    const int v = sTile[(i >> 6) * kTileLd + phys_col(i & 63)];
+    if (v != 0) sink |= __hip_atomic_fetch_add(&acc[i], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  asm volatile("" ::"v"(sink));  // every returned value (so every add) is waited for
   __syncthreads();
-  if (tid == 0) *sLast = (atomicAdd(&a.counters[tile_id], 1) == a.P - 1) ? 1 : 0;
+  if (tid == 0)
+    *sLast = (__hip_atomic_fetch_add(&a.counters[tile_id], 1, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == a.P - 1) ? 1 : 0;
   __syncthreads();
   if (!*sLast) return false;
-  __threadfence();
-  for (int i = tid; i < ROWS * 64; i += NT) {
-    int v = 0;
-    for (int q = 0; q < a.P; ++q)
-      v += __hip_atomic_load(a.part + ((size_t)q * n_tiles + tile_id) * slot_elems + i,
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sTile[(i >> 6) * kTileLd + phys_col(i & 63)] = v;
-  }
+  for (int i = tid; i < ROWS * 64; i += NT)
+    sTile[(i >> 6) * kTileLd + phys_col(i & 63)] =
+        __hip_atomic_exchange(&acc[i], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) __hip_atomic_store(&a.counters[tile_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   return true;
 }
@@ -667,7 +674,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   // ---- staging, store phase
   for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
   epi_store<NT>(a, ep, er, tid, x, y);
-  if (from_parts)
+  if (from_parts || (ROWS > 32 && !a.dense && NT >= Kw))
     for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
   if (stats_wg && tid == 0) sStatCnt = 0;
   if (stats_rows)
@@ -679,13 +686,31 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       sS[rdst[k]] = (uint32_t)v;
       sS[rdst[k] + 1] = (uint32_t)(v >> 32);
     }
-  // rows past kRowLoads passes (all rows when the words outnumber the threads)
-  for (int i = tid + kRowLoads * rpp * Kw; i < ROWS * Kw; i += NT) {
-    const int lr = i / Kw, w = i - lr * Kw;
-    const int t = lr / a.Mb, m = y * a.Mb + (lr - t * a.Mb);
-    const unsigned long long v = (t < a.T && m < a.M) ? a.S[(size_t)(t * a.M + m) * Kw + w] : 0ull;
-    sS[lr * lds_row + 2 * w] = (uint32_t)v;
-    sS[lr * lds_row + 2 * w + 1] = (uint32_t)(v >> 32);
+  // rows past kRowLoads passes (all rows when the words outnumber the
+  // threads): batches of kStageBatch words per thread, every load of a batch
+  // issued (at a clamped address) before the first is stored
+  const int items = ROWS * Kw;
+  for (int i0 = tid + kRowLoads * rpp * Kw; i0 - tid < items; i0 += kStageBatch * NT) {
+    unsigned long long v[kStageBatch];
+    uint32_t kp = 0u;  // bit j: item j lies in the tile and the block
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int i = i0 + j * NT, ic = min(i, items - 1);
+      const int lr = div_small(ic, inv_kw), w = ic - lr * Kw;
+      const int t = div_small(lr, inv_mb), m = y * a.Mb + (lr - t * a.Mb);
+      v[j] = a.S[(size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + w];
+      kp |= (uint32_t)(i < items && t < a.T && m < a.M) << j;
+    }
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int i = i0 + j * NT;
+      if (i < items) {
+        const int lr = div_small(i, inv_kw), w = i - lr * Kw;
+        const unsigned long long vv = ((kp >> j) & 1u) ? v[j] : 0ull;
+        sS[lr * lds_row + 2 * w] = (uint32_t)vv;
+        sS[lr * lds_row + 2 * w + 1] = (uint32_t)(vv >> 32);
+      }
+    }
   }
   if (up_regs && s0 < slices) {
 #pragma unroll
@@ -695,6 +720,16 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   __syncthreads();
   if (from_parts) {
     or_merge<NT>(sLU, a.upart, a.nparts, Kw, tid, upart_or, last_mask);
+  } else if (ROWS > 32 && !a.dense && NT >= Kw) {
+    // many rows: thread tid ORs rows r0, r0 + rpp, ... of word wq (the
+    // slices were cleared before the first barrier), one LDS OR per thread
+    unsigned long long u = 0ull;
+    if (r0 < rpp)
+      for (int lr = r0; lr < ROWS; lr += rpp)
+        u |= (unsigned long long)sS[lr * lds_row + 2 * wq] |
+             ((unsigned long long)sS[lr * lds_row + 2 * wq + 1] << 32);
+    if (wq == Kw - 1) u &= last_mask;
+    if (u) atomicOr(&sLU[wq], u);
   } else {
     for (int w = tid; w < Kw; w += NT) {
       unsigned long long u = ~0ull;
@@ -1260,10 +1295,10 @@ void carve_qbsm_scratch(Carver& cv, const QbsmLimits& L, QbsmScratch* s) {
   s->kact = cv.take<int32_t>(1);
   s->sc = cv.take<uint64_t>((size_t)((L.Kmax + 63) / 64) * (size_t)L.Rmax);
   s->U = cv.take<uint64_t>((size_t)((L.Kmax + 63) / 64));
-  // split slots: up to kSplitSlots tiles of (row tiles x 64 columns) per column
-  size_t rows_cap = 0;
-  if (L.split_rows > 0) rows_cap = L.split_rows <= 128 ? 16 * (size_t)pick_rt(L.split_rows) : 256;
-  s->part_elems = (size_t)kSplitSlots * rows_cap * align_up((size_t)L.split_N, 64);
+  // K-split accumulators: one (row tile x 64 columns) tile per output tile;
+  // the row tiles cover at most R + 128 rows
+  const size_t rows_cap = L.split_rows > 0 ? (size_t)L.split_rows + 128 : 0;
+  s->part_elems = rows_cap * align_up((size_t)L.split_N, 64);
   s->part = s->part_elems ? cv.take<int32_t>(s->part_elems) : nullptr;
   s->n_counters = (size_t)L.tiles_max;
   s->counters = cv.take<int32_t>(s->n_counters);
@@ -1394,15 +1429,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   if ((size_t)tiles > scr.n_counters) return NMDLM_ERR_WORKSPACE;
   if (gy_out) *gy_out = gy;
 
+  // K splits (requested by the flags; at the measured shapes the atomic
+  // accumulation costs more round trips than the split saves)
   int P = (int)((c.flags >> NMDLM_SPLIT_SHIFT) & 0xFFu);
-  if (P == 0) P = 1;
   P = std::max(1, std::min(P, Kw));
-  const size_t slot_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one tile slot per split
-  if (P > 1) {
-    const size_t cap = scr.part ? scr.part_elems / slot_elems : 0;
-    P = (int)std::min<size_t>((size_t)P, cap);
-    if (P < 2) P = 1;
-  }
+  const size_t acc_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one accumulator tile per output tile
+  if (P > 1 && (!scr.part || scr.part_elems < acc_elems)) P = 1;
   // waves per workgroup: many when each workgroup has many k-steps
   const int ks_per_wg = (Kw + P - 1) / P;
   int NW = (ks_per_wg >= 8 * kGroup && RT <= 2) ? 16 : 4;
@@ -1458,10 +1490,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
       pa.nparts = 1;
     }
     hipLaunchKernelGGL(k_prep, dim3(Kw, (R + kPrepRows - 1) / kPrepRows), dim3(256), 0, st, pa);
-  } else if (tiles > 0) {
-    // the single-kernel paths zero no counters: clear them for a split product
-    if (P > 1 && (rc0 = launch_fill_zero(scr.counters, align_up((size_t)tiles * 4, 16), st)) != NMDLM_OK)
-      return rc0;
+  }
+  // a split product accumulates into the zeroed split region (accumulators
+  // and counters), which its last arrivers leave zero again
+  if (P > 1 && tiles > 0) {
+    int32_t* base = scr.part ? scr.part : scr.counters;
+    if ((rc0 = launch_fill_zero(base, (size_t)split_region_elems(scr) * 4, st)) != NMDLM_OK) return rc0;
   }
 
   QbsmArgs a;

@@ -184,3 +184,25 @@ def test_mdlm_generation_matches_oracle():
     ids, log = generate(dm, prompt, n_blocks=3, block=8, steps=4, k_unmask=2)
     assert_same(ids, ids_ref)
     assert all(np.array_equal(a, b) for a, b in zip(log, log_ref))
+
+
+def test_block_forced_split_twice():
+    # every product of the step with its K split four ways (device-scope
+    # atomic accumulation into the split region, which the last arrivers
+    # leave zero), two steps on one workspace
+    torch, B = need_gpu()
+    case = synth.block_case(seed=11, C=40, M=16, d=256, H=4, F=1024)
+    L = case.layer
+    T, C, M, d = case.T, case.C, case.M, L.d
+    tr, kref, vref = _oracle_block_case(case)
+    dm = B.DeviceModel([L], T, C + M, d, L.H, L.F)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, B.NMDLM_NO_HEAD)))
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD,
+                                     x_in=B.to_dev_bits(synth.pack_bits(case.X_ctx))), ws)
+    xb = B.to_dev_bits(synth.pack_bits(case.X_blk))
+    for rep in range(2):
+        y = torch.zeros((T, M, d // 64), dtype=torch.int64, device="cuda")
+        B.nmdlm_block_step(dm, B.step_io(M, C, flags=B.NMDLM_NO_HEAD | (4 << 8), x_in=xb, y_out=y), ws)
+        torch.cuda.synchronize()
+        assert_same(synth.unpack_bits(B.from_dev_bits(y), d), tr.Y, f"Y (step {rep})")
