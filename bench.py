@@ -15,7 +15,9 @@ graphs captured on torch's stream.
 Prints one JSON line with block-denoise tokens/s, the weight-skip fraction,
 the touched-weight bandwidth of the whole step, the roofline of the product
 kernel (timed per launch with HIP events recorded by the library around the
-kernel) and the CPU oracle's rate on a bounded sample.
+kernel), the paper's analytic model of the step's products (Eqs. (12)-(14)
+from their measured union fractions and input sparsities, on MI355X and on
+the two systems of Table I) and the CPU oracle's rate on a bounded sample.
 
 Other workloads (--workload):
   ffn-sweep        FFN weight-traffic sweep, d=4096 -> 14336 -> 4096, T=4, B in {1,4,16,64},
@@ -171,6 +173,7 @@ def bench_ffn_sweep(args):
     import torch
 
     from paper_2607_24841_amd import binding as B
+    from paper_2607_24841_amd import perf_model
     from workloads import synth
 
     B.load()
@@ -208,11 +211,18 @@ def bench_ffn_sweep(args):
             t_dn = _time_graph(g_dn, args.reps) / n_copies
             k = st.cpu().numpy()
             rec = {"B": Bk, "density": pt.density}
-            for nm, row, t in (("up", k[0], t_up), ("dn", k[1], t_dn)):
+            for nm, row, t, X in (("up", k[0], t_up, pt.X_up), ("dn", k[1], t_dn, pt.X_dn)):
                 touched = int(row[1] * row[2])
+                # the paper's Eqs. (12)-(14) at MI355X peaks from the measured
+                # union and input sparsity
+                mod = perf_model.layer_report(nm, Bk, T, int(row[0]), int(row[2]),
+                                              float(row[1]) / float(row[0]), b_w=8,
+                                              sigma=1.0 - float(np.mean(X)))
                 rec[nm] = {"us": t * 1e3, "k_active": int(row[1]), "k_total": int(row[0]),
                            "skip": 1.0 - row[1] / row[0], "touched_bytes": touched,
-                           "GBps": touched / (t * 1e-3) / 1e9}
+                           "GBps": touched / (t * 1e-3) / 1e9,
+                           "model_us_MI355X": mod["MI355X"]["us_per_block"],
+                           "model_regime_MI355X": mod["MI355X"]["regime"]}
             rec["tokens_per_s"] = Bk / ((t_up + t_dn) * 1e-3)
             points.append(rec)
             del g_up, g_dn
@@ -364,6 +374,54 @@ def bench_mdlm24_generate(args):
     print(json.dumps(out), flush=True)
 
 
+def product_input_sparsity(B, torch, dl, L, case, xb, y_step):
+    """Fraction of zero input spikes of the step's four products (the paper's
+    sigma, measured per linear layer): the step is replayed, untimed, through
+    the single-call C ABI (products with currents out, attention with spikes
+    out, IF neurons, activation table) after the step itself has written this
+    block's keys and values into the caches; its output must equal the step's."""
+    import numpy as np
+    T, M, C_ctx = case.T, case.M, case.C
+    d, F, H = L.d, L.F, L.H
+    dw, Fw = d // 64, (F + 63) // 64
+    th = L.theta
+    i64 = dict(dtype=torch.int64, device="cuda")
+    i32 = dict(dtype=torch.int32, device="cuda")
+    ws = B.workspace(max(B.nmdlm_qbsm_workspace_size(T, M, d, 3 * d),
+                         B.nmdlm_qbsm_workspace_size(T, M, d, F),
+                         B.nmdlm_qbsm_workspace_size(T, M, F, d),
+                         B.nmdlm_bbm_attn_workspace_size(T, M, H, d // H)))
+    Q = torch.empty((T, M, dw), **i64)
+    B.nmdlm_qbsm(xb, T, M, d, dl.w_qkv, d, 3 * d, theta=th["q"], s_out=Q, ws=ws)
+    A = torch.empty((T, M, dw), **i64)
+    B.nmdlm_bbm_attn(Q, dl.k_cache, dl.vt_cache, dl.k_cache.shape[1], T, M, C_ctx, H, d // H,
+                     dl.lut_att, theta_a=th["a"], s_out=A, ws=ws)
+    cur = torch.empty((T, M, max(d, F)), **i32)
+    X1 = torch.empty((T, M, dw), **i64)
+    c_o = cur[..., :d].contiguous()
+    B.nmdlm_qbsm(A, T, M, d, dl.w_o, d, d, cur_out=c_o, ws=ws)
+    B.nmdlm_if_neuron(c_o, T, M, d, theta=th["o"], resid=xb, s_out=X1)
+    c_up = torch.empty((T, M, F), **i32)
+    B.nmdlm_qbsm(X1, T, M, d, dl.w_up, F, F, cur_out=c_up, ws=ws)
+    g8 = torch.empty((T, M, F), dtype=torch.uint8, device="cuda")
+    B.nmdlm_qnl_lut(c_up, T * M * F, L.s_up, B.NMDLM_QNL_S8, dl.lut_act, g8)
+    Hs = torch.empty((T, M, Fw), **i64)
+    B.nmdlm_if_neuron(g8.view(torch.int8).to(torch.int32), T, M, F, theta=th["up"], s_out=Hs)
+    c_dn = torch.empty((T, M, d), **i32)
+    B.nmdlm_qbsm(Hs, T, M, F, dl.w_dn, d, d, cur_out=c_dn, ws=ws)
+    Y = torch.empty((T, M, dw), **i64)
+    B.nmdlm_if_neuron(c_dn, T, M, d, theta=th["dn"], resid=X1, s_out=Y)
+    torch.cuda.synchronize()
+    if not torch.equal(Y, y_step):
+        raise RuntimeError("single-call replay of the block step differs from the step")
+
+    def zero_frac(t, k):
+        ones = int(np.unpackbits(t.cpu().numpy().view(np.uint8)).sum())
+        return 1.0 - ones / float(T * M * k)
+
+    return [zero_frac(xb, d), zero_frac(A, d), zero_frac(X1, d), zero_frac(Hs, F)]
+
+
 def bench_block(args):
     import numpy as np
     import torch
@@ -470,6 +528,16 @@ def bench_block(args):
     avg_ms = float(np.mean(dur))
     achieved = sum(nbytes) / (sum(dur) * 1e-3) / 1e9
     traffic = product_traffic()
+    # the paper's analytic model (Eqs. (12)-(14)) of the step's four products,
+    # from their measured union fractions, beside their measured kernel times
+    from paper_2607_24841_amd import perf_model
+    dims = (("qkv", d, 3 * d), ("o", d, d), ("up", d, F), ("down", F, d))
+    sig = product_input_sparsity(B, torch, dms[0].layers[0], L, case, xb, y)
+    reports = [perf_model.layer_report(nm, M, T, di, do, float(k_active[p]) / float(k_total[p]),
+                                       b_w=8, measured_us=1e3 * float(np.mean(dur[p::4])),
+                                       sigma=sig[p])
+               for p, (nm, di, do) in enumerate(dims)]
+    paper_model = perf_model.block_report(reports, measured_step_us=1e3 * ms_per_step)
 
     out = {
         "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
@@ -506,6 +574,7 @@ def bench_block(args):
             "launches_timed": len(dur),
             "timing_issue": timing_issue,
         },
+        "paper_model": paper_model,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
