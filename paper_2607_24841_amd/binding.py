@@ -283,6 +283,26 @@ class DeviceModel:
             l.k_cache.zero_()
             l.vt_cache.zero_()
 
+    def view(self, first: int, count: int, head: bool) -> "ModelView":
+        """Layers [first, first+count) of this model (their weights and caches
+        are shared, not copied), with the token tables, and the head if asked."""
+        return ModelView(self, self.layers[first:first + count], head)
+
+
+class ModelView:
+    """A model struct over a slice of another model's layers."""
+
+    def __init__(self, parent: DeviceModel, layers, head: bool):
+        self.parent = parent                      # keeps the device tensors alive
+        self.layers = list(layers)
+        self.T, self.d, self.H, self.F = parent.T, parent.d, parent.H, parent.F
+        self.V, self.cache_cap = parent.V, parent.cache_cap
+        self._c_layers = (Layer * max(1, len(self.layers)))(*[l.c for l in self.layers])
+        p = parent.c
+        self.c = Model(len(self.layers), p.d, p.H, p.F, p.V, p.T, p.cache_cap, p.max_pos,
+                       self._c_layers, p.emb, p.pos_ch, p.w_head if head else None,
+                       p.head_scale if head else None)
+
 
 def step_io(M, C_, pos0=0, flags=0, x_in=None, tokens=None, masked=None, k_unmask=0, y_out=None,
             logits=None, pred=None, conf=None, unmasked_pos=None, stats=None,

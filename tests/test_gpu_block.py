@@ -206,3 +206,19 @@ def test_block_forced_split_twice():
         B.nmdlm_block_step(dm, B.step_io(M, C, flags=B.NMDLM_NO_HEAD | (4 << 8), x_in=xb, y_out=y), ws)
         torch.cuda.synchronize()
         assert_same(synth.unpack_bits(B.from_dev_bits(y), d), tr.Y, f"Y (step {rep})")
+
+
+# ----------------------------------------------------------------------------
+# encoder-decoder generation (the paper's E2D2 split), T = 8
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("n_enc,n_layers", [(2, 4), (0, 1)], ids=["enc2-dec2", "dec1"])
+def test_e2d2_generation_matches_oracle(n_enc, n_layers):
+    torch, B = need_gpu()
+    from paper_2607_24841_amd.e2d2 import e2d2_generate
+    m = synth.make_mdlm(44 + n_enc, n_layers, d=128, H=2, F=256, V=64, T=8, max_pos=64)
+    prompt = synth.random_tokens(8, 12, m.V)
+    ids_ref, log_ref = O.e2d2_generate(m, n_enc, prompt, n_blocks=2, B=4, steps=4, k_unmask=1)
+    dm = B.DeviceModel.from_mdlm(m, 12 + 8)
+    ids, log = e2d2_generate(dm, n_enc, prompt, n_blocks=2, block=4, steps=4, k_unmask=1)
+    assert_same(ids, ids_ref)
+    assert all(np.array_equal(a, b) for a, b in zip(log, log_ref))

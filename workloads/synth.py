@@ -35,7 +35,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-SEEDS = {"linear": 1001, "block": 1002, "ffn_sweep": 1003, "mdlm12": 1004, "mdlm24": 1005}
+SEEDS = {"linear": 1001, "block": 1002, "ffn_sweep": 1003, "mdlm12": 1004, "mdlm24": 1005,
+         "e2d2": 1006}
 
 
 # ----------------------------------------------------------------------------
@@ -341,3 +342,30 @@ def mdlm24_generation_case(seed: int = SEEDS["mdlm24"], n_layers: int = 24, prom
     model = make_mdlm(seed, n_layers, max_pos=prompt_len + n_blocks * B, **kw)
     prompt = random_tokens(seed, prompt_len, model.V)
     return GenerationCase(model, prompt, n_blocks, B, steps, k_unmask)
+
+
+@dataclass
+class E2d2Case:
+    model: MdlmModel          # layers [0, n_enc) encoder, [n_enc, n_layers) decoder
+    n_enc: int
+    prompt: np.ndarray        # int32 [P]
+    n_blocks: int
+    B: int
+    steps: int
+    k_unmask: int
+
+
+def e2d2_case(seed: int = SEEDS["e2d2"], n_enc: int = 28, n_dec: int = 4, d: int = 512,
+              H: int = 8, F: int = 1536, V: int = 32000, T: int = 8, prompt_len: int = 64,
+              n_blocks: int = 4, B: int = 4, steps: int = 4, k_unmask: int = 1,
+              **kw) -> E2d2Case:
+    """The paper's own model shape (Sec. V-A): 28 encoder and 4 decoder
+    layers, D = 512, D_hid = 1536, T = 8, one token revealed per step (S = B).
+    Synthetic weights and token tables stand in for the converted E2D2 model
+    and WMT14 sentences (neither is available); a 64-token prompt stands in
+    for a source sentence."""
+    model = make_mdlm(seed, n_enc + n_dec, d=d, H=H, F=F, V=V, T=T,
+                      max_pos=prompt_len + n_blocks * B, **kw)
+    prompt = random_tokens(seed, prompt_len, model.V)
+    return E2d2Case(model, n_enc, prompt, n_blocks, B, steps, k_unmask)
+
