@@ -431,3 +431,72 @@ def e2d2_generate(model, n_enc: int, prompt: np.ndarray, n_blocks: int, B: int, 
         encode(tokens, C)
         C += B
     return np.concatenate(out), log
+
+
+# ----------------------------------------------------------------------------
+# Ternary bitwise-coded conversion (Sec. III-B, Eqs. (7)-(11))
+# ----------------------------------------------------------------------------
+def ternary_quantize(a: np.ndarray, K: int, T: int):
+    """Eq. (7): q = round(a / V_th(a)) with V_th(a) = mean(|a|) / K, per token.
+
+    Activations reach the conversion as integers (a layer's int32 output), so
+    V_th = S / (D K) with S = sum_i |a_i| is kept as the exact rational and
+    q_i = round(a_i D K / S) is computed in integers: rounding half away from
+    zero, q = 0 for an all-zero vector, |q| saturating at 2^T - 1 (T bits).
+    a: int [M][D].  Returns (q int64 [M][D], S int64 [M])."""
+    a = np.asarray(a, dtype=np.int64)
+    M, D = a.shape
+    S = np.abs(a).sum(axis=1)
+    q = np.zeros_like(a)
+    lim = (1 << T) - 1
+    for m in range(M):
+        if S[m] == 0:
+            continue
+        num = np.abs(a[m]) * (D * K)
+        mag = (2 * num + S[m]) // (2 * S[m])        # floor(|a| D K / S + 1/2)
+        q[m] = np.sign(a[m]) * np.minimum(mag, lim)
+    return q, S
+
+
+def ternary_planes(q: np.ndarray, T: int) -> np.ndarray:
+    """Eq. (8): bitwise coding with ternary spikes, s_{i,t} = sign(q_i) times
+    bit t-1 of |q_i| for t = 1..T (q = sum_t 2^(t-1) s_t).  Returns int8
+    [T][M][D] in {-1, 0, 1}."""
+    q = np.asarray(q, dtype=np.int64)
+    mag, sgn = np.abs(q), np.sign(q)
+    if mag.max(initial=0) >= (1 << T):
+        raise ValueError("value needs more than T bits")
+    return np.stack([(sgn * ((mag >> t) & 1)).astype(np.int8) for t in range(T)])
+
+
+def ternary_union(s: np.ndarray) -> np.ndarray:
+    """Assumption (ii) of Sec. IV-A on ternary spikes: input i needs its weight
+    row iff s_{i,t} != 0 for some timestep and token of the block."""
+    s = np.asarray(s)
+    return (s != 0).reshape(-1, s.shape[-1]).any(axis=0)
+
+
+def qbsm_ternary(s: np.ndarray, W: np.ndarray):
+    """The spiking product on ternary spikes: I_t = sum_i w_i s_{i,t} per
+    timestep over every input, and the bitwise reconstruction of Eq. (11)
+    acc = sum_t 2^(t-1) I_t (the inner product with the decoded q).
+    s: int8 [T][M][K]; W: int8 [K][N].  Returns (I int64 [T][M][N], acc int64 [M][N])."""
+    s = np.asarray(s)
+    T, M, K = s.shape
+    I = _exact_matmul(s.reshape(T * M, K), W).reshape(T, M, W.shape[1])
+    acc = np.zeros((M, W.shape[1]), dtype=np.int64)
+    for t in range(T):
+        acc += I[t] << t
+    _check_int32(acc, "ternary accumulator")
+    return I, acc
+
+
+def ternary_scale_f32(S: np.ndarray, D: int, K: int) -> np.ndarray:
+    """V_th = S / (D K) as one IEEE fp32 division of the fp32 conversions."""
+    return np.asarray(S, dtype=np.float32) / np.float32(D * K)
+
+
+def ternary_output_f32(acc: np.ndarray, vth32: np.ndarray) -> np.ndarray:
+    """The layer output y = V_th w^T q (Eq. (11)) in fp32: one multiply of the
+    fp32 accumulator by the token's fp32 step."""
+    return np.asarray(acc, dtype=np.float32) * np.asarray(vth32, dtype=np.float32)[:, None]

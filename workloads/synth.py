@@ -36,7 +36,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 SEEDS = {"linear": 1001, "block": 1002, "ffn_sweep": 1003, "mdlm12": 1004, "mdlm24": 1005,
-         "e2d2": 1006}
+         "e2d2": 1006, "ternary": 1007}
 
 
 # ----------------------------------------------------------------------------
@@ -368,4 +368,30 @@ def e2d2_case(seed: int = SEEDS["e2d2"], n_enc: int = 28, n_dec: int = 4, d: int
                       max_pos=prompt_len + n_blocks * B, **kw)
     prompt = random_tokens(seed, prompt_len, model.V)
     return E2d2Case(model, n_enc, prompt, n_blocks, B, steps, k_unmask)
+
+
+@dataclass
+class TernaryCase:
+    a: np.ndarray             # int32 [M][D] activations (a layer's integer output)
+    W: np.ndarray             # int8 [D][N]
+    K: int                    # quantisation levels per mean magnitude
+    T: int                    # bits (timesteps)
+
+
+def ternary_activations(rng: np.random.Generator, M: int, D: int, scale: float = 1000.0,
+                        beta=(0.5, 6.0)) -> np.ndarray:
+    """Integer activations with per-channel magnitudes drawn from Beta(0.5, 6)
+    (a few large channels, many small ones, the same for every token) times
+    Laplace noise per token: small channels quantise to zero for the whole
+    block, which is what the row-load rule skips."""
+    c = rng.beta(beta[0], beta[1], size=D)
+    x = rng.laplace(0.0, 1.0, size=(M, D)) * c[None, :] * scale
+    return np.rint(x).astype(np.int32)
+
+
+def ternary_case(seed: int = SEEDS["ternary"], M: int = 4, D: int = 4096, N: int = 14336,
+                 K: int = 2, T: int = 8) -> TernaryCase:
+    a = ternary_activations(stream(seed, 1), M, D)
+    W = int8_uniform(stream(seed, 2), (D, N))
+    return TernaryCase(a, W, K, T)
 
