@@ -31,7 +31,7 @@
 extern "C" {
 #endif
 
-#define NMDLM_ABI_VERSION 1
+#define NMDLM_ABI_VERSION 2
 
 typedef enum nmdlm_status {
   NMDLM_OK = 0,
@@ -63,6 +63,7 @@ typedef enum nmdlm_status {
 #define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)
 
 /* Supported envelope (NMDLM_ERR_UNSUPPORTED beyond it). */
+#define NMDLM_MAX_TERNARY_K 16384
 #define NMDLM_MAX_T 8
 #define NMDLM_MAX_K 65536
 #define NMDLM_MAX_HEAD_M 4096   /* block tokens of a step that runs the head */
@@ -117,6 +118,50 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K,
                         unsigned flags, void* ws, size_t ws_bytes, void* stream);
 
 size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_ternary_encode — adaptive quantisation and ternary bitwise coding of
+ * integer activations (Sec. III-B, Eqs. (7)-(8)), per token m:
+ *     S = sum_i |a_i|;  V_th = S / (D K)   (mean(|a|) / K, kept exact)
+ *     q_i = round(a_i / V_th) = round(a_i D K / S), halves away from zero,
+ *           0 when S = 0, |q_i| capped at 2^T - 1;
+ *     s_{i,t} = sign(q_i) * bit t-1 of |q_i|,  t = 1..T  (q = sum 2^(t-1) s_t)
+ *
+ *   a       device int32 [M][D] (a layer's integer output)
+ *   K       quantisation levels per mean magnitude (>= 1; D*K < 2^20)
+ *   T       bits = timesteps (1..NMDLM_MAX_T)
+ *   s_pos   device spikes [T][M][ceil(D/64)]: bit set where s = +1
+ *   s_neg   device spikes [T][M][ceil(D/64)]: bit set where s = -1
+ *   s_sum   device int64 [M] or NULL: S per token (V_th = S / (D K))
+ * Integer arithmetic throughout: the result does not depend on rounding.
+ * ------------------------------------------------------------------------ */
+nmdlm_status nmdlm_ternary_encode(const int32_t* a, int M, int D, int K, int T,
+                                  uint64_t* s_pos, uint64_t* s_neg, int64_t* s_sum,
+                                  void* stream);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_qbsm_ternary — the spiking product on ternary bitwise-coded spikes
+ * and its reconstruction (Sec. III-B, Eqs. (10)-(11); row-load rule of
+ * Sec. IV-A on either spike plane):
+ *     I_t[m,n] = sum_k (s_pos - s_neg)[t,m,k] * W[k,n]      t = 1..T
+ *     acc[m,n] = sum_t 2^(t-1) I_t[m,n]   (= sum_k q[m,k] W[k,n], exact)
+ * A weight row k is read only if input k spikes (either sign) somewhere in
+ * the block.  The layer output is V_th[m] * acc[m,n] (V_th from
+ * nmdlm_ternary_encode); acc can feed nmdlm_ternary_encode of the next
+ * layer directly, since the per-token scale cancels in Eq. (7).
+ *
+ *   s_pos, s_neg  device spikes [T][M][ceil(K/64)] (never both set)
+ *   W, ldw, N     as nmdlm_qbsm; K <= NMDLM_MAX_TERNARY_K and
+ *                 (2^T - 1) * K * 127 < 2^31 (else NMDLM_ERR_UNSUPPORTED)
+ *   acc_out       device int32 [M][N]
+ *   stats         as nmdlm_qbsm (active rows of the union of both planes)
+ *   flags, ws     as nmdlm_qbsm (ws of nmdlm_qbsm_workspace_size(T, M, K, N))
+ * ------------------------------------------------------------------------ */
+nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, int T,
+                                int M, int K, const int8_t* W, int N, int64_t ldw,
+                                int32_t* acc_out, nmdlm_qbsm_stats* stats,
+                                unsigned flags, void* ws, size_t ws_bytes,
+                                void* stream);
 
 /* ------------------------------------------------------------------------
  * nmdlm_if_neuron — integrate-and-fire with soft reset (Sec. II-B,

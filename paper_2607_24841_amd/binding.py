@@ -40,7 +40,7 @@ EXPORTS = (
     "nmdlm_qbsm", "nmdlm_qbsm_workspace_size", "nmdlm_if_neuron", "nmdlm_qnl_lut",
     "nmdlm_bbm_attn", "nmdlm_bbm_attn_workspace_size", "nmdlm_block_step",
     "nmdlm_block_step_workspace_size", "nmdlm_workspace_clear", "nmdlm_status_string",
-    "nmdlm_abi_version",
+    "nmdlm_abi_version", "nmdlm_ternary_encode", "nmdlm_qbsm_ternary",
 )
 
 
@@ -114,6 +114,9 @@ def load(path: str = LIB_PATH):
     lib.nmdlm_qbsm_workspace_size.argtypes = [C.c_int] * 4
     lib.nmdlm_qbsm_workspace_size.restype = sz
     lib.nmdlm_if_neuron.argtypes = [vp, C.c_int, C.c_int, C.c_int, i32, vp, vp, vp, vp, vp]
+    lib.nmdlm_ternary_encode.argtypes = [vp, C.c_int, C.c_int, C.c_int, C.c_int, vp, vp, vp, vp]
+    lib.nmdlm_qbsm_ternary.argtypes = [vp, vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64, vp, vp,
+                                       u, vp, sz, vp]
     lib.nmdlm_qnl_lut.argtypes = [vp, i64, C.c_int, C.c_int, vp, vp, vp]
     lib.nmdlm_bbm_attn.argtypes = [vp, vp, vp, i64, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                    vp, vp, i32, vp, vp, sz, vp]
@@ -127,7 +130,8 @@ def load(path: str = LIB_PATH):
     lib.nmdlm_status_string.restype = C.c_char_p
     lib.nmdlm_abi_version.restype = C.c_int
     for fn in ("nmdlm_qbsm", "nmdlm_if_neuron", "nmdlm_qnl_lut", "nmdlm_bbm_attn",
-               "nmdlm_block_step", "nmdlm_workspace_clear"):
+               "nmdlm_block_step", "nmdlm_workspace_clear", "nmdlm_ternary_encode",
+               "nmdlm_qbsm_ternary"):
         getattr(lib, fn).restype = C.c_int
     runtimes = _hip_runtimes_mapped()
     if len(runtimes) > 1:
@@ -187,6 +191,21 @@ def nmdlm_qbsm(s_in, T, M, K, W, N, ldw, bias=None, cur_out=None, theta=0, theta
 
 def nmdlm_qbsm_workspace_size(T, M, K, N) -> int:
     return load().nmdlm_qbsm_workspace_size(T, M, K, N)
+
+
+def nmdlm_ternary_encode(a, M, D, K, T, s_pos, s_neg, s_sum=None, stream=None) -> None:
+    st = load().nmdlm_ternary_encode(ptr(a), M, D, K, T, ptr(s_pos), ptr(s_neg), ptr(s_sum),
+                                     stream_handle(stream))
+    check(st, "nmdlm_ternary_encode")
+
+
+def nmdlm_qbsm_ternary(s_pos, s_neg, T, M, K, W, N, ldw, acc_out, stats=None, flags=0, ws=None,
+                       stream=None) -> None:
+    st = load().nmdlm_qbsm_ternary(ptr(s_pos), ptr(s_neg), T, M, K, ptr(W), N, ldw, ptr(acc_out),
+                                   ptr(stats), flags, ptr(ws),
+                                   0 if ws is None else ws.numel() * ws.element_size(),
+                                   stream_handle(stream))
+    check(st, "nmdlm_qbsm_ternary")
 
 
 def nmdlm_if_neuron(cur, T, M, N, theta=0, theta_vec=None, resid=None, v_inout=None, s_out=None,

@@ -98,6 +98,72 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
   c.flags = flags;
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
+  c.s_neg = nullptr;
+  c.u_in = nullptr;
+  c.u_nparts = 0;
+  c.u_out = nullptr;
+
+  Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
+  QbsmScratch scr;
+  carve_qbsm_scratch(cv, qbsm_limits_single(T, M, K, N), &scr);
+  if (!cv.ok) return NMDLM_ERR_WORKSPACE;
+  return launch_qbsm(c, scr, static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_ternary_encode(const int32_t* a, int M, int D, int K, int T, uint64_t* s_pos,
+                                  uint64_t* s_neg, int64_t* s_sum, void* stream) {
+  if (!a || !s_pos || !s_neg || M < 1 || D < 1 || K < 1 || T < 1) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T || D > NMDLM_MAX_K || (int64_t)D * K >= ((int64_t)1 << 20))
+    return NMDLM_ERR_UNSUPPORTED;
+  return launch_ternary_encode(a, M, D, K, T, s_pos, s_neg, s_sum, static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M, int K,
+                                const int8_t* W, int N, int64_t ldw, int32_t* acc_out,
+                                nmdlm_qbsm_stats* stats, unsigned flags, void* ws, size_t ws_bytes,
+                                void* stream) {
+  if (!s_pos || !s_neg || !acc_out || T < 1 || M < 1 || K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T || K > NMDLM_MAX_TERNARY_K) return NMDLM_ERR_UNSUPPORTED;
+  if (!weights_ok(W, K, N, ldw)) return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)T * M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
+  // |sum_t 2^(t-1) I_t| <= (2^T - 1) K 127 must fit int32
+  if ((((int64_t)1 << T) - 1) * K * 127 >= ((int64_t)1 << 31)) return NMDLM_ERR_UNSUPPORTED;
+  if (!ws || !aligned(ws, 256) || ws_bytes < qbsm_ws(T, M, K, N)) return NMDLM_ERR_WORKSPACE;
+
+  QbsmCall c;
+  c.s_in = s_pos;
+  c.s_neg = s_neg;
+  c.T = T;
+  c.M = M;
+  c.K = K;
+  c.W = W;
+  c.ldw = ldw;
+  c.N = N;
+  c.mode = EPI_BITWISE;
+  c.bias = nullptr;
+  c.cur_out = acc_out;
+  c.theta_vec = nullptr;
+  c.nseg = 1;
+  c.seg_w = 1 << 30;
+  for (int i = 0; i < kMaxSeg; ++i) {
+    c.seg[i].ptr = nullptr;
+    c.seg[i].ld_t = 0;
+    c.seg[i].ld_m = 0;
+    c.seg[i].theta = 1;
+    c.seg[i].transposed = 0;
+    c.seg[i].pos0 = 0;
+    c.seg[i].ld_p = 0;
+  }
+  c.resid = nullptr;
+  c.rld_t = c.rld_m = 0;
+  c.lut = nullptr;
+  c.lut_shift = 0;
+  c.logits = nullptr;
+  c.scale = nullptr;
+  c.stats = stats;
+  c.flags = flags;
+  c.ev_begin = nullptr;
+  c.ev_end = nullptr;
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;

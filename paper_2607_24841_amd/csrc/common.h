@@ -70,7 +70,8 @@ enum EpiMode : int {
   EPI_CUR = 0,     // write int32 currents only
   EPI_IF = 1,      // integrate-and-fire -> packed spikes
   EPI_QNL_IF = 2,  // table non-linearity, then integrate-and-fire
-  EPI_HEAD = 3     // sum over t, fp32 dequantisation -> logits
+  EPI_HEAD = 3,    // sum over t, fp32 dequantisation -> logits
+  EPI_BITWISE = 4  // sum over t weighted 2^t (bitwise-coded input) -> int32 [M][N]
 };
 
 // Destination of the spikes of one column segment of a product.
@@ -118,6 +119,7 @@ struct QbsmArgs {
   int u_ld;
   // single-kernel product: union sources and statistics
   const uint64_t* S;         // input spikes [R][ceil(K/64)]
+  const uint64_t* Sn;        // ternary input: the -1 spikes (S holds the +1 spikes), or null
   const uint64_t* upart;     // partial unions [nparts][ceil(K/64)] or null
   int nparts;
   int dense;
@@ -168,6 +170,7 @@ struct QbsmCall {
   unsigned flags;
   hipEvent_t ev_begin;    // recorded around the product kernel when non-null
   hipEvent_t ev_end;
+  const uint64_t* s_neg;  // ternary input: -1 spikes [T][M][ceil(K/64)] (s_in: +1), or null
   const uint64_t* u_in;   // partial unions of s_in [u_nparts][ceil(K/64)] or null
   int u_nparts;
   uint64_t* u_out;        // where to write the partial unions of the output
@@ -225,6 +228,8 @@ nmdlm_status launch_attn_if(const uint64_t* q, const uint64_t* k_cache, const ui
                             int64_t cap, int T, int M, int C, int H, int dh, const uint8_t* lut,
                             int32_t theta, uint64_t* s_out, uint64_t* u_out, hipStream_t st);
 nmdlm_status launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+nmdlm_status launch_ternary_encode(const int32_t* a, int M, int D, int K, int T, uint64_t* sp,
+                                   uint64_t* sn, int64_t* s_sum, hipStream_t st);
 
 inline nmdlm_status hip_status() {
   return hipGetLastError() == hipSuccess ? NMDLM_OK : NMDLM_ERR_HIP;

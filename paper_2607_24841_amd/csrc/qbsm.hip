@@ -230,6 +230,15 @@ __device__ __forceinline__ v4i a_operand(uint32_t b16) {
              (int)expand4((b16 >> 8) & 0xFu), (int)expand4(b16 >> 12)};
 }
 
+// Signed A operand of ternary spikes: byte 1 where the +1 bit is set, 0xFF
+// (-1) where the -1 bit is set (the two never coincide), else 0.
+__device__ __forceinline__ v4i a_operand_tern(uint32_t p16, uint32_t n16) {
+  return v4i{(int)(expand4(p16 & 0xFu) | expand4(n16 & 0xFu) * 0xFFu),
+             (int)(expand4((p16 >> 4) & 0xFu) | expand4((n16 >> 4) & 0xFu) * 0xFFu),
+             (int)(expand4((p16 >> 8) & 0xFu) | expand4((n16 >> 8) & 0xFu) * 0xFFu),
+             (int)(expand4(p16 >> 12) | expand4(n16 >> 12) * 0xFFu)};
+}
+
 // Four B operands (columns 4c+v) from 16 row dwords (rows 0..15, 4 columns each).
 __device__ __forceinline__ void b_operands(const uint32_t* xw, v4i (&b)[4]) {
 #pragma unroll
@@ -372,6 +381,18 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   const int col = lane, n = n0 + col;
   const bool nv = n < a.N;
   const int pc = phys_col(col);
+  if (a.mode == EPI_BITWISE) {
+    // Eq. (11): sum_t 2^(t-1) I_t, t = 1..T (row t-1 of the tile); exact in
+    // int32 within the bound the launcher checks
+    for (int ml = wave; ml < a.Mb; ml += NW) {
+      const int m = y * a.Mb + ml;
+      if (m >= a.M) break;
+      int s = 0;
+      for (int t = 0; t < a.T; ++t) s += sTile[(t * a.Mb + ml) * kTileLd + pc] << t;
+      if (nv) a.cur_out[(size_t)m * a.N + n] = s;
+    }
+    return;
+  }
   if (a.mode == EPI_HEAD) {
     const float sc = nv ? a.scale[n] : 0.f;
     for (int ml = wave; ml < a.Mb; ml += NW) {
@@ -590,7 +611,7 @@ __device__ __forceinline__ void stats_write(const QbsmArgs& a, int total) {
 // slot (left stale) is multiplied by zero.  Across row blocks the rows read
 // are the block union; repeated reads hit the cache.  Words with no active
 // row are skipped.
-template <int RT, int NW>
+template <int RT, int NW, bool TERN = false>
 __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
@@ -614,6 +635,8 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   unsigned long long* sLU = sDyn;
   unsigned long long* sStat = sDyn + Kw;
   uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + 2 * Kw);
+  // ternary input: the -1 spike rows follow the +1 rows, same layout
+  uint32_t* sSn = sS + ROWS * lds_row;
   const bool stats_wg = a.stats && x == 0 && y == 0 && z == 0;  // workgroup-uniform
 
   const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
@@ -648,7 +671,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   }
   // this row block's spike rows: tile row lr = r0 + k * rpp, word wq; rows
   // past the tile or the block load a valid word and drop it
-  unsigned long long rv[kRowLoads];
+  unsigned long long rv[kRowLoads], rvn[kRowLoads];
   int rdst[kRowLoads];  // dword offset of the item in sS, or -1
   uint32_t keep = 0u;   // bit k: item k lies in the block (else it is stored as zero)
 #pragma unroll
@@ -656,10 +679,13 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     const int lr = r0 + k * rpp;
     rdst[k] = -1;
     rv[k] = 0ull;
+    rvn[k] = 0ull;
     if (wr0 < rpp && wr0 + k * rpp < ROWS) {  // wave-uniform
       const int lc = min(lr, ROWS - 1);
       const int t = div_small(lc, inv_mb), m = y * a.Mb + (lc - t * a.Mb);
-      rv[k] = a.S[(size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + wq];
+      const size_t src = (size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + wq;
+      rv[k] = a.S[src];
+      if constexpr (TERN) rvn[k] = a.Sn[src];
       rdst[k] = (r0 < rpp && lr < ROWS) ? lr * lds_row + 2 * wq : -1;
       keep |= (uint32_t)(t < a.T && m < a.M) << k;
     }
@@ -669,6 +695,9 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   if (from_parts && !up_regs) upart_or = or_slice<NT>(a.upart, a.nparts, Kw, tid);
   unsigned long long spart = 0ull;
   if (stats_rows) spart = or_slice<NT>(a.S, a.T * a.M, Kw, tid);
+  if constexpr (TERN) {
+    if (stats_rows) spart |= or_slice<NT>(a.Sn, a.T * a.M, Kw, tid);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- staging, store phase
@@ -685,20 +714,27 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       const unsigned long long v = ((keep >> k) & 1u) ? rv[k] : 0ull;
       sS[rdst[k]] = (uint32_t)v;
       sS[rdst[k] + 1] = (uint32_t)(v >> 32);
+      if constexpr (TERN) {
+        const unsigned long long vn = ((keep >> k) & 1u) ? rvn[k] : 0ull;
+        sSn[rdst[k]] = (uint32_t)vn;
+        sSn[rdst[k] + 1] = (uint32_t)(vn >> 32);
+      }
     }
   // rows past kRowLoads passes (all rows when the words outnumber the
   // threads): batches of kStageBatch words per thread, every load of a batch
   // issued (at a clamped address) before the first is stored
   const int items = ROWS * Kw;
   for (int i0 = tid + kRowLoads * rpp * Kw; i0 - tid < items; i0 += kStageBatch * NT) {
-    unsigned long long v[kStageBatch];
+    unsigned long long v[kStageBatch], vn[kStageBatch];
     uint32_t kp = 0u;  // bit j: item j lies in the tile and the block
 #pragma unroll
     for (int j = 0; j < kStageBatch; ++j) {
       const int i = i0 + j * NT, ic = min(i, items - 1);
       const int lr = div_small(ic, inv_kw), w = ic - lr * Kw;
       const int t = div_small(lr, inv_mb), m = y * a.Mb + (lr - t * a.Mb);
-      v[j] = a.S[(size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + w];
+      const size_t src = (size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + w;
+      v[j] = a.S[src];
+      if constexpr (TERN) vn[j] = a.Sn[src];
       kp |= (uint32_t)(i < items && t < a.T && m < a.M) << j;
     }
 #pragma unroll
@@ -709,6 +745,11 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
         const unsigned long long vv = ((kp >> j) & 1u) ? v[j] : 0ull;
         sS[lr * lds_row + 2 * w] = (uint32_t)vv;
         sS[lr * lds_row + 2 * w + 1] = (uint32_t)(vv >> 32);
+        if constexpr (TERN) {
+          const unsigned long long vvn = ((kp >> j) & 1u) ? vn[j] : 0ull;
+          sSn[lr * lds_row + 2 * w] = (uint32_t)vvn;
+          sSn[lr * lds_row + 2 * w + 1] = (uint32_t)(vvn >> 32);
+        }
       }
     }
   }
@@ -725,9 +766,13 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     // slices were cleared before the first barrier), one LDS OR per thread
     unsigned long long u = 0ull;
     if (r0 < rpp)
-      for (int lr = r0; lr < ROWS; lr += rpp)
+      for (int lr = r0; lr < ROWS; lr += rpp) {
         u |= (unsigned long long)sS[lr * lds_row + 2 * wq] |
              ((unsigned long long)sS[lr * lds_row + 2 * wq + 1] << 32);
+        if constexpr (TERN)
+          u |= (unsigned long long)sSn[lr * lds_row + 2 * wq] |
+               ((unsigned long long)sSn[lr * lds_row + 2 * wq + 1] << 32);
+      }
     if (wq == Kw - 1) u &= last_mask;
     if (u) atomicOr(&sLU[wq], u);
   } else {
@@ -735,14 +780,18 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       unsigned long long u = ~0ull;
       if (!a.dense) {
         u = 0ull;
-        for (int lr = 0; lr < ROWS; ++lr)
+        for (int lr = 0; lr < ROWS; ++lr) {
           u |= (unsigned long long)sS[lr * lds_row + 2 * w] |
                ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+          if constexpr (TERN)
+            u |= (unsigned long long)sSn[lr * lds_row + 2 * w] |
+                 ((unsigned long long)sSn[lr * lds_row + 2 * w + 1] << 32);
+        }
       }
       sLU[w] = (w == Kw - 1) ? (u & last_mask) : u;
     }
   }
-  if (stats_rows) or_merge<NT>(sStat, a.S, a.T * a.M, Kw, tid, spart, ~0ull);
+  if (stats_rows) or_merge<NT>(sStat, a.S, a.T * a.M, Kw, tid, spart, ~0ull);  // ternary: NT >= Kw
   __syncthreads();
   // first active row (the target of the loads of inactive rows), per wave
   int first = 0x7fffffff;
@@ -790,8 +839,11 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     b_operands(xg, b);
 #pragma unroll
     for (int q = 0; q < RT; ++q) {
-      const uint32_t b16 = (sS[(q * 16 + c) * lds_row + 2 * w + (g >> 1)] >> (16 * (g & 1))) & 0xFFFFu;
-      const v4i af = a_operand(b16);
+      const int sidx = (q * 16 + c) * lds_row + 2 * w + (g >> 1);
+      const uint32_t b16 = (sS[sidx] >> (16 * (g & 1))) & 0xFFFFu;
+      v4i af;
+      if constexpr (TERN) af = a_operand_tern(b16, (sSn[sidx] >> (16 * (g & 1))) & 0xFFFFu);
+      else af = a_operand(b16);
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
@@ -1315,6 +1367,16 @@ static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
 template <int RT, int NW>
 static nmdlm_status launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
                                  hipEvent_t e0, hipEvent_t e1) {
+  // ternary input (-1 spikes given): the variant staging both spike planes
+  if (a.Sn) {
+    if (dyn > 65536 &&
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_words<RT, NW, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+      return NMDLM_ERR_HIP;
+    hipExtLaunchKernelGGL((k_qbsm_words<RT, NW, true>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0,
+                          e1, 0, a);
+    return NMDLM_OK;
+  }
   if (dyn > 65536 &&
       hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_words<RT, NW>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
@@ -1348,9 +1410,9 @@ static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st, hip
 }
 
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
-static size_t words_lds(int RT, int NW, int Kw) {
+static size_t words_lds(int RT, int NW, int Kw, bool tern = false) {
   return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
-         (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4;
+         (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
 }
 
 // Static LDS of k_qbsm_fused<RT, NW> (mirrors its declarations).
@@ -1414,12 +1476,19 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   }
   while (RT > 1 && 16 * RT / 2 >= R && 16 * RT / 2 >= c.T) RT >>= 1;  // no empty tiles
   while (has_tr && RT > 1 && (16 * RT) / c.T > 32) RT >>= 1;  // channel-major: <= 32 tokens
+  const bool tern = c.s_neg != nullptr;
+  if (tern) {
+    // ternary input: the word product only (both spike planes staged)
+    path = 3;
+    while (RT > 1 && words_lds(RT, 4, Kw, true) > kWordsLdsBudget && !rt_forced) RT >>= 1;
+    if (words_lds(RT, 4, Kw, true) > kWordsLdsBudget || Kw > 256) return NMDLM_ERR_UNSUPPORTED;
+  }
   if (path == 0) {
     path = 3;
     while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
     if (words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
   }
-  if (path == 3 && words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
+  if (path == 3 && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
@@ -1453,7 +1522,8 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     // 8 waves, not 16: a 1024-thread bound caps registers at 128 and spills
     NW = words_waves(RT, ks_per_wg);
     if (words_lds(RT, NW, Kw) > kWordsLdsBudget) NW = 4;
-    dyn = (size_t)Kw * 16 + (size_t)16 * RT * (2 * Kw + 1) * 4;
+    if (words_lds(RT, NW, Kw, tern) > kWordsLdsBudget) NW = 4;
+    dyn = (size_t)Kw * 16 + (size_t)16 * RT * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
   } else if (path == 2) {
     // one kernel (union, list and spike compaction in LDS) when the tile's
     // spike rows fit; else the prep pass builds them in global memory
@@ -1529,6 +1599,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.u_out = c.u_out;
   a.u_ld = gx;
   a.S = c.s_in;
+  a.Sn = c.s_neg;
   a.upart = pa.upart;
   a.nparts = pa.nparts;
   a.dense = dense;

@@ -264,6 +264,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
                      (0x7u << NMDLM_PATH_SHIFT));
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
+  c.s_neg = nullptr;
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;

@@ -31,7 +31,7 @@ def test_exports_every_declared_function(lib):
     assert set(B.EXPORTS) <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.nmdlm_abi_version() == 1
+    assert lib.nmdlm_abi_version() == 2
     assert lib.nmdlm_status_string(0) == b"ok"
     assert lib.nmdlm_status_string(3).startswith(b"workspace")
 
@@ -123,3 +123,28 @@ def test_block_step_argument_errors(lib):
     big = B.step_io(4097, 0, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
     nb = lib.nmdlm_block_step_workspace_size(C.byref(mh), 4097, 0)
     assert nb > 0 and call(mh, big, nb=nb) == B.NMDLM_ERR_UNSUPPORTED
+
+
+def test_ternary_argument_errors(lib):
+    def enc(**kw):
+        a = dict(a=FAKE, M=4, D=512, K=2, T=8, sp=FAKE, sn=FAKE, ss=None)
+        a.update(kw)
+        return lib.nmdlm_ternary_encode(a["a"], a["M"], a["D"], a["K"], a["T"], a["sp"], a["sn"],
+                                        a["ss"], None)
+    assert enc(a=None) == B.NMDLM_ERR_INVALID_ARG
+    assert enc(sn=None) == B.NMDLM_ERR_INVALID_ARG
+    assert enc(K=0) == B.NMDLM_ERR_INVALID_ARG
+    assert enc(T=9) == B.NMDLM_ERR_UNSUPPORTED
+    assert enc(D=4096, K=256) == B.NMDLM_ERR_UNSUPPORTED          # D K >= 2^20
+
+    def prod(**kw):
+        a = dict(sp=FAKE, sn=FAKE, T=8, M=4, K=4096, W=FAKE, N=512, ldw=512, acc=FAKE, ws=FAKE,
+                 ws_bytes=1 << 30)
+        a.update(kw)
+        return lib.nmdlm_qbsm_ternary(a["sp"], a["sn"], a["T"], a["M"], a["K"], a["W"], a["N"],
+                                      a["ldw"], a["acc"], None, 0, a["ws"], a["ws_bytes"], None)
+    assert prod(sn=None) == B.NMDLM_ERR_INVALID_ARG
+    assert prod(acc=None) == B.NMDLM_ERR_INVALID_ARG
+    assert prod(K=20000) == B.NMDLM_ERR_UNSUPPORTED                # beyond the staged planes
+    assert prod(ldw=500) == B.NMDLM_ERR_INVALID_ARG
+    assert prod(ws=None) == B.NMDLM_ERR_WORKSPACE
