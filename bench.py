@@ -32,6 +32,9 @@ Other workloads (--workload):
   e2d2-generate    the paper's own shape: encoder-decoder MDLM with 28 encoder and 4
      decoder layers, d=512, FFN 1536, T=8; 64-id prompt, 4 blocks of 4 tokens, one
      token unmasked per step (block-causal encoder, each token encoded once).
+  ternary-ffn      the paper's ternary bitwise coding (T=8) through the FFN
+     4096 -> 14336 -> 4096: encode, up product, encode, down product, for B in
+     {1, 4, 16} tokens and K in {1, 2, 4} quantisation levels.
 """
 from __future__ import annotations
 
@@ -58,7 +61,7 @@ def parse():
                    help="extra block-step flags (path overrides; results do not change)")
     p.add_argument("--workload", default="block",
                    choices=("block", "ffn-sweep", "mdlm12-step", "mdlm24-generate",
-                            "e2d2-generate"),
+                            "e2d2-generate", "ternary-ffn"),
                    help="block: one transformer block at one denoising step (default)")
     p.add_argument("--reps", type=int, default=20,
                    help="timed repetitions (ffn-sweep, mdlm12-step)")
@@ -135,7 +138,7 @@ def main():
         sys.exit(2)
     {"block": bench_block, "ffn-sweep": bench_ffn_sweep, "mdlm12-step": bench_mdlm12_step,
      "mdlm24-generate": bench_mdlm24_generate,
-     "e2d2-generate": bench_e2d2_generate}[args.workload](args)
+     "e2d2-generate": bench_e2d2_generate, "ternary-ffn": bench_ternary_ffn}[args.workload](args)
 
 
 def _graph(fn):
@@ -375,6 +378,85 @@ def bench_mdlm24_generate(args):
         "generated_tokens_per_s": n_tok / (t_gen * 1e-3),
         "generated_tokens_per_s_with_prefill": n_tok / ((t_pre + t_gen) * 1e-3),
         "prefill_ms": t_pre, "generation_ms": t_gen, "issue": "eager",
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_ternary_ffn(args):
+    """Ternary bitwise-coded FFN (Sec. III-B): integer activations [B][4096]
+    -> encode (T=8) -> up product 4096->14336 -> encode its output -> down
+    product 14336->4096, for B in {1, 4, 16} and K in {1, 2, 4} quantisation
+    levels; 4 rotating weight copies (470 MB) so that weights stream from HBM."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from workloads import synth
+
+    B.load()
+    ffn = synth.ffn_sweep_weights()
+    d, F = ffn.W_up.shape
+    T = 8
+    n_copies = 4
+    W_up = [torch.from_numpy(ffn.W_up).cuda() for _ in range(n_copies)]
+    W_dn = [torch.from_numpy(ffn.W_dn).cuda() for _ in range(n_copies)]
+    points = []
+    for Bk in (1, 4, 16):
+        for Kq in (1, 2, 4):
+            a = torch.from_numpy(synth.ternary_activations(synth.stream(1007, 40 + Bk, Kq), Bk, d)).cuda()
+            dw, Fw = d // 64, F // 64
+            up_p = torch.empty((T, Bk, dw), dtype=torch.int64, device="cuda")
+            up_n = torch.empty_like(up_p)
+            dn_p = torch.empty((T, Bk, Fw), dtype=torch.int64, device="cuda")
+            dn_n = torch.empty_like(dn_p)
+            h = torch.empty((Bk, F), dtype=torch.int32, device="cuda")
+            y = torch.empty((Bk, d), dtype=torch.int32, device="cuda")
+            st = torch.zeros((2, 4), dtype=torch.int64, device="cuda")
+            ws = B.workspace(max(B.nmdlm_qbsm_workspace_size(T, Bk, d, F),
+                                 B.nmdlm_qbsm_workspace_size(T, Bk, F, d)))
+
+            def chain(c):
+                B.nmdlm_ternary_encode(a, Bk, d, Kq, T, up_p, up_n)
+                B.nmdlm_qbsm_ternary(up_p, up_n, T, Bk, d, W_up[c], F, F, h, stats=st[0], ws=ws)
+                B.nmdlm_ternary_encode(h, Bk, F, Kq, T, dn_p, dn_n)
+                B.nmdlm_qbsm_ternary(dn_p, dn_n, T, Bk, F, W_dn[c], d, d, y, stats=st[1], ws=ws)
+
+            def up(c):
+                B.nmdlm_qbsm_ternary(up_p, up_n, T, Bk, d, W_up[c], F, F, h, ws=ws)
+
+            def dn(c):
+                B.nmdlm_qbsm_ternary(dn_p, dn_n, T, Bk, F, W_dn[c], d, d, y, ws=ws)
+
+            g_chain = _graph(lambda: [chain(c) for c in range(n_copies)])
+            t_chain = _time_graph(g_chain, args.reps) / n_copies
+            g_up = _graph(lambda: [up(c) for c in range(n_copies)])
+            g_dn = _graph(lambda: [dn(c) for c in range(n_copies)])
+            t_up = _time_graph(g_up, args.reps) / n_copies
+            t_dn = _time_graph(g_dn, args.reps) / n_copies
+            k = st.cpu().numpy()
+            rec = {"B": Bk, "K": Kq, "T": T, "chain_us": t_chain * 1e3,
+                   "tokens_per_s": Bk / (t_chain * 1e-3)}
+            for nm, row, t in (("up", k[0], t_up), ("dn", k[1], t_dn)):
+                touched = int(row[1] * row[2])
+                rec[nm] = {"us": t * 1e3, "skip": 1.0 - row[1] / row[0], "touched_bytes": touched,
+                           "GBps": touched / (t * 1e-3) / 1e9}
+            points.append(rec)
+            del g_chain, g_up, g_dn
+    head = [p for p in points if p["B"] == 16 and p["K"] == 2][0]
+    best = max((p[m]["GBps"], p, m) for p in points for m in ("up", "dn"))
+    out = {
+        "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
+        "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": args.reps,
+        "warmup": 1, "ms_per_step": head["chain_us"] / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "config": {"workload": "ternary bitwise-coded FFN d=4096->14336->4096, T=8, integer "
+                               "activations with Beta(0.5,6) channel scales; value at B=16, K=2",
+                   "weight_copies_rotated": n_copies},
+        "roofline": {"kernel": "k_qbsm (ternary word product, 2^(t-1)-weighted reconstruction)",
+                     "bound": "hbm", "achieved": best[0], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": best[0] / HBM_PEAK_GBPS, "traffic": None,
+                     "at": f"B={best[1]['B']} K={best[1]['K']} {best[2]}"},
+        "points": points,
     }
     print(json.dumps(out), flush=True)
 
