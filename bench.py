@@ -35,6 +35,10 @@ Other workloads (--workload):
   ternary-ffn      the paper's ternary bitwise coding (T=8) through the FFN
      4096 -> 14336 -> 4096: encode, up product, encode, down product, for B in
      {1, 4, 16} tokens and K in {1, 2, 4} quantisation levels.
+  block-batch      the default block step over n_seq in {1, 2, 4, 8, 16, 32} sequences at
+     once (each with its own 512-token context and 16-token block): every product
+     reads a weight row once for the whole batch; tokens/s, union fractions and
+     touched bytes per point, beside the analytic model at the measured unions.
 """
 from __future__ import annotations
 
@@ -61,7 +65,7 @@ def parse():
                    help="extra block-step flags (path overrides; results do not change)")
     p.add_argument("--workload", default="block",
                    choices=("block", "ffn-sweep", "mdlm12-step", "mdlm24-generate",
-                            "e2d2-generate", "ternary-ffn"),
+                            "e2d2-generate", "ternary-ffn", "block-batch"),
                    help="block: one transformer block at one denoising step (default)")
     p.add_argument("--reps", type=int, default=20,
                    help="timed repetitions (ffn-sweep, mdlm12-step)")
@@ -75,8 +79,8 @@ def parse():
 # with the commands is profiles/k_qbsm_words_one_block_step_traffic.md.  Valid
 # only for the product-kernel sources with this digest: any change to them
 # reports null until the counters are taken again.
-TRAFFIC = {"sources_sha256": "953ea93ba8b6b6f634ba7d56ec5d6929b4ec931009dc790f8fc3d1d9aa8eab2d",
-           "bytes_per_launch": 2584308.1}
+TRAFFIC = {"sources_sha256": "acaaaf647dd48b2b386da0667ed657308c8e207f503c7c363f2578b66909377b",
+           "bytes_per_launch": 2631235.6}
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
 
@@ -138,7 +142,8 @@ def main():
         sys.exit(2)
     {"block": bench_block, "ffn-sweep": bench_ffn_sweep, "mdlm12-step": bench_mdlm12_step,
      "mdlm24-generate": bench_mdlm24_generate,
-     "e2d2-generate": bench_e2d2_generate, "ternary-ffn": bench_ternary_ffn}[args.workload](args)
+     "e2d2-generate": bench_e2d2_generate, "ternary-ffn": bench_ternary_ffn,
+     "block-batch": bench_block_batch}[args.workload](args)
 
 
 def _graph(fn):
@@ -751,6 +756,96 @@ def bench_block(args):
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+BATCH_SEQS = (1, 2, 4, 8, 16, 32)
+
+
+def bench_block_batch(args):
+    """The one-block step over several sequences per call (each sequence its
+    own seeded context and block inputs, one shared layer)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from paper_2607_24841_amd import perf_model
+    from workloads import synth
+
+    B.load()
+    nmax = max(BATCH_SEQS)
+    base = synth.block_case(seed=args.seed)
+    L = base.layer
+    T, C_ctx, M, d, H, F = base.T, base.C, base.M, L.d, L.H, L.F
+    inputs = [synth.block_inputs(args.seed + 1000 * s, C_ctx, M, d, T) for s in range(nmax)]
+    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F, max_seq=nmax) for _ in range(args.copies)]
+    nb = max(B.nmdlm_block_step_workspace_size(dms[0], nmax * C_ctx, B.NMDLM_NO_HEAD),
+             B.nmdlm_block_step_workspace_size(dms[0], nmax * M, B.NMDLM_NO_HEAD))
+    ws = B.workspace(nb)
+    xc = B.to_dev_bits(synth.pack_bits(np.concatenate([x for x, _ in inputs], axis=1)))
+    B.nmdlm_block_step(dms[0], B.step_io(C_ctx, 0, flags=B.NMDLM_NO_HEAD, x_in=xc, n_seq=nmax), ws)
+    for dm in dms[1:]:                     # identical layers: copy the prefilled caches
+        dm.layers[0].k_seq.copy_(dms[0].layers[0].k_seq)
+        dm.layers[0].vt_seq.copy_(dms[0].layers[0].vt_seq)
+    del xc
+    xb_all = np.concatenate([x for _, x in inputs], axis=1)        # [T][nmax M][d]
+    torch.cuda.synchronize()
+    dims = (("qkv", d, 3 * d), ("o", d, d), ("up", d, F), ("down", F, d))
+    points = []
+    for n in BATCH_SEQS:
+        xb = B.to_dev_bits(synth.pack_bits(np.ascontiguousarray(xb_all[:, :n * M])))
+        y = torch.zeros((T, n * M, d // 64), dtype=torch.int64, device="cuda")
+        stats = torch.zeros((4, 4), dtype=torch.int64, device="cuda")
+        io = B.step_io(M, C_ctx, flags=B.NMDLM_NO_HEAD | args.flags, x_in=xb, y_out=y,
+                       stats=stats, n_seq=n)
+
+        def steps():
+            for dm in dms:
+                B.nmdlm_block_step(dm, io, ws)
+        g = _graph(steps)
+        ms = _time_graph(g, args.reps) / len(dms)
+        del g
+        st = stats.cpu().numpy()
+        k_total, k_active, n_col = st[:, 0], st[:, 1], st[:, 2]
+        touched = int((k_active * n_col).sum())
+        reps = [perf_model.layer_report(nm, n * M, T, di, do, float(k_active[p]) / float(k_total[p]),
+                                        b_w=8)
+                for p, (nm, di, do) in enumerate(dims)]
+        model = perf_model.block_report(reps)
+        points.append({
+            "n_seq": n, "tokens_per_step": n * M, "ms_per_step": ms,
+            "tokens_per_s": n * M / (ms * 1e-3),
+            "union_frac": {nm: float(k_active[p]) / float(k_total[p])
+                           for p, (nm, _, _) in enumerate(dims)},
+            "touched_weight_bytes_per_step": touched,
+            "touched_weight_bytes_per_token": touched / (n * M),
+            "touched_weight_GBps": touched / (ms * 1e-3) / 1e9,
+            "model_us_per_step_MI355X": model["MI355X_us_per_block"],
+        })
+        print(json.dumps({"progress": "block-batch", **points[-1]}), file=sys.stderr, flush=True)
+    best = points[-1]
+    out = {
+        "metric": "batched block-denoise tokens/s",
+        "value": best["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.reps * len(dms),
+        "warmup": 1,
+        "ms_per_step": best["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {
+            "workload": f"one spiking transformer block at a single denoising step over {nmax} "
+                        "sequences at once: d=1024, 16 heads x 64, FFN 4096, T=4, per sequence a "
+                        "block of 16 masked tokens over 512 context tokens, input spike rate "
+                        "0.10, int8 weights",
+            "layer_copies_rotated": len(dms), "issue": "hip_graph",
+        },
+        "points": points,
+    }
     print(json.dumps(out), flush=True)
 
 

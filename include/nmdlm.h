@@ -31,7 +31,7 @@
 extern "C" {
 #endif
 
-#define NMDLM_ABI_VERSION 2
+#define NMDLM_ABI_VERSION 3
 
 typedef enum nmdlm_status {
   NMDLM_OK = 0,
@@ -247,6 +247,17 @@ size_t nmdlm_bbm_attn_workspace_size(int T, int M, int H, int dh);
  * conf = 1 / sum_v exp(logit_v - logit_pred) (fp64); then the k_unmask
  * masked positions of highest confidence (ties: lower position) take their
  * predicted token (B/S tokens per step, Sec. III-A).
+ *
+ * Several sequences in one step (io->n_seq > 1): n_seq independent
+ * sequences at the same block (same M, C, pos0) share every product, so a
+ * weight row is read once when it is active for any of their n_seq*M tokens
+ * (the row-load rule of Sec. IV over the batch); attention, the caches and
+ * the unmasking stay per sequence.  Token-indexed buffers then hold the
+ * sequences one after the other: tokens/masked/pred/conf [n_seq][M], spikes
+ * [T][n_seq*M][d/64], logits [n_seq*M][V], unmasked_pos [n_seq][k_unmask];
+ * the caches of sequence s start s*T*cache_cap*d/64 words into k_cache and
+ * vt_cache (both hold model->max_seq sequences).  With n_seq > 1, M must be
+ * a multiple of 16/T (integer division) and NMDLM_ATTN_FUSED is ignored.
  * ------------------------------------------------------------------------ */
 typedef struct nmdlm_layer {
   const int8_t* w_qkv;   /* device [d][3d]: columns Q | K | V */
@@ -272,6 +283,9 @@ typedef struct nmdlm_model {
                                  position spike ORed into the token spikes */
   const int8_t* w_head;       /* device [d][V] (NULL allowed with NO_HEAD) */
   const float* head_scale;    /* device [V]                                */
+  int max_seq;                /* sequences the caches hold (0 counts as 1):
+                                 k_cache [max_seq][T][cache_cap][d/64],
+                                 vt_cache [max_seq][T][cache_cap/64][d]     */
 } nmdlm_model;
 
 typedef struct nmdlm_step_io {
@@ -299,11 +313,15 @@ typedef struct nmdlm_step_io {
                               order as stats), stamped by its dispatch;
                               NMDLM_ERR_UNSUPPORTED inside stream capture  */
   int n_prof_events;       /* length of prof_events                         */
+  int n_seq;               /* sequences in the step, 1..max(1, max_seq) (0
+                              counts as 1); M is per sequence              */
 } nmdlm_step_io;
 
 nmdlm_status nmdlm_block_step(const nmdlm_model* model, nmdlm_step_io* io,
                               void* ws, size_t ws_bytes, void* stream);
 
+/* Workspace of a step over M block tokens in all (n_seq * M for a step of
+ * several sequences). */
 size_t nmdlm_block_step_workspace_size(const nmdlm_model* model, int M,
                                        unsigned flags);
 

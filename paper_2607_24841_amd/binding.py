@@ -71,7 +71,7 @@ class Model(C.Structure):
         ("n_layers", C.c_int), ("d", C.c_int), ("H", C.c_int), ("F", C.c_int), ("V", C.c_int),
         ("T", C.c_int), ("cache_cap", C.c_int64), ("max_pos", C.c_int),
         ("layers", C.POINTER(Layer)), ("emb", C.c_void_p), ("pos_ch", C.c_void_p),
-        ("w_head", C.c_void_p), ("head_scale", C.c_void_p),
+        ("w_head", C.c_void_p), ("head_scale", C.c_void_p), ("max_seq", C.c_int),
     ]
 
 
@@ -82,6 +82,7 @@ class StepIO(C.Structure):
         ("k_unmask", C.c_int), ("y_out", C.c_void_p), ("logits", C.c_void_p),
         ("pred", C.c_void_p), ("conf", C.c_void_p), ("unmasked_pos", C.c_void_p),
         ("stats", C.c_void_p), ("prof_events", C.POINTER(C.c_void_p)), ("n_prof_events", C.c_int),
+        ("n_seq", C.c_int),
     ]
 
 
@@ -259,7 +260,11 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
 
 
 class DeviceLayer:
-    def __init__(self, L, T: int, cache_cap: int, device="cuda"):
+    """One layer's weights and tables on the GPU, with K/V caches for
+    max_seq sequences: k_seq [max_seq][T][cap][d/64], vt_seq
+    [max_seq][T][cap/64][d]; k_cache / vt_cache are sequence 0's."""
+
+    def __init__(self, L, T: int, cache_cap: int, device="cuda", max_seq: int = 1):
         d = L.d
         self.w_qkv = _dev(L.W_qkv, device)
         self.w_o = _dev(L.W_o, device)
@@ -267,8 +272,9 @@ class DeviceLayer:
         self.w_dn = _dev(L.W_dn, device)
         self.lut_att = _dev(L.lut_att, device)
         self.lut_act = _dev(L.lut_act, device)
-        self.k_cache = torch.zeros((T, cache_cap, d // 64), dtype=torch.int64, device=device)
-        self.vt_cache = torch.zeros((T, cache_cap // 64, d), dtype=torch.int64, device=device)  # word-major
+        self.k_seq = torch.zeros((max_seq, T, cache_cap, d // 64), dtype=torch.int64, device=device)
+        self.vt_seq = torch.zeros((max_seq, T, cache_cap // 64, d), dtype=torch.int64, device=device)
+        self.k_cache, self.vt_cache = self.k_seq[0], self.vt_seq[0]  # word-major values
         th = L.theta
         self.c = Layer(ptr(self.w_qkv), ptr(self.w_o), ptr(self.w_up), ptr(self.w_dn),
                        th["q"], th["k"], th["v"], th["a"], th["o"], th["up"], th["dn"], L.s_up,
@@ -279,10 +285,11 @@ class DeviceModel:
     """A stack of layers (and optionally token tables and a head) on the GPU."""
 
     def __init__(self, layers, T: int, cache_cap: int, d: int, H: int, F: int, V: int = 1,
-                 emb=None, pos_ch=None, W_head=None, scale=None, device="cuda"):
+                 emb=None, pos_ch=None, W_head=None, scale=None, device="cuda", max_seq: int = 1):
         cache_cap = (cache_cap + 63) // 64 * 64
         self.T, self.d, self.H, self.F, self.V, self.cache_cap = T, d, H, F, V, cache_cap
-        self.layers = [DeviceLayer(L, T, cache_cap, device) for L in layers]
+        self.max_seq = max(1, int(max_seq))
+        self.layers = [DeviceLayer(L, T, cache_cap, device, self.max_seq) for L in layers]
         self._c_layers = (Layer * max(1, len(self.layers)))(*[l.c for l in self.layers])
         self.emb = _dev(emb, device) if emb is not None else None
         self.pos_ch = _dev(pos_ch.astype(np.int32), device) if pos_ch is not None else None
@@ -290,17 +297,18 @@ class DeviceModel:
         self.scale = _dev(scale.astype(np.float32), device) if scale is not None else None
         self.max_pos = 0 if pos_ch is None else int(pos_ch.shape[0])
         self.c = Model(len(self.layers), d, H, F, V, T, cache_cap, self.max_pos, self._c_layers,
-                       ptr(self.emb), ptr(self.pos_ch), ptr(self.w_head), ptr(self.scale))
+                       ptr(self.emb), ptr(self.pos_ch), ptr(self.w_head), ptr(self.scale),
+                       self.max_seq)
 
     @classmethod
-    def from_mdlm(cls, m, cache_cap: int, device="cuda"):
+    def from_mdlm(cls, m, cache_cap: int, device="cuda", max_seq: int = 1):
         return cls(m.layers, m.T, cache_cap, m.d, m.H, m.F, m.V, emb=m.emb, pos_ch=m.pos_ch,
-                   W_head=m.W_head, scale=m.scale, device=device)
+                   W_head=m.W_head, scale=m.scale, device=device, max_seq=max_seq)
 
     def reset_caches(self):
         for l in self.layers:
-            l.k_cache.zero_()
-            l.vt_cache.zero_()
+            l.k_seq.zero_()
+            l.vt_seq.zero_()
 
     def view(self, first: int, count: int, head: bool) -> "ModelView":
         """Layers [first, first+count) of this model (their weights and caches
@@ -315,22 +323,24 @@ class ModelView:
         self.parent = parent                      # keeps the device tensors alive
         self.layers = list(layers)
         self.T, self.d, self.H, self.F = parent.T, parent.d, parent.H, parent.F
-        self.V, self.cache_cap = parent.V, parent.cache_cap
+        self.V, self.cache_cap, self.max_seq = parent.V, parent.cache_cap, parent.max_seq
         self._c_layers = (Layer * max(1, len(self.layers)))(*[l.c for l in self.layers])
         p = parent.c
         self.c = Model(len(self.layers), p.d, p.H, p.F, p.V, p.T, p.cache_cap, p.max_pos,
                        self._c_layers, p.emb, p.pos_ch, p.w_head if head else None,
-                       p.head_scale if head else None)
+                       p.head_scale if head else None, p.max_seq)
 
 
 def step_io(M, C_, pos0=0, flags=0, x_in=None, tokens=None, masked=None, k_unmask=0, y_out=None,
             logits=None, pred=None, conf=None, unmasked_pos=None, stats=None,
-            prof_events=None) -> StepIO:
-    """prof_events: optional ctypes array of hipEvent_t handles (see HipEvents)."""
+            prof_events=None, n_seq: int = 1) -> StepIO:
+    """prof_events: optional ctypes array of hipEvent_t handles (see HipEvents).
+    n_seq: sequences in the step; M is per sequence, token buffers hold the
+    sequences one after the other."""
     ev = prof_events if prof_events is not None else None
     return StepIO(M, C_, pos0, flags, ptr(x_in), ptr(tokens), ptr(masked), k_unmask, ptr(y_out),
                   ptr(logits), ptr(pred), ptr(conf), ptr(unmasked_pos), ptr(stats),
-                  ev, 0 if ev is None else len(ev))
+                  ev, 0 if ev is None else len(ev), n_seq)
 
 
 class HipEvents:

@@ -87,6 +87,8 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
     c.seg[i].transposed = 0;
     c.seg[i].pos0 = 0;
     c.seg[i].ld_p = 0;
+    c.seg[i].seq_len = 0;
+    c.seg[i].ld_s = 0;
   }
   c.resid = nullptr;
   c.rld_t = c.rld_m = 0;
@@ -99,6 +101,7 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
   c.s_neg = nullptr;
+  c.seq_len = 0;
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;
@@ -133,6 +136,7 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
   QbsmCall c;
   c.s_in = s_pos;
   c.s_neg = s_neg;
+  c.seq_len = 0;
   c.T = T;
   c.M = M;
   c.K = K;
@@ -153,6 +157,8 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
     c.seg[i].transposed = 0;
     c.seg[i].pos0 = 0;
     c.seg[i].ld_p = 0;
+    c.seg[i].seq_len = 0;
+    c.seg[i].ld_s = 0;
   }
   c.resid = nullptr;
   c.rld_t = c.rld_m = 0;
@@ -243,7 +249,13 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   if (dh != 64 && dh != 128) return NMDLM_ERR_UNSUPPORTED;
   if (md->d > NMDLM_MAX_K || md->F > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
   if (io->M < 1 || io->C < 0 || io->pos0 < 0) return NMDLM_ERR_INVALID_ARG;
-  if ((int64_t)md->T * io->M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
+  if (md->max_seq < 0 || io->n_seq < 0) return NMDLM_ERR_INVALID_ARG;
+  const int n_seq = std::max(io->n_seq, 1);
+  if (n_seq > std::max(md->max_seq, 1)) return NMDLM_ERR_INVALID_ARG;
+  // several sequences: one row block of every product lies within a sequence
+  if (n_seq > 1 && io->M % (16 / md->T) != 0) return NMDLM_ERR_UNSUPPORTED;
+  const int64_t Mt = (int64_t)n_seq * io->M;
+  if ((int64_t)md->T * Mt > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
   if (md->cache_cap % 64 != 0 || md->cache_cap < (int64_t)io->C + io->M)
     return NMDLM_ERR_INVALID_ARG;
   if (md->n_layers > 0 && !md->layers) return NMDLM_ERR_INVALID_ARG;
@@ -271,7 +283,7 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
     if (!io->tokens || !io->masked || io->k_unmask < 0) return NMDLM_ERR_INVALID_ARG;
     if (io->M > NMDLM_MAX_HEAD_M) return NMDLM_ERR_UNSUPPORTED;
   }
-  if (!ws || !aligned(ws, 256) || ws_bytes < block_step_ws_size(md, io->M, io->flags))
+  if (!ws || !aligned(ws, 256) || ws_bytes < block_step_ws_size(md, (int)Mt, io->flags))
     return NMDLM_ERR_WORKSPACE;
   if (io->prof_events && io->n_prof_events > 0) {
     // timing events are plain records: not available inside stream capture

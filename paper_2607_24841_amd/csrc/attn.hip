@@ -31,7 +31,9 @@ __device__ __forceinline__ int32_t attn_norm(long long num, long long den, bool 
   return (int32_t)((256LL * num) / den);
 }
 
-// grid (H, ceil(M/16), T); wave i takes 64-key chunks i, i+NW, ...  Every
+// grid (H, n_seq * ceil(M/16), T), M queries per sequence, rows of q and
+// a_out sequence-major (n_seq * M per timestep), the caches of sequence s at
+// s * seq_words words past kc / vt; wave i takes 64-key chunks i, i+NW, ...  Every
 // load of a chunk (16 keys per lane, NT value words) is issued before it is
 // scored; with up to 64*NW keys each wave has one chunk, so all the key and
 // value loads of the workgroup are in flight together.  The table is read
@@ -42,7 +44,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
                                                   const uint64_t* __restrict__ vt, int64_t cap,
                                                   int T, int M, int C, int H,
                                                   const uint8_t* __restrict__ lut,
-                                                  int32_t* __restrict__ a_out) {
+                                                  int32_t* __restrict__ a_out, int n_seq,
+                                                  int64_t seq_words) {
   constexpr int DH = DHW * 64;
   constexpr int NT = DH / 16;
   constexpr int NTH = NW * 64;
@@ -55,8 +58,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   // neighbouring heads share key lines: consecutive logical ids, head fastest
   const int nwg = gridDim.x * gridDim.y * gridDim.z;
   const int lid = xcd_order(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z), nwg);
-  const int h = lid % gridDim.x, qb = (lid / gridDim.x) % gridDim.y,
+  const int h = lid % gridDim.x, qbg = (lid / gridDim.x) % gridDim.y,
             t = lid / (gridDim.x * gridDim.y);
+  const int qbps = gridDim.y / n_seq;               // query blocks per sequence
+  const int sq = qbg / qbps, qb = qbg - sq * qbps;  // sequence, block within it
+  const int Mt = n_seq * M, r0 = sq * M;            // rows per timestep, first row of sq
+  kc += sq * seq_words;
+  vt += sq * seq_words;
   const int d = H * DH, dw = d / 64;
   const int capw = (int)(cap / 64);
   const int J = C + M;
@@ -66,7 +74,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   const int iq = qb * 16 + c;
   uint64_t qw[DHW];
 #pragma unroll
-  for (int w = 0; w < DHW; ++w) qw[w] = q[((size_t)t * M + min(iq, M - 1)) * dw + h * DHW + w];
+  for (int w = 0; w < DHW; ++w)
+    qw[w] = q[((size_t)t * Mt + r0 + min(iq, M - 1)) * dw + h * DHW + w];
   for (int i = tid; i < 16 * DH; i += NTH) (&sNum[0][0])[i] = 0;
   if (tid < 16) sDen[tid] = 0;
   for (int i = tid; i < DH; i += NTH) sCnt[i] = 0;
@@ -138,28 +147,54 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
     const int iq2 = qb * 16 + qi;
     if (iq2 < M) {
       const long long num = (long long)sNum[qi][ch] + 128LL * sCnt[ch];
-      a_out[((size_t)t * M + iq2) * d + h * DH + ch] = attn_norm(num, sDen[qi], small);
+      a_out[((size_t)t * Mt + r0 + iq2) * d + h * DH + ch] = attn_norm(num, sDen[qi], small);
     }
   }
 }
 
 // waves per workgroup: 16 for dh = 64; 8 for dh = 128 (its 16 keys of two
-// words per lane need more than the 128 registers of a 1024-thread group)
+// words per lane need more than the 128 registers of a 1024-thread group);
+// halved while the grid would not fit the chip in one round (many sequences:
+// fewer waves per workgroup take more key chunks each, the workgroups of all
+// sequences run at once)
 constexpr int kAttnWaves64 = 16, kAttnWaves128 = 8;
+// waves resident at once: 256 CUs x 16 (the kernels' registers allow 4-5
+// waves per SIMD)
+constexpr long long kAttnResidentWaves = 256LL * 16;
+
+struct AttnLaunch {
+  const uint64_t* q;
+  const uint64_t* kc;
+  const uint64_t* vt;
+  int64_t cap;
+  int T, M, C, H;
+  const uint8_t* lut;
+  int32_t* a_out;
+  int n_seq;
+  int64_t seq_words;
+};
+
+template <int DHW, int NW>
+static void attn_launch(const dim3& grid, const AttnLaunch& l, hipStream_t st) {
+  hipLaunchKernelGGL((k_attn<DHW, NW>), grid, dim3(NW * 64), 0, st, l.q, l.kc, l.vt, l.cap, l.T, l.M,
+                     l.C, l.H, l.lut, l.a_out, l.n_seq, l.seq_words);
+}
 
 nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,
                          int64_t cap, int T, int M, int C, int H, int dh, const uint8_t* lut,
-                         int32_t* a_out, hipStream_t st) {
-  const dim3 grid(H, (M + 15) / 16, T);
-  switch (dh / 64) {
-    case 1:
-      hipLaunchKernelGGL((k_attn<1, kAttnWaves64>), grid, dim3(kAttnWaves64 * 64), 0, st, q, k_cache,
-                         vt_cache, cap, T, M, C, H, lut, a_out);
-      break;
-    case 2:
-      hipLaunchKernelGGL((k_attn<2, kAttnWaves128>), grid, dim3(kAttnWaves128 * 64), 0, st, q, k_cache,
-                         vt_cache, cap, T, M, C, H, lut, a_out);
-      break;
+                         int32_t* a_out, hipStream_t st, int n_seq, int64_t seq_words) {
+  if (n_seq < 1) return NMDLM_ERR_INVALID_ARG;
+  const dim3 grid(H, n_seq * ((M + 15) / 16), T);
+  const long long wgs = (long long)grid.x * grid.y * grid.z;
+  int nw = (dh == 64) ? kAttnWaves64 : kAttnWaves128;
+  while (nw > 4 && wgs * nw > kAttnResidentWaves) nw >>= 1;
+  const AttnLaunch l{q, k_cache, vt_cache, cap, T, M, C, H, lut, a_out, n_seq, seq_words};
+  switch (dh / 64 * 100 + nw) {
+    case 116: attn_launch<1, 16>(grid, l, st); break;
+    case 108: attn_launch<1, 8>(grid, l, st); break;
+    case 104: attn_launch<1, 4>(grid, l, st); break;
+    case 208: attn_launch<2, 8>(grid, l, st); break;
+    case 204: attn_launch<2, 4>(grid, l, st); break;
     default:
       return NMDLM_ERR_UNSUPPORTED;
   }

@@ -79,6 +79,8 @@ enum EpiMode : int {
 //   transposed : position-packed cache: bit (pos0+m)%64 of the word
 //                ptr[t*ld_t + ch*ld_m + ((pos0+m)/64)*ld_p] holds channel ch
 //                of token m (word-major caches: ld_m = 1, ld_p = channels)
+//   sequences  : with seq_len > 0, token m is token m % seq_len of sequence
+//                m / seq_len, whose words start ld_s words further
 struct SpikeSeg {
   uint64_t* ptr;
   int64_t ld_t;
@@ -87,6 +89,8 @@ struct SpikeSeg {
   int32_t transposed;
   int32_t pos0;
   int32_t ld_p;
+  int32_t seq_len;
+  int64_t ld_s;
 };
 
 struct QbsmArgs {
@@ -171,6 +175,8 @@ struct QbsmCall {
   hipEvent_t ev_begin;    // recorded around the product kernel when non-null
   hipEvent_t ev_end;
   const uint64_t* s_neg;  // ternary input: -1 spikes [T][M][ceil(K/64)] (s_in: +1), or null
+  int seq_len;            // tokens per sequence when M holds several (0: one sequence); a
+                          // channel-major output segment keeps row blocks within a sequence
   const uint64_t* u_in;   // partial unions of s_in [u_nparts][ceil(K/64)] or null
   int u_nparts;
   uint64_t* u_out;        // where to write the partial unions of the output
@@ -218,10 +224,12 @@ nmdlm_status launch_if(const int32_t* cur, int T, int M, int N, int32_t theta,
                        uint64_t* u_out = nullptr);
 nmdlm_status launch_qnl(const int32_t* x, int64_t n, int shift, int mode,
                         const uint8_t* lut, uint8_t* y, hipStream_t st);
+// n_seq sequences of M queries each (rows sequence-major); the caches of
+// sequence s start s * seq_words words after k_cache / vt_cache
 nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache,
                          const uint64_t* vt_cache, int64_t cap, int T, int M, int C,
                          int H, int dh, const uint8_t* lut, int32_t* a_out,
-                         hipStream_t st);
+                         hipStream_t st, int n_seq = 1, int64_t seq_words = 0);
 // attention with the IF of its output fused in (spikes and per-token union
 // over t); NMDLM_ERR_UNSUPPORTED when T*16*dh partial sums exceed its LDS
 nmdlm_status launch_attn_if(const uint64_t* q, const uint64_t* k_cache, const uint64_t* vt_cache,

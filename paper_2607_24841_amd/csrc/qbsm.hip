@@ -405,7 +405,7 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
     return;
   }
   const int segi = (a.mode == EPI_CUR) ? 0 : n0 / a.seg_w;
-  const SpikeSeg seg = a.seg[segi];
+  SpikeSeg seg = a.seg[segi];
   const int wseg = (n0 - segi * a.seg_w) >> 6;
   const int bias_n = ep.bias[col];
   const int theta = ep.theta[col];
@@ -448,7 +448,10 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
           if (!tr) {
             const uint64_t word = __builtin_amdgcn_ballot_w64(s);
             uor |= word;
-            if (lane == 0) seg.ptr[t * seg.ld_t + (int64_t)m * seg.ld_m + wseg] = word;
+            const int64_t mo = seg.seq_len > 0
+                                   ? (int64_t)(m / seg.seq_len) * seg.ld_s + (int64_t)(m % seg.seq_len) * seg.ld_m
+                                   : (int64_t)m * seg.ld_m;
+            if (lane == 0) seg.ptr[t * seg.ld_t + mo + wseg] = word;
           } else if (s) {
             vb[t] |= 1u << ml;
           }
@@ -465,7 +468,11 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
     __syncthreads();
     if (wave == 0 && nv) {
       const int ch = n - segi * a.seg_w;
-      const int p0 = seg.pos0 + y * a.Mb;
+      // several sequences: the row block lies within sequence (y Mb) / seq_len
+      const int yb = y * a.Mb;
+      const int sq = seg.seq_len > 0 ? yb / seg.seq_len : 0;
+      const int p0 = seg.pos0 + (seg.seq_len > 0 ? yb - sq * seg.seq_len : yb);
+      seg.ptr += (int64_t)sq * seg.ld_s;
       const int nvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the block, <= 32
       if (tr_bytes) {
         // p0 is a multiple of 8: store the (up to 4) bytes holding a token of
@@ -1457,6 +1464,15 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
         }
       }
     }
+    if (!found) {
+      // no height keeps the grid resident: when even the tallest tiles
+      // oversubscribe the chip, they re-read each weight tile the fewest times
+      const int r = std::min(rt_full, 4), mb = (16 * r) / c.T;
+      if (mb >= 1) {
+        const long long wgs = (long long)gx * ((c.M + mb - 1) / mb);
+        if (wgs * words_waves(r, Kw) * 64 > (long long)kCus * kThreadsPerCu) RT = r;
+      }
+    }
     // a channel-major output segment is written in whole bytes when a row
     // block's tokens fill them: take the fewest rows that do, if the grid
     // keeps >= 256 workgroups
@@ -1476,6 +1492,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   }
   while (RT > 1 && 16 * RT / 2 >= R && 16 * RT / 2 >= c.T) RT >>= 1;  // no empty tiles
   while (has_tr && RT > 1 && (16 * RT) / c.T > 32) RT >>= 1;  // channel-major: <= 32 tokens
+  if (has_tr && c.seq_len > 0) {
+    // several sequences: a channel-major segment keeps every row block
+    // within one sequence
+    while (RT > 1 && c.seq_len % ((16 * RT) / c.T) != 0) RT >>= 1;
+    if (16 * RT < c.T || c.seq_len % ((16 * RT) / c.T) != 0) return NMDLM_ERR_UNSUPPORTED;
+  }
   const bool tern = c.s_neg != nullptr;
   if (tern) {
     // ternary input: the word product only (both spike planes staged)

@@ -10,13 +10,14 @@
 
 namespace nmdlm {
 
-// X[t,m,:] = E[token_m][t] OR the position spike of (pos0+m, t); masked
-// positions use the mask token (id V).
+// X[t,m,:] = E[token_m][t] OR the position spike of (pos0 + m % Mseq, t)
+// (M rows: sequences of Mseq tokens one after the other); masked positions
+// use the mask token (id V).
 __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ emb,
                                                   const int32_t* __restrict__ pos_ch,
                                                   const int32_t* __restrict__ tokens,
                                                   const uint8_t* __restrict__ masked, int V, int T,
-                                                  int M, int dw, int pos0,
+                                                  int M, int Mseq, int dw, int pos0,
                                                   uint64_t* __restrict__ X) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   const long long total = (long long)T * M * dw;
@@ -27,7 +28,7 @@ __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ e
   int tok = (masked && masked[m]) ? V : (tokens ? tokens[m] : V);
   tok = min(max(tok, 0), V);
   uint64_t word = emb[((size_t)tok * T + t) * dw + w];
-  const int pc = pos_ch[(size_t)(pos0 + m) * T + t];
+  const int pc = pos_ch[(size_t)(pos0 + m % Mseq) * T + t];
   if ((pc >> 6) == w) word |= 1ull << (pc & 63);
   X[i] = word;
 }
@@ -113,7 +114,8 @@ __global__ __launch_bounds__(kConfThreads) void k_conf(const float* __restrict__
 // Top-k unmasking by one wave: among the positions still masked, take the
 // highest confidence (ties -> smaller position) k times.  Lane l owns the
 // positions l + 64 j (j < 64, so M <= kUnmaskMaxM) and keeps their masked
-// flags in a register mask.
+// flags in a register mask.  Workgroup s takes sequence s (its M tokens at
+// s * M, its k chosen positions at s * k).
 constexpr int kUnmaskMaxM = 64 * 64;
 static_assert(kUnmaskMaxM >= NMDLM_MAX_HEAD_M, "unmask register mask covers every head step");
 
@@ -123,6 +125,12 @@ __global__ __launch_bounds__(64) void k_unmask(int32_t* __restrict__ tokens,
                                                const double* __restrict__ conf, int M, int k,
                                                int32_t* __restrict__ chosen) {
   const int lane = threadIdx.x;
+  const size_t so = (size_t)blockIdx.x * M;
+  tokens += so;
+  masked += so;
+  pred += so;
+  conf += so;
+  if (chosen) chosen += (size_t)blockIdx.x * k;
   uint64_t mine = 0ull;
   for (int jj = 0, m = lane; m < M; ++jj, m += 64)
     if (masked[m]) mine |= 1ull << jj;
@@ -232,6 +240,8 @@ static SpikeSeg natural_seg(uint64_t* p, int64_t ld_t, int64_t ld_m, int32_t the
   s.transposed = 0;
   s.pos0 = 0;
   s.ld_p = 0;
+  s.seq_len = 0;
+  s.ld_s = 0;
   return s;
 }
 
@@ -265,6 +275,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.ev_begin = nullptr;
   c.ev_end = nullptr;
   c.s_neg = nullptr;
+  c.seq_len = 0;
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;
@@ -281,9 +292,12 @@ static void attach_events(QbsmCall& c, const nmdlm_step_io* io, int i) {
 
 nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws, size_t ws_bytes,
                              hipStream_t st) {
-  const int T = md->T, M = io->M, C = io->C, d = md->d, F = md->F, H = md->H;
+  // Ms tokens in each of n_seq sequences; every product takes all M rows
+  const int T = md->T, Ms = io->M, n_seq = std::max(io->n_seq, 1), M = n_seq * Ms, C = io->C;
+  const int d = md->d, F = md->F, H = md->H;
   const int dh = d / H, dw = d / 64, Fw = (F + 63) / 64;
   const int64_t cap = md->cache_cap, capw = cap / 64;
+  const int64_t seq_words = (int64_t)T * cap * dw;  // one sequence's K (and V) cache
   const bool head = !(io->flags & NMDLM_NO_HEAD);
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
@@ -297,7 +311,8 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
   if (!X) {
     const long long total = (long long)T * M * dw;
     hipLaunchKernelGGL(k_assemble, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
-                       md->emb, md->pos_ch, io->tokens, io->masked, md->V, T, M, dw, io->pos0, b.X);
+                       md->emb, md->pos_ch, io->tokens, io->masked, md->V, T, M, Ms, dw, io->pos0,
+                       b.X);
     if ((rc = hip_status()) != NMDLM_OK) return rc;
     X = b.X;
   }
@@ -323,18 +338,25 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     qkv.seg[2].transposed = 1;
     qkv.seg[2].ld_p = d;
     qkv.seg[2].pos0 = C;
+    if (n_seq > 1) {
+      qkv.seq_len = Ms;
+      for (int i = 1; i < 3; ++i) {
+        qkv.seg[i].seq_len = Ms;
+        qkv.seg[i].ld_s = seq_words;
+      }
+    }
     qkv.u_in = uX;
     qkv.u_nparts = uX_parts;
     attach_events(qkv, io, 4 * l + 0);
     if ((rc = launch_qbsm(qkv, b.qs, st)) != NMDLM_OK) return rc;
 
     rc = NMDLM_ERR_UNSUPPORTED;
-    if (io->flags & NMDLM_ATTN_FUSED)
+    if ((io->flags & NMDLM_ATTN_FUSED) && n_seq == 1)
       rc = launch_attn_if(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att,
                           ly.theta_a, b.A, b.uA, st);
     if (rc == NMDLM_ERR_UNSUPPORTED) {
-      if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, M, C, H, dh, ly.lut_att, b.a,
-                            st)) != NMDLM_OK)
+      if ((rc = launch_attn(b.Q, ly.k_cache, ly.vt_cache, cap, T, Ms, C, H, dh, ly.lut_att, b.a,
+                            st, n_seq, seq_words)) != NMDLM_OK)
         return rc;
       rc = launch_if(b.a, T, M, d, ly.theta_a, nullptr, nullptr, nullptr, b.A, st, b.uA);
     }
@@ -401,8 +423,8 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
   if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
   hipLaunchKernelGGL(k_conf, dim3(M), dim3(kConfThreads), 0, st, logits, md->V, pred, conf);
   if ((rc = hip_status()) != NMDLM_OK) return rc;
-  hipLaunchKernelGGL(k_unmask, dim3(1), dim3(64), 0, st, io->tokens, io->masked, pred, conf, M,
-                     io->k_unmask, io->unmasked_pos);
+  hipLaunchKernelGGL(k_unmask, dim3(n_seq), dim3(64), 0, st, io->tokens, io->masked, pred, conf,
+                     Ms, io->k_unmask, io->unmasked_pos);
   return hip_status();
 }
 

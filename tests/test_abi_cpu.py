@@ -31,7 +31,7 @@ def test_exports_every_declared_function(lib):
     assert set(B.EXPORTS) <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.nmdlm_abi_version() == 2
+    assert lib.nmdlm_abi_version() == 3
     assert lib.nmdlm_status_string(0) == b"ok"
     assert lib.nmdlm_status_string(3).startswith(b"workspace")
 
@@ -123,6 +123,26 @@ def test_block_step_argument_errors(lib):
     big = B.step_io(4097, 0, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
     nb = lib.nmdlm_block_step_workspace_size(C.byref(mh), 4097, 0)
     assert nb > 0 and call(mh, big, nb=nb) == B.NMDLM_ERR_UNSUPPORTED
+
+
+def test_batched_step_argument_errors(lib):
+    L = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 200, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE, FAKE)
+    layers = (B.Layer * 1)(L)
+    m1 = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, layers, None, None, None, None)   # max_seq 0
+    m4 = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, layers, None, None, None, None, 4)
+    nb = lib.nmdlm_block_step_workspace_size(C.byref(m4), 4 * 16, B.NMDLM_NO_HEAD)
+    assert nb > lib.nmdlm_block_step_workspace_size(C.byref(m4), 16, B.NMDLM_NO_HEAD)
+    call = lambda mm, ii: lib.nmdlm_block_step(C.byref(mm), C.byref(ii), FAKE, nb, None)
+    io = lambda M, n: B.step_io(M, 512, flags=B.NMDLM_NO_HEAD, x_in=FAKE, n_seq=n)
+    assert call(m1, io(16, 2)) == B.NMDLM_ERR_INVALID_ARG          # caches hold one sequence
+    assert call(m4, io(16, 5)) == B.NMDLM_ERR_INVALID_ARG          # more than max_seq
+    assert call(m4, io(16, -1)) == B.NMDLM_ERR_INVALID_ARG
+    assert call(m4, io(6, 2)) == B.NMDLM_ERR_UNSUPPORTED           # T = 4: M a multiple of 4
+    m4.max_seq = -1
+    assert call(m4, io(16, 1)) == B.NMDLM_ERR_INVALID_ARG
+    m4.max_seq = 4
+    small = lib.nmdlm_block_step_workspace_size(C.byref(m4), 16, B.NMDLM_NO_HEAD)
+    assert lib.nmdlm_block_step(C.byref(m4), C.byref(io(16, 4)), FAKE, small, None) == B.NMDLM_ERR_WORKSPACE
 
 
 def test_ternary_argument_errors(lib):

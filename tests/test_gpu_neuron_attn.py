@@ -126,6 +126,10 @@ ATTN = [  # T, M, C, H, dh, p
     (4, 16, 512, 16, 64, 0.3),     # the one-block step (d=1024, 16 heads of 64)
     (4, 32, 1024, 16, 128, 0.4),   # the 12-layer model step (16 heads of 128)
     (3, 17, 63, 2, 128, 0.05),
+    # grids beyond one round of the chip: 8 and 4 waves per workgroup
+    (4, 192, 64, 8, 64, 0.3),
+    (4, 300, 40, 8, 64, 0.25),
+    (4, 520, 30, 4, 128, 0.3),
 ]
 
 

@@ -206,10 +206,15 @@ class BlockCase:
     X_blk: np.ndarray     # bool [T][M][d] block inputs
 
 
+def block_inputs(seed: int, C: int, M: int, d: int, T: int = 4, density: float = 0.10):
+    """Context and block input spikes of one sequence (bool [T][C][d], [T][M][d])."""
+    return (bernoulli(stream(seed, 0), density, (T, C, d)),
+            bernoulli(stream(seed, 1), density, (T, M, d)))
+
+
 def block_case(seed: int = SEEDS["block"], C: int = 512, M: int = 16, d: int = 1024,
             H: int = 16, F: int = 4096, T: int = 4, density: float = 0.10) -> BlockCase:
-    X_ctx = bernoulli(stream(seed, 0), density, (T, C, d))
-    X_blk = bernoulli(stream(seed, 1), density, (T, M, d))
+    X_ctx, X_blk = block_inputs(seed, C, M, d, T, density)
     layer = make_layer(seed, 0, d, F, H)
     return BlockCase(T, C, M, layer, X_ctx, X_blk)
 
