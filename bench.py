@@ -163,6 +163,23 @@ def _graph(fn):
     return g
 
 
+def _time_eager(fn, reps):
+    """Median over reps of fn() issued directly, in ms (torch events)."""
+    import numpy as np
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(reps):
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
+
+
 def _time_graph(g, reps):
     """Median over reps of one replay, in ms (torch events on the replay stream)."""
     import numpy as np
@@ -218,10 +235,15 @@ def bench_ffn_sweep(args):
                 B.nmdlm_qbsm(xd, T, Bk, F, W_dn[c], d, d, theta=th_dn, s_out=sd, stats=st[1],
                              flags=args.flags, ws=ws)
 
-            g_up = _graph(lambda: [up(c) for c in range(n_copies)])
-            g_dn = _graph(lambda: [dn(c) for c in range(n_copies)])
-            t_up = _time_graph(g_up, args.reps) / n_copies
-            t_dn = _time_graph(g_dn, args.reps) / n_copies
+            if args.eager:           # one dispatch per launch (for counter passes)
+                t_up = _time_eager(lambda: [up(c) for c in range(n_copies)], args.reps) / n_copies
+                t_dn = _time_eager(lambda: [dn(c) for c in range(n_copies)], args.reps) / n_copies
+            else:
+                g_up = _graph(lambda: [up(c) for c in range(n_copies)])
+                g_dn = _graph(lambda: [dn(c) for c in range(n_copies)])
+                t_up = _time_graph(g_up, args.reps) / n_copies
+                t_dn = _time_graph(g_dn, args.reps) / n_copies
+                del g_up, g_dn
             k = st.cpu().numpy()
             rec = {"B": Bk, "density": pt.density}
             for nm, row, t, X in (("up", k[0], t_up, pt.X_up), ("dn", k[1], t_dn, pt.X_dn)):
@@ -238,7 +260,6 @@ def bench_ffn_sweep(args):
                            "model_regime_MI355X": mod["MI355X"]["regime"]}
             rec["tokens_per_s"] = Bk / ((t_up + t_dn) * 1e-3)
             points.append(rec)
-            del g_up, g_dn
     head = [p for p in points if p["B"] == 64 and p["density"] == 0.30][0]
     best = max((p[m]["GBps"], p, m) for p in points for m in ("up", "dn"))
     out = {
@@ -249,7 +270,8 @@ def bench_ffn_sweep(args):
         "data": "synthetic",
         "config": {"workload": "FFN weight-traffic sweep d=4096->14336->4096, T=4, "
                                "Beta(0.5,8) per-neuron rates; value at B=64, density 0.30",
-                   "weight_copies_rotated": n_copies},
+                   "weight_copies_rotated": n_copies,
+                   "issue": "eager" if args.eager else "hip_graph"},
         "weight_skip_fraction": 1.0 - (head["up"]["touched_bytes"] + head["dn"]["touched_bytes"])
         / (head["up"]["k_total"] * F + head["dn"]["k_total"] * d),
         "roofline": {"kernel": "k_qbsm (int8 MFMA spike product with fused IF epilogue)",
