@@ -100,6 +100,27 @@ def product_traffic():
     return None
 
 
+def stream_copy_gbps(torch, nbytes=2 << 30, reps=10):
+    """A measured streaming rate of the device's HBM: the median of a
+    device-to-device copy of nbytes, counting the bytes read and written, in
+    GB/s."""
+    import numpy as np
+    x = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(reps):
+        e0.record()
+        y.copy_(x)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    del x, y
+    return 2 * nbytes / (float(np.median(ts)) * 1e-3) / 1e9
+
+
 def product_bytes(k_total, k_active, n, T, M):
     """Algorithmic bytes of one product launch: active weight rows, packed
     input spikes, packed output spikes."""
@@ -691,6 +712,22 @@ def bench_block(args):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_per_step = 1e3 * dt / args.steps
+    # distribution over graph replays (each a run of args.copies steps),
+    # after the timed region
+    pct = None
+    if not args.eager:
+        g = graph_for(args.copies)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        per = []
+        for _ in range(20):
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            per.append(1e3 * e0.elapsed_time(e1) / args.copies)
+        pct = {"p10": float(np.percentile(per, 10)), "p50": float(np.percentile(per, 50)),
+               "p90": float(np.percentile(per, 90)), "replays": len(per),
+               "steps_per_replay": args.copies}
 
     st = stats.cpu().numpy()
     k_total, k_active, n_col = st[:, 0], st[:, 1], st[:, 2]
@@ -738,6 +775,7 @@ def bench_block(args):
                                        sigma=sig[p])
                for p, (nm, di, do) in enumerate(dims)]
     paper_model = perf_model.block_report(reports, measured_step_us=1e3 * ms_per_step)
+    stream = stream_copy_gbps(torch)
 
     out = {
         "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
@@ -759,6 +797,7 @@ def bench_block(args):
             "block_tokens": M, "context_tokens": C_ctx, "timesteps": T,
             "layer_copies_rotated": args.copies, "issue": "eager" if args.eager else "hip_graph",
         },
+        "step_us_percentiles": pct,
         "weight_skip_fraction": skip,
         "touched_weight_bytes_per_step": w_touched,
         "touched_weight_GBps": w_touched / (ms_per_step * 1e-3) / 1e9,
@@ -770,6 +809,8 @@ def bench_block(args):
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
+            "stream_copy_GBps": stream,
+            "frac_of_stream_copy": achieved / stream,
             "avg_launch_ms": avg_ms,
             "launches_timed": len(dur),
             "timing_issue": timing_issue,

@@ -138,3 +138,44 @@ def test_batched_generation_matches_oracle():
         ids_ref, log_ref = O.generate(m, prompts[s], n_blocks=3, B=8, steps=4, k_unmask=2)
         assert_same(ids[s], ids_ref, f"ids of sequence {s}")
         assert all(np.array_equal(a[s], b) for a, b in zip(log, log_ref)), s
+
+
+def test_batched_step_graph_replays_match_eager():
+    # the batched step captured in a HIP graph: every replay equals the eager
+    # step (with eager work and synchronisations between the replays)
+    torch, B = need_gpu()
+    n, C, M, d, H, F = 3, 60, 8, 128, 2, 256
+    cases = _cases(n, C, M, d, H, F, seed=91)
+    L, T = cases[0].layer, cases[0].T
+    dm = B.DeviceModel([L], T, C + M, d, H, F, max_seq=n)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, n * C, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, n * M, B.NMDLM_NO_HEAD)))
+    xc = np.concatenate([c.X_ctx for c in cases], axis=1)
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, n_seq=n,
+                                     x_in=B.to_dev_bits(synth.pack_bits(xc))), ws)
+    xb = B.to_dev_bits(synth.pack_bits(np.concatenate([c.X_blk for c in cases], axis=1)))
+    y = torch.zeros((T, n * M, d // 64), dtype=torch.int64, device="cuda")
+    io = B.step_io(M, C, flags=B.NMDLM_NO_HEAD, n_seq=n, x_in=xb, y_out=y)
+    B.nmdlm_block_step(dm, io, ws)
+    torch.cuda.synchronize()
+    eager = y.clone()
+    Y = synth.unpack_bits(B.from_dev_bits(eager), d)
+    for s, c in enumerate(cases):
+        kc, vc = O.new_caches(1, T, C + M, d)
+        O.prefill(c.X_ctx, [L], kc, vc)
+        assert_same(Y[:, s * M:(s + 1) * M], O.layer_forward(c.X_blk, L, kc[0], vc[0], C).Y,
+                    f"eager Y of sequence {s}")
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        B.nmdlm_block_step(dm, io, ws)
+    torch.cuda.current_stream().wait_stream(st)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        B.nmdlm_block_step(dm, io, ws)
+    for r in range(4):
+        y.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager), f"replay {r} differs from the eager step"
