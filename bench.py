@@ -158,8 +158,8 @@ def cpu_baseline(case, seconds: float):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              f"layout is described in DESIGN.md but not built.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the step over "
+              f"several GPUs is not built.", file=sys.stderr)
         sys.exit(2)
     {"block": bench_block, "ffn-sweep": bench_ffn_sweep, "mdlm12-step": bench_mdlm12_step,
      "mdlm24-generate": bench_mdlm24_generate,
