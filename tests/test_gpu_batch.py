@@ -23,10 +23,10 @@ def _seq_caches_to_host(dm, s, d, J):
     return ks, vs
 
 
-def _cases(n, C, M, d, H, F, seed):
+def _cases(n, C, M, d, H, F, seed, T=4):
     """n sequences sharing one layer's weights, each with its own context and
     block inputs (seeded per sequence)."""
-    base = synth.block_case(seed=seed, C=C, M=M, d=d, H=H, F=F)
+    base = synth.block_case(seed=seed, C=C, M=M, d=d, H=H, F=F, T=T)
     out = []
     for s in range(n):
         xc, xb = synth.block_inputs(seed + 100 * (s + 1), C, M, d, base.T)
@@ -34,18 +34,21 @@ def _cases(n, C, M, d, H, F, seed):
     return out
 
 
-@pytest.mark.parametrize("n,C,M,d,H,F,flags", [
-    (3, 60, 8, 128, 2, 256, 0),          # block positions 60..67 cross a value-cache word
-    (2, 64, 16, 256, 4, 512, 0),         # whole-byte value-cache stores
-    (4, 40, 12, 128, 2, 256, 2 << 16),   # forced 2-row tiles: 8-token row blocks straddle the
-                                         # 12-token sequences (QKV falls back to 4-token blocks)
-    (5, 32, 4, 128, 2, 256, 1),          # dense product
-    (4, 512, 16, 1024, 16, 4096, 0),     # full-size layer, four sequences
-    (16, 64, 4, 1024, 16, 4096, 0),      # 16 sequences: attention beyond one round of the chip
-], ids=["straddle", "bytes", "rt2-ragged", "dense", "full-4seq", "16seq"])
-def test_batched_block_step_matches_independent_sequences(n, C, M, d, H, F, flags):
+@pytest.mark.parametrize("n,C,M,d,H,F,flags,T", [
+    (3, 60, 8, 128, 2, 256, 0, 4),          # block positions 60..67 cross a value-cache word
+    (2, 64, 16, 256, 4, 512, 0, 4),         # whole-byte value-cache stores
+    (4, 40, 12, 128, 2, 256, 2 << 16, 4),   # forced 2-row tiles: 8-token row blocks straddle the
+                                            # 12-token sequences (QKV falls back to 4-token blocks)
+    (5, 32, 4, 128, 2, 256, 1, 4),          # dense product
+    (4, 512, 16, 1024, 16, 4096, 0, 4),     # full-size layer, four sequences
+    (16, 64, 4, 1024, 16, 4096, 0, 4),      # 16 sequences: attention beyond one round of the chip
+    (3, 62, 6, 128, 2, 256, 0, 8),          # T = 8: 2-token row blocks, positions cross a word
+    (3, 35, 5, 128, 2, 256, 0, 3),          # T = 3: 5-token row blocks (16 // 3)
+    (2, 48, 16, 256, 2, 512, 0, 4),         # heads of 128 channels
+], ids=["straddle", "bytes", "rt2-ragged", "dense", "full-4seq", "16seq", "T8", "T3", "dh128"])
+def test_batched_block_step_matches_independent_sequences(n, C, M, d, H, F, flags, T):
     torch, B = need_gpu()
-    cases = _cases(n, C, M, d, H, F, seed=71)
+    cases = _cases(n, C, M, d, H, F, seed=71, T=T)
     L, T = cases[0].layer, cases[0].T
     dm = B.DeviceModel([L], T, C + M, d, H, F, max_seq=n)
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, n * C, B.NMDLM_NO_HEAD),
