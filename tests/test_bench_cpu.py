@@ -1,0 +1,45 @@
+"""Host-side checks of bench.py's contract (no GPU): more than one GPU is
+refused with a message, the workloads parse, and the product-source digest
+that guards the stored HBM traffic figure is the one of the sources."""
+import hashlib
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout.strip() == ""
+
+
+@pytest.mark.parametrize("w", ["block", "ffn-sweep", "mdlm12-step", "mdlm24-generate",
+                               "e2d2-generate", "ternary-ffn", "block-batch"])
+def test_workloads_parse(w, monkeypatch):
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", w, "--flags", "0x10000"])
+    a = bench.parse()
+    assert a.workload == w and a.flags == 0x10000 and a.gpus == 1
+
+
+def test_traffic_digest_covers_the_product_sources():
+    h = hashlib.sha256()
+    for rel in bench.PRODUCT_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    assert bench.product_sources_sha256() == h.hexdigest()
+    # the stored figure is reported only for the sources it was measured on
+    assert bench.product_traffic() == (bench.TRAFFIC["bytes_per_launch"]
+                                       if bench.TRAFFIC["sources_sha256"] == h.hexdigest() else None)
+
+
+def test_product_bytes_is_the_row_load_rule():
+    # K_active * N weight bytes + packed spikes in and out (T*M rows)
+    assert bench.product_bytes(1024, 100, 512, 4, 16) == 100 * 512 + 4 * 16 * 16 * 8 + 4 * 16 * 8 * 8
