@@ -1520,9 +1520,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   if ((size_t)tiles > scr.n_counters) return NMDLM_ERR_WORKSPACE;
   if (gy_out) *gy_out = gy;
 
-  // K splits (requested by the flags; at the measured shapes the atomic
-  // accumulation costs more round trips than the split saves)
+  // K splits: requested by the flags, or, unrequested, four ways for a short
+  // grid over a long K (at most 64 output tiles, K of 128 words or more:
+  // 256 workgroups then share the weight rows instead of 64).  Elsewhere the
+  // atomic accumulation costs more round trips than the split saves.
   int P = (int)((c.flags >> NMDLM_SPLIT_SHIFT) & 0xFFu);
+  if (P == 0 && path == 3 && !tern && tiles <= 64 && Kw >= 128) P = 4;
   P = std::max(1, std::min(P, Kw));
   const size_t acc_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one accumulator tile per output tile
   if (P > 1 && (!scr.part || scr.part_elems < acc_elems)) P = 1;
