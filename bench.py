@@ -281,6 +281,21 @@ def bench_ffn_sweep(args):
                            "model_regime_MI355X": mod["MI355X"]["regime"]}
             rec["tokens_per_s"] = Bk / ((t_up + t_dn) * 1e-3)
             points.append(rec)
+    # time against the active-row fraction per block size and product: a
+    # least-squares line t = t0 + slope * (K_active / K) over the densities
+    lin = []
+    for Bk in sorted({p["B"] for p in points}):
+        for nm in ("up", "dn"):
+            xs = np.array([p[nm]["k_active"] / p[nm]["k_total"] for p in points if p["B"] == Bk])
+            ys = np.array([p[nm]["us"] for p in points if p["B"] == Bk])
+            slope, t0 = np.polyfit(xs, ys, 1)
+            fit = t0 + slope * xs
+            ss = float(((ys - ys.mean()) ** 2).sum())
+            r2 = 1.0 - float(((ys - fit) ** 2).sum()) / ss if ss > 0 else 1.0
+            lin.append({"B": Bk, "product": nm, "active_frac": [round(float(x), 4) for x in xs],
+                        "us": [round(float(y), 2) for y in ys], "t0_us": float(t0),
+                        "slope_us_per_active_frac": float(slope), "r2": r2,
+                        "scaling_share_at_max": float(slope * xs.max() / ys.max())})
     head = [p for p in points if p["B"] == 64 and p["density"] == 0.30][0]
     best = max((p[m]["GBps"], p, m) for p in points for m in ("up", "dn"))
     out = {
@@ -300,6 +315,7 @@ def bench_ffn_sweep(args):
                      "frac": best[0] / HBM_PEAK_GBPS, "traffic": None,
                      "at": f"B={best[1]['B']} density={best[1]['density']} {best[2]}"},
         "sweep": points,
+        "time_vs_active_fraction": lin,
     }
     print(json.dumps(out), flush=True)
 
