@@ -66,6 +66,7 @@ def test_qbsm_argument_errors(lib):
     assert _qbsm(lib, s_in=None) == B.NMDLM_ERR_INVALID_ARG
     assert _qbsm(lib, T=0) == B.NMDLM_ERR_INVALID_ARG
     assert _qbsm(lib, M=-1) == B.NMDLM_ERR_INVALID_ARG
+    assert _qbsm(lib, M=0) == B.NMDLM_ERR_INVALID_ARG            # an empty block is rejected
     assert _qbsm(lib, T=9) == B.NMDLM_ERR_UNSUPPORTED
     assert _qbsm(lib, K=70000) == B.NMDLM_ERR_UNSUPPORTED
     assert _qbsm(lib, ldw=500) == B.NMDLM_ERR_INVALID_ARG          # < N

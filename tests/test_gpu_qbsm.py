@@ -100,6 +100,23 @@ def test_large_k_shapes(flags):
     _check(synth.make_qbsm_case(42, 4, 300, 700, 200, 0.05), flags=flags)
 
 
+@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS, DMA, 1], ids=["auto", "nofuse", "words", "dma", "dense"])
+def test_maximum_k(flags):
+    # K = NMDLM_MAX_K = 65536: the tile's staged spike rows exceed the word
+    # kernel's LDS, so every requested path falls back to the list kernels
+    need_gpu()
+    _check(synth.make_qbsm_case(45, 4, 2, 65536, 96, 0.003), flags=flags)
+
+
+@pytest.mark.parametrize("M,flags", [(3, 0), (9, 0), (9, 1 << 8), (3, 1)],
+                         ids=["auto-split", "auto-split-3blocks", "P1-requested", "dense-split"])
+def test_short_grid_long_k_split(M, flags):
+    # at most 64 output tiles over 128 or more words of K: unrequested, K is
+    # split four ways (K = 8257: a partial last word; N = 100: a ragged tile)
+    need_gpu()
+    _check(synth.make_qbsm_case(46, 4, M, 8257, 100, 0.02), flags=flags)
+
+
 def test_words_with_more_than_64k_lds():
     need_gpu()
     # K = 14336 with two row groups: the staged spike rows need more than
