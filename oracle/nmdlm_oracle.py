@@ -175,7 +175,8 @@ def bbm_attention(Q: np.ndarray, Kc: np.ndarray, Vc: np.ndarray, n_keys: int,
             p = lut[s]                                 # [M][n_keys]
             den = p.sum(axis=1)                        # [M]
             num = _exact_matmul(p, v)                  # [M][dh]
-            _check_int32(256 * num, "attention numerator")
+            # 256 * num <= 256 * 255 * n_keys: exact in int64 for any number
+            # of keys (it leaves int32 from about 32 thousand keys on)
             safe = np.where(den > 0, den, 1)
             a[t, :, c0:c1] = np.where(den[:, None] > 0,
                                       (256 * num) // safe[:, None], 0)
