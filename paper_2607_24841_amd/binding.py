@@ -28,6 +28,7 @@ NMDLM_NO_HEAD = 0x2
 NMDLM_SPLIT_SHIFT = 8
 NMDLM_ROWTILE_SHIFT = 16
 NMDLM_ATTN_FUSED = 0x4
+NMDLM_MAX_HEAD_M = 4096   # block tokens of a step that runs the head
 NMDLM_PATH_SHIFT = 20
 NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-row list
 NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list

@@ -169,3 +169,13 @@ def test_ternary_argument_errors(lib):
     assert prod(K=20000) == B.NMDLM_ERR_UNSUPPORTED                # beyond the staged planes
     assert prod(ldw=500) == B.NMDLM_ERR_INVALID_ARG
     assert prod(ws=None) == B.NMDLM_ERR_WORKSPACE
+
+
+def test_binding_constants_match_the_header():
+    text = open(HEADER).read()
+    for name in ("NMDLM_FORCE_DENSE", "NMDLM_NO_HEAD", "NMDLM_ATTN_FUSED", "NMDLM_SPLIT_SHIFT",
+                 "NMDLM_ROWTILE_SHIFT", "NMDLM_MAX_HEAD_M", "NMDLM_MAX_T", "NMDLM_MAX_K"):
+        m = re.search(r"#define\s+%s\s+([0-9xXa-fA-F]+)u?" % name, text)
+        assert m, name
+        if hasattr(B, name):
+            assert getattr(B, name) == int(m.group(1).rstrip("u"), 0), name

@@ -222,3 +222,95 @@ def test_e2d2_generation_matches_oracle(n_enc, n_layers):
     ids, log = e2d2_generate(dm, n_enc, prompt, n_blocks=2, block=4, steps=4, k_unmask=1)
     assert_same(ids, ids_ref)
     assert all(np.array_equal(a, b) for a, b in zip(log, log_ref))
+
+
+# ----------------------------------------------------------------------------
+# degenerate and maximum steps
+# ----------------------------------------------------------------------------
+def _head_step(m, M, C, tok0, msk0, k, prompt=None):
+    """Run one step with head on a fresh device model (prefill of `prompt`
+    first when given); returns the device outputs as numpy arrays."""
+    torch, B = need_gpu()
+    dm = B.DeviceModel.from_mdlm(m, max(C + M, 64))
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, max(C, 1), B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, 0)))
+    if prompt is not None:
+        pr = torch.from_numpy(prompt.astype(np.int32)).cuda()
+        B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, tokens=pr,
+                                         masked=torch.zeros(C, dtype=torch.uint8, device="cuda")), ws)
+    tok = torch.from_numpy(np.asarray(tok0, dtype=np.int32)).cuda()
+    msk = torch.from_numpy(np.asarray(msk0, dtype=np.uint8)).cuda()
+    logits = torch.empty((M, m.V), dtype=torch.float32, device="cuda")
+    pred = torch.empty(M, dtype=torch.int32, device="cuda")
+    conf = torch.empty(M, dtype=torch.float64, device="cuda")
+    chosen = torch.full((max(k, 1),), -7, dtype=torch.int32, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, C, pos0=C, tokens=tok, masked=msk, k_unmask=k, logits=logits,
+                                     pred=pred, conf=conf, unmasked_pos=chosen), ws)
+    torch.cuda.synchronize()
+    return (logits.cpu().numpy(), pred.cpu().numpy(), conf.cpu().numpy(), chosen.cpu().numpy(),
+            tok.cpu().numpy(), msk.cpu().numpy().astype(bool))
+
+
+def _check_head_step(ref, out, k):
+    logits, pred, conf, chosen, tok, msk = out
+    assert_same(logits, ref.logits, "logits")
+    assert_same(pred, ref.pred, "pred")
+    assert np.allclose(conf, ref.conf, rtol=1e-12, atol=0)
+    nc = len(ref.chosen)
+    assert np.array_equal(chosen[:nc], ref.chosen) and (k == 0 or (chosen[nc:k] == -1).all())
+    assert np.array_equal(tok, ref.tokens)
+    assert np.array_equal(msk, ref.masked)
+
+
+def test_zero_layer_model():
+    # no layers: the step's output is its assembled input (NO_HEAD copies it
+    # to y_out), and the head reads the input spikes directly
+    torch, B = need_gpu()
+    m = synth.make_mdlm(35, 0, d=128, H=2, F=256, V=64, T=4, max_pos=64)
+    emb = O.unpack_model_emb(m)
+    M, C = 8, 8
+    tok0 = synth.random_tokens(62, M, m.V).astype(np.int32)
+    msk0 = np.zeros(M, dtype=bool)
+    msk0[::3] = True
+    X_ref = O.block_input(np.where(msk0, m.V, tok0), np.arange(C, C + M), emb, m.pos_ch)
+    dm = B.DeviceModel.from_mdlm(m, C + M)
+    ws = B.workspace(B.nmdlm_block_step_workspace_size(dm, M, 0))
+    y = torch.full((m.T, M, m.d // 64), -1, dtype=torch.int64, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, C, pos0=C, flags=B.NMDLM_NO_HEAD, y_out=y,
+                                     tokens=torch.from_numpy(tok0).cuda(),
+                                     masked=torch.from_numpy(msk0.astype(np.uint8)).cuda()), ws)
+    torch.cuda.synchronize()
+    assert_same(synth.unpack_bits(B.from_dev_bits(y), m.d), X_ref, "y_out of a zero-layer step")
+    kc, vc = O.new_caches(0, m.T, C + M, m.d)
+    ref = O.block_step(m, emb, tok0, msk0, C, C, kc, vc, 2)
+    _check_head_step(ref, _head_step(m, M, C, tok0, msk0, 2), 2)
+
+
+def test_single_token_block_without_unmasking():
+    # a one-token block, k_unmask = 0: predictions and confidences are
+    # produced, the token state is left as it was
+    need_gpu()
+    m = _tiny(seed=36)
+    emb = O.unpack_model_emb(m)
+    P = 12
+    prompt = synth.random_tokens(63, P, m.V)
+    kc, vc = O.new_caches(m.n_layers, m.T, P + 1, m.d)
+    O.prefill(O.block_input(prompt, np.arange(P), emb, m.pos_ch), m.layers, kc, vc)
+    tok0, msk0 = np.zeros(1, dtype=np.int32), np.ones(1, dtype=bool)
+    ref = O.block_step(m, emb, tok0, msk0, P, P, kc, vc, 0)
+    out = _head_step(m, 1, P, tok0, msk0, 0, prompt=prompt)
+    _check_head_step(ref, out, 0)
+    assert out[5].all() and (out[4] == 0).all()
+
+
+def test_head_at_maximum_block():
+    # NMDLM_MAX_HEAD_M = 4096 block tokens, all masked, all revealed in one
+    # step: the unmask wave's register mask is full
+    torch, B = need_gpu()
+    m = synth.make_mdlm(37, 1, d=128, H=2, F=256, V=64, T=4, max_pos=4096)
+    emb = O.unpack_model_emb(m)
+    M = B.NMDLM_MAX_HEAD_M
+    tok0, msk0 = np.zeros(M, dtype=np.int32), np.ones(M, dtype=bool)
+    kc, vc = O.new_caches(m.n_layers, m.T, M, m.d)
+    ref = O.block_step(m, emb, tok0, msk0, 0, 0, kc, vc, M)
+    _check_head_step(ref, _head_step(m, M, 0, tok0, msk0, M), M)
