@@ -31,13 +31,17 @@ def _planes_ref(a, K, T):
     return O.ternary_planes(q, T), S
 
 
-ENC = [(1, 1, 1, 1), (3, 63, 2, 8), (2, 65, 1, 4), (5, 300, 4, 8), (4, 4096, 2, 8), (2, 129, 3, 3)]
+ENC = [(1, 1, 1, 1), (3, 63, 2, 8), (2, 65, 1, 4), (5, 300, 4, 8), (4, 4096, 2, 8), (2, 129, 3, 3),
+       (3, 16384, 63, 8)]   # the largest D K accepted (< 2^20)
 
 
 @pytest.mark.parametrize("M,D,K,T", ENC, ids=[f"M{e[0]}D{e[1]}K{e[2]}T{e[3]}" for e in ENC])
 def test_encode_bit_exact(M, D, K, T):
     a = synth.ternary_activations(synth.stream(10 + D, M), M, D)
     a[0, : min(D, 3)] = [2 ** 31 - 1, -(2 ** 31), 7][: min(D, 3)]   # extreme magnitudes
+    if M > 1 and D > 1:
+        a[1] = 0                                                     # a single nonzero channel:
+        a[1, D // 2] = -5                                            # |q| = D K saturates at 2^T - 1
     if M > 2:
         a[2] = 0                                                     # an all-zero token
     sp, sn, ss = _encode_gpu(a, K, T)
@@ -65,7 +69,8 @@ def _product_gpu(sp, sn, T, M, K, W, flags=0):
 
 
 PROD = [(8, 4, 300, 70, 2), (8, 16, 1024, 512, 2), (4, 3, 65, 129, 1), (1, 1, 1, 1, 1),
-        (8, 9, 2000, 100, 4), (8, 64, 512, 64, 2)]
+        (8, 9, 2000, 100, 4), (8, 64, 512, 64, 2),
+        (8, 2, 16384, 64, 2)]   # K = NMDLM_MAX_TERNARY_K
 
 
 @pytest.mark.parametrize("T,M,K,N,Kq", PROD, ids=[f"T{p[0]}M{p[1]}K{p[2]}N{p[3]}" for p in PROD])
