@@ -174,6 +174,7 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
  *   resid     device spikes [T][M][ceil(N/64)] or NULL: membrane shortcut
  *   v_inout   device int32 [M][N] or NULL: initial membrane in, final out
  *   s_out     device spikes [T][M][ceil(N/64)]
+ * Limits: T <= 8192 and M * ceil(N/64) <= 2^26, else NMDLM_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------ */
 nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N,
                              int32_t theta, const int32_t* theta_vec,
@@ -213,6 +214,7 @@ nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode,
  *   cache_cap multiple of 64, >= C+M
  *   dh        64 or 128 (else NMDLM_ERR_UNSUPPORTED): scores stay within
  *             the 256-entry table
+ *   limits    T*M <= 2^19 and d <= NMDLM_MAX_K, else NMDLM_ERR_UNSUPPORTED
  *   lut_att   device uint8 [256]
  *   a_out     device int32 [T][M][d] or NULL
  *   theta_a   threshold (> 0) when s_out is given

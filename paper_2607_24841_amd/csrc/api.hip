@@ -185,8 +185,10 @@ nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N, int32_t th
                              const int32_t* theta_vec, const uint64_t* resid, int32_t* v_inout,
                              uint64_t* s_out, void* stream) {
   if (!cur || !s_out || T < 1 || M < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
-  if (T > NMDLM_MAX_T * 1024) return NMDLM_ERR_UNSUPPORTED;
   if (!theta_vec && theta <= 0) return NMDLM_ERR_INVALID_ARG;
+  // one wave per (token, 64-neuron word): the launch grid stays within 2^32 threads
+  if (T > NMDLM_MAX_T * 1024 || (int64_t)M * ((N + 63) / 64) > ((int64_t)1 << 26))
+    return NMDLM_ERR_UNSUPPORTED;
   return launch_if(cur, T, M, N, theta, theta_vec, resid, v_inout, s_out,
                    static_cast<hipStream_t>(stream));
 }
@@ -214,6 +216,7 @@ nmdlm_status nmdlm_bbm_attn(const uint64_t* q, const uint64_t* k_cache, const ui
   if (s_out && theta_a <= 0) return NMDLM_ERR_INVALID_ARG;
   if (T > NMDLM_MAX_T) return NMDLM_ERR_UNSUPPORTED;
   if (dh != 64 && dh != 128) return NMDLM_ERR_UNSUPPORTED;
+  if ((int64_t)T * M > (1 << 19) || (int64_t)H * dh > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
   if (cache_cap % 64 != 0 || cache_cap < (int64_t)C + M) return NMDLM_ERR_INVALID_ARG;
   int32_t* a = a_out;
   if (!a) {

@@ -95,6 +95,14 @@ def test_other_argument_errors(lib):
     assert a(cap=600) == B.NMDLM_ERR_INVALID_ARG                   # cap not a multiple of 64
     assert lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, 576, 4, 16, 512, 16, 64, FAKE, None, 256, None,
                               None, 0, None) == 1                  # no output requested
+    assert a(M=(1 << 17) + 1) == B.NMDLM_ERR_UNSUPPORTED           # T*M beyond 2^19
+    assert lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, 576, 4, 16, 512, 1025, 64, FAKE, FAKE, 256,
+                              None, None, 0, None) == B.NMDLM_ERR_UNSUPPORTED   # d > 65536
+    # IF grid beyond 2^32 threads, and T beyond 8192
+    assert lib.nmdlm_if_neuron(FAKE, 4, 1 << 20, 64 * 65, 256, None, None, None, FAKE,
+                               None) == B.NMDLM_ERR_UNSUPPORTED
+    assert lib.nmdlm_if_neuron(FAKE, 8193, 1, 1, 256, None, None, None, FAKE,
+                               None) == B.NMDLM_ERR_UNSUPPORTED
     assert lib.nmdlm_workspace_clear(FAKE, 17, None) == 1
 
 
