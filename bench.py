@@ -838,7 +838,7 @@ def bench_block(args):
     print(json.dumps(out), flush=True)
 
 
-BATCH_SEQS = (1, 2, 4, 8, 16, 32)
+BATCH_SEQS = (1, 2, 4, 8, 16, 32, 64, 128)
 
 
 def bench_block_batch(args):

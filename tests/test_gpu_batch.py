@@ -46,8 +46,9 @@ def _cases(n, C, M, d, H, F, seed, T=4):
     (3, 35, 5, 128, 2, 256, 0, 3),          # T = 3: 5-token row blocks (16 // 3)
     (2, 48, 16, 256, 2, 512, 0, 4),         # heads of 128 channels
     (3, 60, 8, 128, 2, 256, 0x4, 4),        # the fused-attention flag (single-sequence) is ignored
+    (128, 40, 16, 128, 2, 256, 0, 4),       # 128 sequences: attention at 4 waves per workgroup
 ], ids=["straddle", "bytes", "rt2-ragged", "dense", "full-4seq", "16seq", "T8", "T3", "dh128",
-        "attn-fused-flag"])
+        "attn-fused-flag", "128seq"])
 def test_batched_block_step_matches_independent_sequences(n, C, M, d, H, F, flags, T):
     torch, B = need_gpu()
     cases = _cases(n, C, M, d, H, F, seed=71, T=T)
