@@ -43,3 +43,13 @@ def test_traffic_digest_covers_the_product_sources():
 def test_product_bytes_is_the_row_load_rule():
     # K_active * N weight bytes + packed spikes in and out (T*M rows)
     assert bench.product_bytes(1024, 100, 512, 4, 16) == 100 * 512 + 4 * 16 * 16 * 8 + 4 * 16 * 8 * 8
+
+
+def test_batched_prefill_fits_the_step_row_limit():
+    # the block-batch mode prefills every sequence's context in one call:
+    # T * n * C must stay within a step's 2^19 rows (and so must the block)
+    from workloads import synth
+    c = synth.block_case()
+    n = max(bench.BATCH_SEQS)
+    assert c.T * n * c.C <= 1 << 19 and c.T * n * c.M <= 1 << 19
+    assert c.M % (16 // c.T) == 0          # batched steps need M a multiple of 16/T
