@@ -35,8 +35,8 @@ Other workloads (--workload):
   ternary-ffn      the paper's ternary bitwise coding (T=8) through the FFN
      4096 -> 14336 -> 4096: encode, up product, encode, down product, for B in
      {1, 4, 16} tokens and K in {1, 2, 4} quantisation levels.
-  block-batch      the default block step over n_seq in {1, 2, 4, 8, 16, 32} sequences at
-     once (each with its own 512-token context and 16-token block): every product
+  block-batch      the default block step over n_seq in {1, 2, 4, 8, 16, 32, 64, 128}
+     sequences at once (each with its own 512-token context and 16-token block): every product
      reads a weight row once for the whole batch; tokens/s, union fractions and
      touched bytes per point, beside the analytic model at the measured unions.
 """
