@@ -1,32 +1,35 @@
 #!/usr/bin/env python3
 """Benchmark of the N-MDLM block-denoising step on one MI355X.
 
-Workload (default): one spiking transformer block (d=1024, 16 heads of 64,
-FFN 4096, T=4) at a single denoising step for a block of 16 masked tokens
-over 512 context tokens; inputs Bernoulli(0.10), int8 weights, seeded
-(see workloads/synth.py).  The context prefill is done once, untimed.
+Workload (default, --workload mdlm12-step): a 12-layer spiking MDLM
+(d=2048, 16 heads of 128, FFN 8192, vocab 32000 with an int8 head
+dequantised to fp32 logits, T=4) at one block-denoising step: 32 masked
+tokens over 1024 context tokens, head, confidence and top-8 unmasking.  The
+context prefill runs once, untimed.  Weights are seeded int8 uniforms
+(workloads/synth.py); 640 MB of weights per step, more than the 256 MB
+last-level cache, so every step streams its weights from HBM.
 
-A "step" is one nmdlm_block_step (QKV product, attention, O, up, down,
-all neurons).  Layer copies (identical values, different addresses) rotate
-so that the weights a step reads are not resident in the 256 MB last-level
-cache: every step streams its weights from HBM.  Steps are issued from HIP
-graphs captured on torch's stream.
+A "step" is one nmdlm_block_step (block input, per layer the QKV product,
+attention, O, up and down products with their neurons, then the head,
+confidence and unmasking), preceded by two small copies that reset the
+block to fully masked so that every step is the same workload.  One step is
+captured as a HIP graph before the timed region; the timed region replays it
+--steps times after --warmup replays.
 
-Prints one JSON line with block-denoise tokens/s, the weight-skip fraction,
-the touched-weight bandwidth of the whole step, the roofline of the product
-kernel (timed per launch with HIP events recorded by the library around the
-kernel), the paper's analytic model of the step's products (Eqs. (12)-(14)
-from their measured union fractions and input sparsities, on MI355X and on
-the two systems of Table I) and the CPU oracle's rate on a bounded sample.
+Prints one JSON line: block-denoise tokens/s, the weight-skip fraction, the
+touched-weight bandwidth of the whole step, the roofline of the product
+kernel (every product launch of one step timed with HIP events stamped by
+its own dispatch), and the CPU oracle's rate on a bounded sample.
 
 Other workloads (--workload):
+  block            one spiking transformer block (d=1024, 16 heads of 64, FFN 4096, T=4) at
+     one denoising step, 16 masked tokens over 512 context tokens, inputs
+     Bernoulli(0.10); 32 rotating layer copies (403 MB) so that weights stream
+     from HBM; with the paper's analytic model beside the measured products.
   ffn-sweep        FFN weight-traffic sweep, d=4096 -> 14336 -> 4096, T=4, B in {1,4,16,64},
      mean input density in {.02,.05,.10,.30}: skipped-row fraction, touched
      bytes and GB/s of the up and down products at every point (4 rotating
      weight copies, 470 MB, so that weights stream from HBM).
-  mdlm12-step      12-layer MDLM (d=2048, 16 heads of 128, FFN 8192, vocab 32000, T=4), one
-     block step of 32 masked tokens over 1024 context tokens with head,
-     confidence and top-8 unmasking (640 MB of weights per step).
   mdlm24-generate  24-layer MDLM generation: prompt of 2048 ids, 8 blocks of 32 tokens,
      8 steps per block, 4 tokens unmasked per step.
   e2d2-generate    the paper's own shape: encoder-decoder MDLM with 28 encoder and 4
@@ -35,7 +38,7 @@ Other workloads (--workload):
   ternary-ffn      the paper's ternary bitwise coding (T=8) through the FFN
      4096 -> 14336 -> 4096: encode, up product, encode, down product, for B in
      {1, 4, 16} tokens and K in {1, 2, 4} quantisation levels.
-  block-batch      the default block step over n_seq in {1, 2, 4, 8, 16, 32, 64, 128}
+  block-batch      the block step over n_seq in {1, 2, 4, 8, 16, 32, 64, 128}
      sequences at once (each with its own 512-token context and 16-token block): every product
      reads a weight row once for the whole batch; tokens/s, union fractions and
      touched bytes per point, beside the analytic model at the measured unions.
@@ -54,33 +57,36 @@ HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=320)
-    p.add_argument("--warmup", type=int, default=32)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--copies", type=int, default=32, help="rotating layer copies (>= 256 MB total)")
     p.add_argument("--eager", action="store_true", help="issue kernels directly, no HIP graph")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="host seconds of oracle steps for cpu_baseline")
     p.add_argument("--seed", type=int, default=1002)
     p.add_argument("--flags", type=lambda x: int(x, 0), default=0,
                    help="extra block-step flags (path overrides; results do not change)")
-    p.add_argument("--workload", default="block",
-                   choices=("block", "ffn-sweep", "mdlm12-step", "mdlm24-generate",
+    p.add_argument("--workload", default="mdlm12-step",
+                   choices=("mdlm12-step", "block", "ffn-sweep", "mdlm24-generate",
                             "e2d2-generate", "ternary-ffn", "block-batch"),
-                   help="block: one transformer block at one denoising step (default)")
+                   help="mdlm12-step: the 12-layer MDLM at one block step (default)")
     p.add_argument("--reps", type=int, default=20,
                    help="timed repetitions (ffn-sweep, mdlm12-step)")
     return p.parse_args()
 
 
-# HBM bytes per launch of the product kernel in the one-block step (mean of
-# its four products), from two rocprofv3 --pmc passes (FETCH_SIZE, then
-# WRITE_SIZE) over `bench.py --eager`, each scaled by what the counter reads
-# for a 64 MiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0); the summary
-# with the commands is profiles/k_qbsm_words_one_block_step_traffic.md.  Valid
-# only for the product-kernel sources with this digest: any change to them
-# reports null until the counters are taken again.
-TRAFFIC = {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
-           "bytes_per_launch": 2631235.6}
+# HBM bytes per launch of the product kernel, per workload, from two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE) over `bench.py --eager`, each
+# scaled by what the counter reads for a 64 MiB device copy (FETCH_SIZE x 2.0,
+# WRITE_SIZE x 1.0); the summaries with their commands are under profiles/.
+# A value holds only for the product-kernel sources with the recorded digest:
+# any change to them reports null until the counters are taken again.
+TRAFFIC = {
+    "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
+              "bytes_per_launch": 2631235.6},
+    "mdlm12": {"sources_sha256": "", "bytes_per_launch": None},
+}
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
 
@@ -94,9 +100,10 @@ def product_sources_sha256():
     return h.hexdigest()
 
 
-def product_traffic():
-    if TRAFFIC["sources_sha256"] and TRAFFIC["sources_sha256"] == product_sources_sha256():
-        return TRAFFIC["bytes_per_launch"]
+def product_traffic(workload: str):
+    rec = TRAFFIC.get(workload)
+    if rec and rec["sources_sha256"] and rec["sources_sha256"] == product_sources_sha256():
+        return rec["bytes_per_launch"]
     return None
 
 
@@ -337,8 +344,92 @@ def _mdlm_step_io(B, torch, m, C, M, k, flags, ev=None):
     return io, bufs
 
 
+def cpu_info():
+    """Host CPU model and logical core count (for the oracle's timing)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count() or 1
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def cpu_baseline_mdlm12(case, seconds: float, one_thread_layers: int = 2):
+    """The oracle (as it stands) on the host for the 12-layer step: the same
+    step (block input, 12 layers, head, confidence, top-8 unmasking of 32
+    masked tokens over 1024 context rows) timed in full for about `seconds`.
+    The context keys/values the step attends to come from a seeded
+    Bernoulli(0.3) fill of the caches instead of the oracle's prefill (about
+    4 minutes of host time): the oracle's work does not depend on the cache
+    values, only on their shapes.  A 1-thread rate is taken on a sample of
+    `one_thread_layers` layers plus the head, scaled to the 12 layers."""
+    import numpy as np
+    from oracle import nmdlm_oracle as O
+    m = case.model
+    C, M, k = case.C, case.B, case.k_unmask
+    emb = O.unpack_model_emb(m)
+    kc, vc = O.new_caches(m.n_layers, m.T, C + M, m.d)
+    rng = np.random.default_rng(20261202)
+    for l in range(m.n_layers):
+        kc[l][:, :C] = rng.random((m.T, C, m.d)) < 0.3
+        vc[l][:, :C] = rng.random((m.T, C, m.d)) < 0.3
+    tokens = np.zeros(M, dtype=np.int32)
+    masked = np.ones(M, dtype=bool)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        O.block_step(m, emb, tokens, masked, C, C, kc, vc, k)
+        n += 1
+        dt = time.perf_counter() - t0
+        if dt >= seconds or n >= 100:
+            break
+    threads = blas_threads()
+    # 1 thread: a sample of layers and the head, scaled to the whole stack
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            X = O.block_input(np.full(M, m.mask_id, dtype=np.int32), np.arange(C, C + M), emb,
+                              m.pos_ch)
+            t1 = time.perf_counter()
+            for l in range(one_thread_layers):
+                X = O.layer_forward(X, m.layers[l], kc[l], vc[l], C).Y
+            t_layers = time.perf_counter() - t1
+            t1 = time.perf_counter()
+            logits = O.head_logits(X, m.W_head, m.scale)
+            pred, conf = O.confidence(logits)
+            O.unmask(tokens, masked, pred, conf, k)
+            t_head = time.perf_counter() - t1
+        t_step1 = t_layers * m.n_layers / one_thread_layers + t_head
+        one = {"value": M / t_step1, "unit": "tokens/s", "cores": 1,
+               "sample": f"{one_thread_layers} oracle layers ({t_layers:.1f} s) + head, "
+                         f"confidence and unmasking ({t_head:.1f} s) at 1 thread, the layers "
+                         f"scaled to {m.n_layers}"}
+    except Exception as e:  # threadpoolctl missing: no 1-thread figure
+        one = {"error": repr(e)}
+    model_name, nproc = cpu_info()
+    return {"value": M * n / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} full oracle block steps of the 12-layer workload (32 block tokens "
+                      f"each) in {dt:.1f} s; context keys/values from a seeded Bernoulli(0.3) "
+                      f"cache fill instead of the oracle prefill",
+            "cpu_model": model_name, "nproc": nproc, "one_thread": one}
+
+
 def bench_mdlm12_step(args):
-    """12-layer MDLM, one block step with head, confidence and unmasking."""
+    """12-layer MDLM, one block step with head, confidence and unmasking
+    (the default workload)."""
     import numpy as np
     import torch
 
@@ -353,25 +444,63 @@ def bench_mdlm12_step(args):
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
                          B.nmdlm_block_step_workspace_size(dm, M, 0)))
     ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()
+    # context prefill (Eq. (5)), untimed
     B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, tokens=ctx,
                                      masked=torch.zeros(C, dtype=torch.uint8, device="cuda")), ws)
     io, b = _mdlm_step_io(B, torch, m, C, M, k, args.flags)
 
     def step():
-        # every timed step starts from the fully masked block
+        # every step starts from the fully masked block (two small copies),
+        # so that each timed step is the same workload
         b["tok"].copy_(b["tok0"])
         b["msk"].copy_(b["msk0"])
         B.nmdlm_block_step(dm, io, ws)
 
-    g = _graph(step)
-    t = _time_graph(g, args.reps)
+    # --- everything the timed region replays is captured before it -----------
+    g = None if args.eager else _graph(step)
+
+    def run(n):
+        for _ in range(n):
+            if g is None:
+                step()
+            else:
+                g.replay()
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(args.steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = 1e3 * dt / args.steps
+    # per-step distribution after the timed region (HIP events around single steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    per = []
+    for _ in range(20):
+        e0.record()
+        run(1)
+        e1.record()
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1))
+    pct = {"p10": float(np.percentile(per, 10)), "p50": float(np.percentile(per, 50)),
+           "p90": float(np.percentile(per, 90)), "samples": len(per)}
     st = b["stats"].cpu().numpy()
     touched = int((st[:, 1] * st[:, 2]).sum())
     dense = int((st[:, 0] * st[:, 2]).sum())
-    # products timed per launch
+
+    # --- product kernel timed per launch: the library stamps a HIP event pair
+    #     with the start and end of every product kernel (from its dispatch).
+    #     Events cannot be graph nodes here, so one step is issued directly
+    #     behind a spin kernel: the queue fills while it spins and the kernels
+    #     then run back to back, as in the timed region.
     n_prod = 4 * m.n_layers + 1
     ev = B.HipEvents(2 * n_prod)
     pio, pb = _mdlm_step_io(B, torch, m, C, M, k, args.flags, ev=ev.arr)
+    B.nmdlm_block_step(dm, pio, ws)          # warm the event path
+    torch.cuda.synchronize()
+    pb["tok"].copy_(pb["tok0"])
+    pb["msk"].copy_(pb["msk0"])
+    torch.cuda._sleep(50_000_000)
     B.nmdlm_block_step(dm, pio, ws)
     torch.cuda.synchronize()
     dur = [ev.elapsed_ms(2 * p, 2 * p + 1) for p in range(n_prod)]
@@ -379,24 +508,48 @@ def bench_mdlm12_step(args):
     nbytes = [product_bytes(int(r[0]), int(r[1]), int(r[2]), m.T, M) for r in pst]
     ev.close()
     achieved = sum(nbytes) / (sum(dur) * 1e-3) / 1e9
+    kinds = {}
+    for p in range(n_prod):
+        nm = "head" if p == n_prod - 1 else ("qkv", "o", "up", "down")[p % 4]
+        kd = kinds.setdefault(nm, {"launches": 0, "us": 0.0, "bytes": 0})
+        kd["launches"] += 1
+        kd["us"] += 1e3 * dur[p]
+        kd["bytes"] += nbytes[p]
+    per_kind = {nm: {"launches": v["launches"], "avg_us": v["us"] / v["launches"],
+                     "avg_bytes": v["bytes"] / v["launches"],
+                     "GBps": v["bytes"] / (v["us"] * 1e-6) / 1e9} for nm, v in kinds.items()}
+    traffic = product_traffic("mdlm12")
+    stream = stream_copy_gbps(torch)
     out = {
         "metric": "block-denoise tokens/s; weight-skip fraction; achieved HBM GB/s on touched bytes",
-        "value": M / (t * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.reps, "warmup": 2,
-        "ms_per_step": t, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "int8", "data": "synthetic",
+        "value": M / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
         "config": {"workload": "12-layer spiking MDLM, one block step: d=2048, 16 heads x 128, "
-                               "FFN 8192, vocab 32000, T=4, 32 masked tokens over 1024 context "
-                               "tokens, head + confidence + top-8 unmasking"},
-        "unmasked_tokens_per_s": k / (t * 1e-3),
+                               "FFN 8192, vocab 32000 (int8 head, fp32 logits), T=4, 32 masked "
+                               "tokens over 1024 context tokens (prefilled, untimed), head + "
+                               "confidence + top-8 unmasking",
+                   "block_tokens": M, "context_tokens": C, "layers": m.n_layers,
+                   "issue": "eager" if args.eager else "hip_graph (one step per replay)"},
+        "step_ms_percentiles": pct,
+        "timing_check": {"ms_per_step_over_replay_p50": ms_per_step / pct["p50"]},
+        "unmasked_tokens_per_s": k / (ms_per_step * 1e-3),
         "weight_skip_fraction": 1.0 - touched / dense,
         "touched_weight_bytes_per_step": touched,
-        "touched_weight_GBps": touched / (t * 1e-3) / 1e9,
-        "roofline": {"kernel": "k_qbsm (int8 MFMA spike product with fused epilogue)",
+        "touched_weight_GBps": touched / (ms_per_step * 1e-3) / 1e9,
+        "roofline": {"kernel": "k_qbsm_words (int8 MFMA spike product with fused epilogue; all "
+                               "49 product launches of the step)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "avg_launch_ms": float(np.mean(dur)), "launches_timed": len(dur)},
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "stream_copy_GBps": stream, "frac_of_stream_copy": achieved / stream,
+                     "avg_launch_ms": float(np.mean(dur)), "launches_timed": len(dur),
+                     "algorithmic_bytes_per_launch": float(np.mean(nbytes)),
+                     "per_product": per_kind,
+                     "timing_issue": "direct issue behind a spin kernel (queue full)"},
         "per_layer_k_active": st[:-1, 1].reshape(m.n_layers, 4).tolist(),
     }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_mdlm12(case, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
@@ -720,7 +873,12 @@ def bench_block(args):
         if rest:
             graph_for(rest).replay()
 
-    # --- warmup + timed region ---------------------------------------------------
+    # --- warmup + timed region: every graph the timed region replays is
+    #     captured before it (runs of args.copies steps and the remainder)
+    if not args.eager:
+        for n in (args.copies, args.steps % args.copies, args.warmup % args.copies):
+            if n:
+                graph_for(n)
     run(args.warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -780,7 +938,7 @@ def bench_block(args):
     ev.close()
     avg_ms = float(np.mean(dur))
     achieved = sum(nbytes) / (sum(dur) * 1e-3) / 1e9
-    traffic = product_traffic()
+    traffic = product_traffic("block")
     # the paper's analytic model (Eqs. (12)-(14)) of the step's four products,
     # from their measured union fractions, beside their measured kernel times
     from paper_2607_24841_amd import perf_model

@@ -31,7 +31,7 @@
 extern "C" {
 #endif
 
-#define NMDLM_ABI_VERSION 3
+#define NMDLM_ABI_VERSION 4
 
 typedef enum nmdlm_status {
   NMDLM_OK = 0,
@@ -67,6 +67,13 @@ typedef enum nmdlm_status {
 #define NMDLM_MAX_T 8
 #define NMDLM_MAX_K 65536
 #define NMDLM_MAX_HEAD_M 4096   /* block tokens of a step that runs the head */
+#define NMDLM_MAX_KEYS 8388608  /* attention keys C+M per sequence (2^23): the
+                                   sum of the table weights over the keys,
+                                   at most 255 per key, stays below 2^31   */
+
+/* bits of the device status word of a block step (nmdlm_step_io.status) */
+#define NMDLM_STATUS_TOKEN_CLAMPED 0x1  /* a token id outside [0, V] was read as
+                                           the nearest of 0 and V (the mask id) */
 
 /*
  * Statistics of one spike product, written by the device (int64 so the
@@ -182,14 +189,20 @@ nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N,
                              uint64_t* s_out, void* stream);
 
 /* ------------------------------------------------------------------------
- * nmdlm_qnl_lut — 8-bit-in / 8-bit-out table non-linearity (the quantised
- * non-linearity of the paper's op list).
+ * nmdlm_qnl_lut — 8-bit-in / 8-bit-out table non-linearity.
+ * The paper names this operation only in its list of acronyms (QNL: a
+ * quantised non-linearity implemented as a look-up table), as one of the
+ * operations of the neuromorphic layers of Fig. 1; it gives no formula.
+ * This library's reading, also used by the block step on the FFN up
+ * current:
  *   NMDLM_QNL_S8: index = byte of clamp(floor(x / 2^shift), -128, 127)
  *   NMDLM_QNL_U8: index = clamp(x, 0, 255)            (shift ignored)
  *   y[i] = lut[index]  (the raw table byte; read it as int8 in S8 mode)
  *
  *   x    device int32 [n];  lut device uint8 [256];  y device uint8 [n]
- *   0 <= shift <= 31
+ *   0 <= shift <= 31; n = 0 enqueues nothing
+ * Errors: NMDLM_ERR_INVALID_ARG for n < 0, a missing pointer, a shift out of
+ * range or an unknown mode (nothing is enqueued).
  * ------------------------------------------------------------------------ */
 #define NMDLM_QNL_S8 0
 #define NMDLM_QNL_U8 1
@@ -197,9 +210,14 @@ nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode,
                            const uint8_t* lut, uint8_t* y, void* stream);
 
 /* ------------------------------------------------------------------------
- * nmdlm_bbm_attn — attention on spike operands (binary-binary products,
- * table weights, fixed-point normalisation).  For every timestep t, head h,
- * block query i < M and key j < C+M:
+ * nmdlm_bbm_attn — attention on spike operands.  The paper names the
+ * operations involved only in its list of acronyms: binary-binary
+ * multiplication (BBM, here the query-key product of two spike vectors),
+ * quantised dynamic multiplication (QDM, the table weights times the value
+ * spikes), a look-up-table non-linearity (QNL) and fixed-point arithmetic
+ * (FixP, the integer normalisation); Fig. 1 places attention in every
+ * neuromorphic layer.  The formula below is this library's reading.  For
+ * every timestep t, head h, block query i < M and key j < C+M:
  *     s = popcount(Q[t,i,head h] AND K[t,j,head h])       in [0, dh]
  *     p = lut_att[s]                                       (uint8)
  *     a[t,i,c] = floor(256 * sum_j p * V[t,j,c] / sum_j p)   (0 if sum_j p = 0)
@@ -214,7 +232,8 @@ nmdlm_status nmdlm_qnl_lut(const int32_t* x, int64_t n, int shift, int mode,
  *   cache_cap multiple of 64, >= C+M
  *   dh        64 or 128 (else NMDLM_ERR_UNSUPPORTED): scores stay within
  *             the 256-entry table
- *   limits    T*M <= 2^19 and d <= NMDLM_MAX_K, else NMDLM_ERR_UNSUPPORTED
+ *   limits    T*M <= 2^19, d <= NMDLM_MAX_K and C+M <= NMDLM_MAX_KEYS, else
+ *             NMDLM_ERR_UNSUPPORTED
  *   lut_att   device uint8 [256]
  *   a_out     device int32 [T][M][d] or NULL
  *   theta_a   threshold (> 0) when s_out is given
@@ -260,6 +279,13 @@ size_t nmdlm_bbm_attn_workspace_size(int T, int M, int H, int dh);
  * the caches of sequence s start s*T*cache_cap*d/64 words into k_cache and
  * vt_cache (both hold model->max_seq sequences).  With n_seq > 1, M must be
  * a multiple of 16/T (integer division) and NMDLM_ATTN_FUSED is ignored.
+ *
+ * Token ids: the block input reads the token table at row tokens[m] for an
+ * unmasked position and at row V (the mask token) for a masked one; ids are
+ * expected in [0, V).  An id outside [0, V] is read as the nearest of 0 and V
+ * (never out of bounds) and flags NMDLM_STATUS_TOKEN_CLAMPED in io->status.
+ * Limits: C+M <= NMDLM_MAX_KEYS and cache_cap/64 <= 2^31-1, else
+ * NMDLM_ERR_UNSUPPORTED.
  * ------------------------------------------------------------------------ */
 typedef struct nmdlm_layer {
   const int8_t* w_qkv;   /* device [d][3d]: columns Q | K | V */
@@ -317,6 +343,11 @@ typedef struct nmdlm_step_io {
   int n_prof_events;       /* length of prof_events                         */
   int n_seq;               /* sequences in the step, 1..max(1, max_seq) (0
                               counts as 1); M is per sequence              */
+  int32_t* status;         /* device int32 or NULL: the step ORs in
+                              NMDLM_STATUS_* bits (the caller clears it);
+                              a token id outside [0, V] is read as the
+                              nearest of 0 and V and sets
+                              NMDLM_STATUS_TOKEN_CLAMPED                   */
 } nmdlm_step_io;
 
 nmdlm_status nmdlm_block_step(const nmdlm_model* model, nmdlm_step_io* io,

@@ -29,6 +29,8 @@ NMDLM_SPLIT_SHIFT = 8
 NMDLM_ROWTILE_SHIFT = 16
 NMDLM_ATTN_FUSED = 0x4
 NMDLM_MAX_HEAD_M = 4096   # block tokens of a step that runs the head
+NMDLM_MAX_KEYS = 1 << 23   # attention keys C+M per sequence
+NMDLM_STATUS_TOKEN_CLAMPED = 0x1
 NMDLM_PATH_SHIFT = 20
 NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-row list
 NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
@@ -83,7 +85,7 @@ class StepIO(C.Structure):
         ("k_unmask", C.c_int), ("y_out", C.c_void_p), ("logits", C.c_void_p),
         ("pred", C.c_void_p), ("conf", C.c_void_p), ("unmasked_pos", C.c_void_p),
         ("stats", C.c_void_p), ("prof_events", C.POINTER(C.c_void_p)), ("n_prof_events", C.c_int),
-        ("n_seq", C.c_int),
+        ("n_seq", C.c_int), ("status", C.c_void_p),
     ]
 
 
@@ -334,14 +336,15 @@ class ModelView:
 
 def step_io(M, C_, pos0=0, flags=0, x_in=None, tokens=None, masked=None, k_unmask=0, y_out=None,
             logits=None, pred=None, conf=None, unmasked_pos=None, stats=None,
-            prof_events=None, n_seq: int = 1) -> StepIO:
+            prof_events=None, n_seq: int = 1, status=None) -> StepIO:
     """prof_events: optional ctypes array of hipEvent_t handles (see HipEvents).
     n_seq: sequences in the step; M is per sequence, token buffers hold the
-    sequences one after the other."""
+    sequences one after the other.  status: optional device int32 word that
+    the step ORs NMDLM_STATUS_* bits into."""
     ev = prof_events if prof_events is not None else None
     return StepIO(M, C_, pos0, flags, ptr(x_in), ptr(tokens), ptr(masked), k_unmask, ptr(y_out),
                   ptr(logits), ptr(pred), ptr(conf), ptr(unmasked_pos), ptr(stats),
-                  ev, 0 if ev is None else len(ev), n_seq)
+                  ev, 0 if ev is None else len(ev), n_seq, ptr(status))
 
 
 class HipEvents:

@@ -1,6 +1,7 @@
 // C ABI of libnmdlm: argument validation (before any HIP call), workspace
 // sizing and dispatch to the launchers.
 #include <algorithm>
+#include <climits>
 
 #include "common.h"
 
@@ -218,6 +219,7 @@ nmdlm_status nmdlm_bbm_attn(const uint64_t* q, const uint64_t* k_cache, const ui
   if (dh != 64 && dh != 128) return NMDLM_ERR_UNSUPPORTED;
   if ((int64_t)T * M > (1 << 19) || (int64_t)H * dh > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
   if (cache_cap % 64 != 0 || cache_cap < (int64_t)C + M) return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)C + M > NMDLM_MAX_KEYS || cache_cap / 64 > INT_MAX) return NMDLM_ERR_UNSUPPORTED;
   int32_t* a = a_out;
   if (!a) {
     if (!ws || !aligned(ws, 256) || ws_bytes < nmdlm_bbm_attn_workspace_size(T, M, H, dh))
@@ -261,6 +263,8 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   if ((int64_t)md->T * Mt > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
   if (md->cache_cap % 64 != 0 || md->cache_cap < (int64_t)io->C + io->M)
     return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)io->C + io->M > NMDLM_MAX_KEYS || md->cache_cap / 64 > INT_MAX)
+    return NMDLM_ERR_UNSUPPORTED;
   if (md->n_layers > 0 && !md->layers) return NMDLM_ERR_INVALID_ARG;
   for (int l = 0; l < md->n_layers; ++l) {
     const nmdlm_layer& L = md->layers[l];

@@ -425,7 +425,9 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   for (int ml = wave; ml < a.Mb; ml += NW) {
     const int m = y * a.Mb + ml;
     if (m >= a.M) break;
-    int V = 0;
+    // the membrane (and a current with its residual) is int64: T steps of
+    // currents up to 2^31 in magnitude plus theta stay exact
+    long long V = 0;
 #pragma unroll
     for (int t = 0; t < NMDLM_MAX_T; ++t) {
       if (t < a.T) {
@@ -437,12 +439,13 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
             qv = min(127, max(-128, qv));
             I = (int)ep.lut[qv & 0xFF];
           }
+          long long Iv = I;
           if (a.resid) {
             // staged at entry: T * Mb <= 16 * RT <= kMaxEpiTokens rows
             const unsigned long long rw = ep.resid[t * a.Mb + ml];
-            if ((rw >> col) & 1ull) I += theta;
+            if ((rw >> col) & 1ull) Iv += theta;
           }
-          V += I;
+          V += Iv;
           const bool s = nv && V >= theta;
           if (s) V -= theta;
           if (!tr) {

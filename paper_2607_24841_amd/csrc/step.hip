@@ -12,13 +12,15 @@ namespace nmdlm {
 
 // X[t,m,:] = E[token_m][t] OR the position spike of (pos0 + m % Mseq, t)
 // (M rows: sequences of Mseq tokens one after the other); masked positions
-// use the mask token (id V).
+// use the mask token (id V).  An id outside [0, V] reads the nearest row and
+// sets NMDLM_STATUS_TOKEN_CLAMPED in the caller's status word (if given).
 __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ emb,
                                                   const int32_t* __restrict__ pos_ch,
                                                   const int32_t* __restrict__ tokens,
                                                   const uint8_t* __restrict__ masked, int V, int T,
                                                   int M, int Mseq, int dw, int pos0,
-                                                  uint64_t* __restrict__ X) {
+                                                  uint64_t* __restrict__ X,
+                                                  int32_t* __restrict__ status) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   const long long total = (long long)T * M * dw;
   if (i >= total) return;
@@ -26,7 +28,11 @@ __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ e
   const int m = (int)((i / dw) % M);
   const int t = (int)(i / ((long long)dw * M));
   int tok = (masked && masked[m]) ? V : (tokens ? tokens[m] : V);
-  tok = min(max(tok, 0), V);
+  if (tok < 0 || tok > V) {
+    // an id outside the table is read as the nearest valid row and reported
+    if (status && t == 0 && w == 0) atomicOr(status, NMDLM_STATUS_TOKEN_CLAMPED);
+    tok = min(max(tok, 0), V);
+  }
   uint64_t word = emb[((size_t)tok * T + t) * dw + w];
   const int pc = pos_ch[(size_t)(pos0 + m % Mseq) * T + t];
   if ((pc >> 6) == w) word |= 1ull << (pc & 63);
@@ -312,7 +318,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     const long long total = (long long)T * M * dw;
     hipLaunchKernelGGL(k_assemble, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
                        md->emb, md->pos_ch, io->tokens, io->masked, md->V, T, M, Ms, dw, io->pos0,
-                       b.X);
+                       b.X, io->status);
     if ((rc = hip_status()) != NMDLM_OK) return rc;
     X = b.X;
   }

@@ -31,7 +31,7 @@ def test_exports_every_declared_function(lib):
     assert set(B.EXPORTS) <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.nmdlm_abi_version() == 3
+    assert lib.nmdlm_abi_version() == 4
     assert lib.nmdlm_status_string(0) == b"ok"
     assert lib.nmdlm_status_string(3).startswith(b"workspace")
 
@@ -96,6 +96,9 @@ def test_other_argument_errors(lib):
     assert lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, 576, 4, 16, 512, 16, 64, FAKE, None, 256, None,
                               None, 0, None) == 1                  # no output requested
     assert a(M=(1 << 17) + 1) == B.NMDLM_ERR_UNSUPPORTED           # T*M beyond 2^19
+    big = (1 << 23) + 64                                            # keys beyond NMDLM_MAX_KEYS
+    assert a(C=(1 << 23) - 15, cap=big) == B.NMDLM_ERR_UNSUPPORTED
+    assert a(C=0, cap=64 * (2 ** 31)) == B.NMDLM_ERR_UNSUPPORTED   # cap/64 beyond INT_MAX
     assert lib.nmdlm_bbm_attn(FAKE, FAKE, FAKE, 576, 4, 16, 512, 1025, 64, FAKE, FAKE, 256,
                               None, None, 0, None) == B.NMDLM_ERR_UNSUPPORTED   # d > 65536
     # IF grid beyond 2^32 threads, and T beyond 8192
@@ -118,6 +121,11 @@ def test_block_step_argument_errors(lib):
     assert call(m, io, nb=ws_need - 256) == B.NMDLM_ERR_WORKSPACE
     bad = B.step_io(16, 600, flags=B.NMDLM_NO_HEAD, x_in=FAKE)      # C + M > cache_cap
     assert call(m, bad) == 1
+    # more attention keys than NMDLM_MAX_KEYS, with a cache that holds them
+    mk = B.Model(1, 1024, 16, 4096, 32000, 4, (1 << 23) + 64, 0, layers, None, None, None, None)
+    nbk = lib.nmdlm_block_step_workspace_size(C.byref(mk), 16, B.NMDLM_NO_HEAD)
+    many = B.step_io(16, (1 << 23) - 15, flags=B.NMDLM_NO_HEAD, x_in=FAKE)
+    assert lib.nmdlm_block_step(C.byref(mk), C.byref(many), FAKE, nbk, None) == B.NMDLM_ERR_UNSUPPORTED
     L2 = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 0, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE, FAKE)
     m2 = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, (B.Layer * 1)(L2), None, None, None, None)
     assert call(m2, io) == 1                                        # threshold 0
@@ -182,7 +190,8 @@ def test_ternary_argument_errors(lib):
 def test_binding_constants_match_the_header():
     text = open(HEADER).read()
     for name in ("NMDLM_FORCE_DENSE", "NMDLM_NO_HEAD", "NMDLM_ATTN_FUSED", "NMDLM_SPLIT_SHIFT",
-                 "NMDLM_ROWTILE_SHIFT", "NMDLM_MAX_HEAD_M", "NMDLM_MAX_T", "NMDLM_MAX_K"):
+                 "NMDLM_ROWTILE_SHIFT", "NMDLM_MAX_HEAD_M", "NMDLM_MAX_T", "NMDLM_MAX_K",
+                 "NMDLM_MAX_KEYS", "NMDLM_STATUS_TOKEN_CLAMPED"):
         m = re.search(r"#define\s+%s\s+([0-9xXa-fA-F]+)u?" % name, text)
         assert m, name
         if hasattr(B, name):

@@ -35,9 +35,17 @@ def test_traffic_digest_covers_the_product_sources():
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     assert bench.product_sources_sha256() == h.hexdigest()
-    # the stored figure is reported only for the sources it was measured on
-    assert bench.product_traffic() == (bench.TRAFFIC["bytes_per_launch"]
-                                       if bench.TRAFFIC["sources_sha256"] == h.hexdigest() else None)
+    # a stored figure is reported only for the sources it was measured on
+    for w, rec in bench.TRAFFIC.items():
+        want = rec["bytes_per_launch"] if rec["sources_sha256"] == h.hexdigest() else None
+        assert bench.product_traffic(w) == want
+    assert bench.product_traffic("no such workload") is None
+
+
+def test_default_workload_is_the_twelve_layer_step(monkeypatch):
+    monkeypatch.setattr(sys, "argv", ["bench.py"])
+    a = bench.parse()
+    assert a.workload == "mdlm12-step" and a.gpus == 1 and a.steps > 0 and a.warmup >= 0
 
 
 def test_product_bytes_is_the_row_load_rule():

@@ -314,3 +314,39 @@ def test_head_at_maximum_block():
     kc, vc = O.new_caches(m.n_layers, m.T, M, m.d)
     ref = O.block_step(m, emb, tok0, msk0, 0, 0, kc, vc, M)
     _check_head_step(ref, _head_step(m, M, 0, tok0, msk0, M), M)
+
+
+def test_out_of_range_token_ids_are_clamped_and_reported():
+    """An unmasked token id outside [0, V] reads the nearest table row (0 or
+    the mask row V) and sets NMDLM_STATUS_TOKEN_CLAMPED; in-range ids leave
+    the status word untouched.  Outputs equal the oracle's on the clamped ids."""
+    torch, B = need_gpu()
+    m = _tiny()
+    emb = O.unpack_model_emb(m)
+    P, M = 12, 8
+    prompt = synth.random_tokens(3, P, m.V)
+    kc, vc = O.new_caches(m.n_layers, m.T, P + M, m.d)
+    O.prefill(O.block_input(prompt, np.arange(P), emb, m.pos_ch), m.layers, kc, vc)
+    dm = B.DeviceModel.from_mdlm(m, P + M)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, P, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, B.NMDLM_NO_HEAD)))
+    pr = torch.from_numpy(prompt.astype(np.int32)).cuda()
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(P, 0, flags=B.NMDLM_NO_HEAD, tokens=pr,
+                                     masked=torch.zeros(P, dtype=torch.uint8, device="cuda"),
+                                     status=status), ws)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    tok0 = np.array([5, -3, m.V + 9, 2, m.V, 1, 0, 4], dtype=np.int32)
+    msk0 = np.zeros(M, dtype=bool)
+    clamped = np.clip(tok0, 0, m.V)
+    X = O.block_input(clamped, np.arange(P, P + M), emb, m.pos_ch)
+    Yref, _ = O.stack_forward(X, m.layers, kc, vc, P)
+    y = torch.zeros((m.T, M, m.d // 64), dtype=torch.int64, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, P, pos0=P, flags=B.NMDLM_NO_HEAD,
+                                     tokens=torch.from_numpy(tok0).cuda(),
+                                     masked=torch.from_numpy(msk0.astype(np.uint8)).cuda(),
+                                     y_out=y, status=status), ws)
+    torch.cuda.synchronize()
+    assert int(status.item()) == B.NMDLM_STATUS_TOKEN_CLAMPED
+    assert_same(synth.unpack_bits(B.from_dev_bits(y), m.d), Yref, "Y")

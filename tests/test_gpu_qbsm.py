@@ -158,3 +158,28 @@ def test_determinism():
     a = run_qbsm(c.S, c.W, c.bias, theta=300)
     b = run_qbsm(c.S, c.W, c.bias, theta=300)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[3], b[3])
+
+
+LARGE_BIAS_PATHS = [0, NOFUSE, FUSED, WORDS, DMA]
+
+
+@pytest.mark.parametrize("T", [4, 8])
+@pytest.mark.parametrize("path", LARGE_BIAS_PATHS, ids=["auto", "list", "fused", "words", "dma"])
+def test_membrane_beyond_int32_with_large_bias(T, path):
+    """Biases near 2^30 with a threshold near 1.6e9: the membrane passes 2^31
+    after two steps, so the fused IF must integrate in 64 bits as the oracle
+    does (K*127 + |bias| < 2^31 keeps every current itself in int32)."""
+    need_gpu()
+    rng = np.random.default_rng(77 + T)
+    K, N, M = 64, 130, 5
+    S = rng.random((T, M, K)) < 0.3
+    W = rng.integers(-127, 128, size=(K, N)).astype(np.int8)
+    bias = (2 ** 30 + rng.integers(-20000, 20000, size=N)).astype(np.int32)
+    bias[::7] = -bias[::7]                     # some neurons driven negative
+    theta = 3 * 2 ** 29
+    I_ref = O.qbsm(S, W, bias)
+    s_ref, _ = O.if_neuron(I_ref, theta)
+    assert s_ref.any() and not s_ref.all()
+    cur, spk, _, _, _ = run_qbsm(S, W, bias, theta=theta, flags=path)
+    assert_same(cur, I_ref)
+    assert_same(spk, s_ref)
