@@ -492,12 +492,48 @@ def qbsm_ternary(s: np.ndarray, W: np.ndarray):
     return I, acc
 
 
-def ternary_scale_f32(S: np.ndarray, D: int, K: int) -> np.ndarray:
-    """V_th = S / (D K) as one IEEE fp32 division of the fp32 conversions."""
-    return np.asarray(S, dtype=np.float32) / np.float32(D * K)
+def modified_if(I: np.ndarray, thr_num, thr_den: int):
+    """The modified IF neuron of Eqs. (9)-(10) over the T bit-timesteps of a
+    ternary bitwise-coded input (axis 0 of I), with threshold
+    V_th = thr_num / thr_den (one numerator per token: the last-but-one
+    axis of I; thr_den > 0).
+
+    Readings: timesteps run t = 1..T and the input at step t carries the
+    weight 2^(t-1) of its bit (Eq. (8); the 2^t of Eqs. (9)-(10) counts steps
+    from zero); as for the plain IF neuron the membrane integrates before it
+    fires.  Per neuron, starting from V = 0:
+        V += 2^(t-1) I_t
+        s_t = +1 if V >= 2^(t-1) V_th,  -1 if V <= -2^(t-1) V_th,  else 0
+        V -= 2^(t-1) s_t V_th
+    so that V_th sum_t 2^(t-1) s_t = sum_t 2^(t-1) I_t - V_final (Eq. (11)'s
+    reconstruction, with the final membrane as its error).  A token whose
+    threshold numerator is 0 (an all-zero activation vector, V_th = 0) emits
+    no spike.  The membrane is kept multiplied by thr_den so that every step
+    is integer arithmetic.
+    I: int [T][M][N]; thr_num: int [M].
+    Returns (s int8 [T][M][N] in {-1, 0, 1}, thr_den * V_final int64 [M][N])."""
+    I = np.asarray(I, dtype=np.int64)
+    num = np.asarray(thr_num, dtype=np.int64)
+    den = int(thr_den)
+    if den <= 0:
+        raise ValueError("threshold denominator must be positive")
+    T = I.shape[0]
+    silent = (num <= 0)[:, None]
+    V = np.zeros(I.shape[1:], dtype=np.int64)          # den * membrane
+    s = np.zeros(I.shape, dtype=np.int8)
+    for t in range(T):                                  # t here is the paper's t - 1
+        w = 1 << t
+        V = V + den * w * I[t]
+        thr = (w * num)[:, None]
+        up = ~silent & (V >= thr)
+        dn = ~silent & ~up & (V <= -thr)
+        s[t] = up.astype(np.int8) - dn.astype(np.int8)
+        V = V - s[t].astype(np.int64) * thr
+    return s, V
 
 
-def ternary_output_f32(acc: np.ndarray, vth32: np.ndarray) -> np.ndarray:
-    """The layer output y = V_th w^T q (Eq. (11)) in fp32: one multiply of the
-    fp32 accumulator by the token's fp32 step."""
-    return np.asarray(acc, dtype=np.float32) * np.asarray(vth32, dtype=np.float32)[:, None]
+def bitwise_value(s: np.ndarray) -> np.ndarray:
+    """sum_t 2^(t-1) s_t over axis 0 (t = 1..T): the integer a ternary spike
+    train codes (Eq. (8)), and the sum Eq. (11) scales by V_th."""
+    s = np.asarray(s, dtype=np.int64)
+    return sum((1 << t) * s[t] for t in range(s.shape[0]))
