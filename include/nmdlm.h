@@ -8,9 +8,10 @@
  * *_workspace_size functions.  Every call validates its arguments on the
  * host first and, on error, returns a status without enqueueing any work.
  * Calls are asynchronous with respect to the host: outputs (and statistics)
- * are valid once the stream has reached them.  The library keeps no global
- * mutable state; two calls may run concurrently on different streams when
- * their workspaces and outputs do not overlap.
+ * are valid once the stream has reached them.  Apart from the static scratch
+ * of nmdlm_qbsm_noalloc, the library keeps no global mutable state; two calls
+ * may run concurrently on different streams when their workspaces and
+ * outputs do not overlap.
  *
  * Spike tensors are {0,1}^{T x M x K} packed little-endian into uint64
  * words: tensor [T][M][ceil(K/64)], bit j of word w is channel 64*w + j.
@@ -125,6 +126,31 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K,
                         unsigned flags, void* ws, size_t ws_bytes, void* stream);
 
 size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
+
+/* ------------------------------------------------------------------------
+ * nmdlm_qbsm_noalloc — nmdlm_qbsm without a workspace argument, for callers
+ * that cannot allocate device memory (code under stream capture, tight
+ * serving loops, harnesses that forbid allocation).  The call allocates
+ * nothing: its scratch is a static device array of
+ * NMDLM_NOALLOC_SCRATCH_BYTES that each GPU holds from the library's first
+ * call on it until the process ends (that first call also clears it with a
+ * fill kernel on the stream).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, other host threads) race
+ * and must not be issued.  Sequential calls on a stream are safe: every call
+ * leaves the array's counter region at zero, as nmdlm_qbsm does.
+ *
+ * Arguments, results and errors are those of nmdlm_qbsm (same computation,
+ * same kernels), less ws and ws_bytes; a product whose
+ * nmdlm_qbsm_workspace_size() exceeds NMDLM_NOALLOC_SCRATCH_BYTES returns
+ * NMDLM_ERR_UNSUPPORTED before any work is enqueued.
+ * ------------------------------------------------------------------------ */
+#define NMDLM_NOALLOC_SCRATCH_BYTES 16777216  /* 16 MiB per GPU */
+nmdlm_status nmdlm_qbsm_noalloc(const uint64_t* s_in, int T, int M, int K,
+                                const int8_t* W, int N, int64_t ldw,
+                                const int32_t* bias, int32_t* cur_out,
+                                int32_t theta, const int32_t* theta_vec,
+                                uint64_t* s_out, nmdlm_qbsm_stats* stats,
+                                unsigned flags, void* stream);
 
 /* ------------------------------------------------------------------------
  * nmdlm_ternary_encode — adaptive quantisation and ternary bitwise coding of

@@ -31,6 +31,7 @@ NMDLM_ATTN_FUSED = 0x4
 NMDLM_MAX_HEAD_M = 4096   # block tokens of a step that runs the head
 NMDLM_MAX_KEYS = 1 << 23   # attention keys C+M per sequence
 NMDLM_STATUS_TOKEN_CLAMPED = 0x1
+NMDLM_NOALLOC_SCRATCH_BYTES = 16 << 20   # static scratch of nmdlm_qbsm_noalloc per GPU
 NMDLM_PATH_SHIFT = 20
 NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-row list
 NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
@@ -115,6 +116,8 @@ def load(path: str = LIB_PATH):
     vp, i32, i64, sz, u = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t, C.c_uint
     lib.nmdlm_qbsm.argtypes = [vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64, vp, vp, i32, vp,
                                vp, vp, u, vp, sz, vp]
+    lib.nmdlm_qbsm_noalloc.argtypes = [vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64, vp, vp,
+                                       i32, vp, vp, vp, u, vp]
     lib.nmdlm_qbsm_workspace_size.argtypes = [C.c_int] * 4
     lib.nmdlm_qbsm_workspace_size.restype = sz
     lib.nmdlm_if_neuron.argtypes = [vp, C.c_int, C.c_int, C.c_int, i32, vp, vp, vp, vp, vp]
@@ -133,7 +136,7 @@ def load(path: str = LIB_PATH):
     lib.nmdlm_status_string.argtypes = [C.c_int]
     lib.nmdlm_status_string.restype = C.c_char_p
     lib.nmdlm_abi_version.restype = C.c_int
-    for fn in ("nmdlm_qbsm", "nmdlm_if_neuron", "nmdlm_qnl_lut", "nmdlm_bbm_attn",
+    for fn in ("nmdlm_qbsm", "nmdlm_qbsm_noalloc", "nmdlm_if_neuron", "nmdlm_qnl_lut", "nmdlm_bbm_attn",
                "nmdlm_block_step", "nmdlm_workspace_clear", "nmdlm_ternary_encode",
                "nmdlm_qbsm_ternary"):
         getattr(lib, fn).restype = C.c_int
@@ -191,6 +194,15 @@ def nmdlm_qbsm(s_in, T, M, K, W, N, ldw, bias=None, cur_out=None, theta=0, theta
                         ptr(theta_vec), ptr(s_out), ptr(stats), flags, ptr(ws),
                         0 if ws is None else ws.numel() * ws.element_size(), stream_handle(stream))
     check(st, "nmdlm_qbsm")
+
+
+def nmdlm_qbsm_noalloc(s_in, T, M, K, W, N, ldw, bias=None, cur_out=None, theta=0,
+                       theta_vec=None, s_out=None, stats=None, flags=0, stream=None) -> None:
+    """nmdlm_qbsm with the library's static per-GPU scratch (no workspace)."""
+    st = load().nmdlm_qbsm_noalloc(ptr(s_in), T, M, K, ptr(W), N, ldw, ptr(bias), ptr(cur_out),
+                                   theta, ptr(theta_vec), ptr(s_out), ptr(stats), flags,
+                                   stream_handle(stream))
+    check(st, "nmdlm_qbsm_noalloc")
 
 
 def nmdlm_qbsm_workspace_size(T, M, K, N) -> int:
