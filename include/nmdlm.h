@@ -197,6 +197,47 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
                                 void* stream);
 
 /* ------------------------------------------------------------------------
+ * nmdlm_qbsm_ternary_if — the spiking product on ternary bitwise-coded
+ * spikes followed by the modified IF neuron of Sec. III-B (Eqs. (9)-(10)),
+ * which turns the per-timestep currents back into ternary spike planes;
+ * row-load rule of Sec. IV-A on either input plane.  Per token m and output
+ * neuron n, with I_t = sum_k (s_pos - s_neg)[t,m,k] * W[k,n] and the
+ * threshold Vth = thr_num[m] / thr_den:
+ *     V = 0; for t = 1..T:
+ *       V += 2^(t-1) I_t
+ *       s_t = +1 if V >= 2^(t-1) Vth, -1 if V <= -2^(t-1) Vth, else 0
+ *       V -= 2^(t-1) s_t Vth
+ * so that Vth sum_t 2^(t-1) s_t = sum_t 2^(t-1) I_t - V (Eq. (11), the final
+ * membrane being its error).  Readings: the 2^t of Eqs. (9)-(10) counts steps
+ * from 0 (weight 2^(t-1) for step t = 1..T, as in Eq. (8)); the membrane
+ * integrates before it fires, as for Eqs. (3)-(4); a token with
+ * thr_num[m] = 0 (Vth = 0, an all-zero activation vector) emits no spike.
+ * The paper's threshold is the input's quantisation step: pass s_sum of
+ * nmdlm_ternary_encode as thr_num and D*K as thr_den.  All arithmetic is
+ * integer (the membrane is kept times thr_den in 64 bits): exact.
+ *
+ *   s_pos, s_neg  device spikes [T][M][ceil(K/64)] (never both set)
+ *   W, ldw, N     as nmdlm_qbsm; K <= NMDLM_MAX_TERNARY_K
+ *   thr_num       device int64 [M], each in [0, 2^55) (larger values give
+ *                 undefined spikes)
+ *   thr_den       1 <= thr_den <= NMDLM_MAX_THR_DEN (else INVALID_ARG /
+ *                 UNSUPPORTED)
+ *   out_pos       device spikes [T][M][ceil(N/64)]: bit set where s_t = +1
+ *   out_neg       device spikes [T][M][ceil(N/64)]: bit set where s_t = -1
+ *                 (padding bits written as zero; the planes can feed the next
+ *                 nmdlm_qbsm_ternary_if directly)
+ *   v_out         device int64 [M][N] or NULL: thr_den * final membrane
+ *   stats, flags, ws   as nmdlm_qbsm_ternary
+ * ------------------------------------------------------------------------ */
+#define NMDLM_MAX_THR_DEN 16777216
+nmdlm_status nmdlm_qbsm_ternary_if(const uint64_t* s_pos, const uint64_t* s_neg, int T,
+                                   int M, int K, const int8_t* W, int N, int64_t ldw,
+                                   const int64_t* thr_num, int64_t thr_den,
+                                   uint64_t* out_pos, uint64_t* out_neg, int64_t* v_out,
+                                   nmdlm_qbsm_stats* stats, unsigned flags, void* ws,
+                                   size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * nmdlm_if_neuron — integrate-and-fire with soft reset (Sec. II-B,
  * Eqs. (3)-(4)), integrate-then-fire order, equality fires, no lower clamp:
  *     V = v_in (or 0); for t: V += cur[t] + theta*resid[t];

@@ -32,6 +32,7 @@ NMDLM_MAX_HEAD_M = 4096   # block tokens of a step that runs the head
 NMDLM_MAX_KEYS = 1 << 23   # attention keys C+M per sequence
 NMDLM_STATUS_TOKEN_CLAMPED = 0x1
 NMDLM_NOALLOC_SCRATCH_BYTES = 16 << 20   # static scratch of nmdlm_qbsm_noalloc per GPU
+NMDLM_MAX_THR_DEN = 1 << 24
 NMDLM_PATH_SHIFT = 20
 NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-row list
 NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
@@ -44,7 +45,7 @@ EXPORTS = (
     "nmdlm_qbsm", "nmdlm_qbsm_workspace_size", "nmdlm_if_neuron", "nmdlm_qnl_lut",
     "nmdlm_bbm_attn", "nmdlm_bbm_attn_workspace_size", "nmdlm_block_step",
     "nmdlm_block_step_workspace_size", "nmdlm_workspace_clear", "nmdlm_status_string",
-    "nmdlm_abi_version", "nmdlm_ternary_encode", "nmdlm_qbsm_ternary",
+    "nmdlm_abi_version", "nmdlm_ternary_encode", "nmdlm_qbsm_ternary", "nmdlm_qbsm_ternary_if",
 )
 
 
@@ -124,6 +125,8 @@ def load(path: str = LIB_PATH):
     lib.nmdlm_ternary_encode.argtypes = [vp, C.c_int, C.c_int, C.c_int, C.c_int, vp, vp, vp, vp]
     lib.nmdlm_qbsm_ternary.argtypes = [vp, vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64, vp, vp,
                                        u, vp, sz, vp]
+    lib.nmdlm_qbsm_ternary_if.argtypes = [vp, vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64,
+                                          vp, i64, vp, vp, vp, vp, u, vp, sz, vp]
     lib.nmdlm_qnl_lut.argtypes = [vp, i64, C.c_int, C.c_int, vp, vp, vp]
     lib.nmdlm_bbm_attn.argtypes = [vp, vp, vp, i64, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                    vp, vp, i32, vp, vp, sz, vp]
@@ -138,7 +141,7 @@ def load(path: str = LIB_PATH):
     lib.nmdlm_abi_version.restype = C.c_int
     for fn in ("nmdlm_qbsm", "nmdlm_qbsm_noalloc", "nmdlm_if_neuron", "nmdlm_qnl_lut", "nmdlm_bbm_attn",
                "nmdlm_block_step", "nmdlm_workspace_clear", "nmdlm_ternary_encode",
-               "nmdlm_qbsm_ternary"):
+               "nmdlm_qbsm_ternary", "nmdlm_qbsm_ternary_if"):
         getattr(lib, fn).restype = C.c_int
     runtimes = _hip_runtimes_mapped()
     if len(runtimes) > 1:
@@ -222,6 +225,16 @@ def nmdlm_qbsm_ternary(s_pos, s_neg, T, M, K, W, N, ldw, acc_out, stats=None, fl
                                    0 if ws is None else ws.numel() * ws.element_size(),
                                    stream_handle(stream))
     check(st, "nmdlm_qbsm_ternary")
+
+
+def nmdlm_qbsm_ternary_if(s_pos, s_neg, T, M, K, W, N, ldw, thr_num, thr_den, out_pos, out_neg,
+                          v_out=None, stats=None, flags=0, ws=None, stream=None) -> None:
+    st = load().nmdlm_qbsm_ternary_if(ptr(s_pos), ptr(s_neg), T, M, K, ptr(W), N, ldw,
+                                      ptr(thr_num), int(thr_den), ptr(out_pos), ptr(out_neg),
+                                      ptr(v_out), ptr(stats), flags, ptr(ws),
+                                      0 if ws is None else ws.numel() * ws.element_size(),
+                                      stream_handle(stream))
+    check(st, "nmdlm_qbsm_ternary_if")
 
 
 def nmdlm_if_neuron(cur, T, M, N, theta=0, theta_vec=None, resid=None, v_inout=None, s_out=None,

@@ -106,6 +106,10 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;
+  c.thr_num = nullptr;
+  c.thr_den = 1;
+  c.s_neg_out = nullptr;
+  c.v_out = nullptr;
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
   QbsmScratch scr;
@@ -122,18 +126,18 @@ nmdlm_status nmdlm_ternary_encode(const int32_t* a, int M, int D, int K, int T, 
   return launch_ternary_encode(a, M, D, K, T, s_pos, s_neg, s_sum, static_cast<hipStream_t>(stream));
 }
 
-nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M, int K,
-                                const int8_t* W, int N, int64_t ldw, int32_t* acc_out,
-                                nmdlm_qbsm_stats* stats, unsigned flags, void* ws, size_t ws_bytes,
-                                void* stream) {
-  if (!s_pos || !s_neg || !acc_out || T < 1 || M < 1 || K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
-  if (T > NMDLM_MAX_T || K > NMDLM_MAX_TERNARY_K) return NMDLM_ERR_UNSUPPORTED;
-  if (!weights_ok(W, K, N, ldw)) return NMDLM_ERR_INVALID_ARG;
-  if ((int64_t)T * M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
-  // |sum_t 2^(t-1) I_t| <= (2^T - 1) K 127 must fit int32
-  if ((((int64_t)1 << T) - 1) * K * 127 >= ((int64_t)1 << 31)) return NMDLM_ERR_UNSUPPORTED;
-  if (!ws || !aligned(ws, 256) || ws_bytes < qbsm_ws(T, M, K, N)) return NMDLM_ERR_WORKSPACE;
+}  // extern "C"
 
+namespace {
+
+// The product on ternary spike planes, with the 2^(t-1)-weighted sum
+// (EPI_BITWISE, acc_out) or the modified IF neuron (EPI_MODIF, spike planes).
+nmdlm_status ternary_product(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M, int K,
+                             const int8_t* W, int N, int64_t ldw, int mode, int32_t* acc_out,
+                             const int64_t* thr_num, int64_t thr_den, uint64_t* out_pos,
+                             uint64_t* out_neg, int64_t* v_out, nmdlm_qbsm_stats* stats,
+                             unsigned flags, void* ws, size_t ws_bytes, void* stream) {
+  const int Nw = (N + 63) / 64;
   QbsmCall c;
   c.s_in = s_pos;
   c.s_neg = s_neg;
@@ -144,16 +148,16 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
   c.W = W;
   c.ldw = ldw;
   c.N = N;
-  c.mode = EPI_BITWISE;
+  c.mode = mode;
   c.bias = nullptr;
   c.cur_out = acc_out;
   c.theta_vec = nullptr;
   c.nseg = 1;
   c.seg_w = 1 << 30;
   for (int i = 0; i < kMaxSeg; ++i) {
-    c.seg[i].ptr = nullptr;
-    c.seg[i].ld_t = 0;
-    c.seg[i].ld_m = 0;
+    c.seg[i].ptr = out_pos;
+    c.seg[i].ld_t = (int64_t)M * Nw;
+    c.seg[i].ld_m = Nw;
     c.seg[i].theta = 1;
     c.seg[i].transposed = 0;
     c.seg[i].pos0 = 0;
@@ -174,12 +178,58 @@ nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, in
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;
+  c.thr_num = thr_num;
+  c.thr_den = thr_den;
+  c.s_neg_out = out_neg;
+  c.v_out = v_out;
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
   QbsmScratch scr;
   carve_qbsm_scratch(cv, qbsm_limits_single(T, M, K, N), &scr);
   if (!cv.ok) return NMDLM_ERR_WORKSPACE;
   return launch_qbsm(c, scr, static_cast<hipStream_t>(stream));
+}
+
+// Checks shared by the two ternary products.
+nmdlm_status ternary_args(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M, int K,
+                          const int8_t* W, int N, int64_t ldw, void* ws, size_t ws_bytes) {
+  if (!s_pos || !s_neg || T < 1 || M < 1 || K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
+  if (T > NMDLM_MAX_T || K > NMDLM_MAX_TERNARY_K) return NMDLM_ERR_UNSUPPORTED;
+  if (!weights_ok(W, K, N, ldw)) return NMDLM_ERR_INVALID_ARG;
+  if ((int64_t)T * M > (1 << 19)) return NMDLM_ERR_UNSUPPORTED;
+  if (!ws || !aligned(ws, 256) || ws_bytes < qbsm_ws(T, M, K, N)) return NMDLM_ERR_WORKSPACE;
+  return NMDLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nmdlm_status nmdlm_qbsm_ternary(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M, int K,
+                                const int8_t* W, int N, int64_t ldw, int32_t* acc_out,
+                                nmdlm_qbsm_stats* stats, unsigned flags, void* ws, size_t ws_bytes,
+                                void* stream) {
+  if (!acc_out) return NMDLM_ERR_INVALID_ARG;
+  const nmdlm_status rc = ternary_args(s_pos, s_neg, T, M, K, W, N, ldw, ws, ws_bytes);
+  if (rc != NMDLM_OK) return rc;
+  // |sum_t 2^(t-1) I_t| <= (2^T - 1) K 127 must fit int32
+  if ((((int64_t)1 << T) - 1) * K * 127 >= ((int64_t)1 << 31)) return NMDLM_ERR_UNSUPPORTED;
+  return ternary_product(s_pos, s_neg, T, M, K, W, N, ldw, EPI_BITWISE, acc_out, nullptr, 1,
+                         nullptr, nullptr, nullptr, stats, flags, ws, ws_bytes, stream);
+}
+
+nmdlm_status nmdlm_qbsm_ternary_if(const uint64_t* s_pos, const uint64_t* s_neg, int T, int M,
+                                   int K, const int8_t* W, int N, int64_t ldw,
+                                   const int64_t* thr_num, int64_t thr_den, uint64_t* out_pos,
+                                   uint64_t* out_neg, int64_t* v_out, nmdlm_qbsm_stats* stats,
+                                   unsigned flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!thr_num || !out_pos || !out_neg) return NMDLM_ERR_INVALID_ARG;
+  if (thr_den < 1) return NMDLM_ERR_INVALID_ARG;
+  if (thr_den > NMDLM_MAX_THR_DEN) return NMDLM_ERR_UNSUPPORTED;
+  const nmdlm_status rc = ternary_args(s_pos, s_neg, T, M, K, W, N, ldw, ws, ws_bytes);
+  if (rc != NMDLM_OK) return rc;
+  return ternary_product(s_pos, s_neg, T, M, K, W, N, ldw, EPI_MODIF, nullptr, thr_num, thr_den,
+                         out_pos, out_neg, v_out, stats, flags, ws, ws_bytes, stream);
 }
 
 nmdlm_status nmdlm_if_neuron(const int32_t* cur, int T, int M, int N, int32_t theta,

@@ -71,7 +71,8 @@ enum EpiMode : int {
   EPI_IF = 1,      // integrate-and-fire -> packed spikes
   EPI_QNL_IF = 2,  // table non-linearity, then integrate-and-fire
   EPI_HEAD = 3,    // sum over t, fp32 dequantisation -> logits
-  EPI_BITWISE = 4  // sum over t weighted 2^t (bitwise-coded input) -> int32 [M][N]
+  EPI_BITWISE = 4, // sum over t weighted 2^t (bitwise-coded input) -> int32 [M][N]
+  EPI_MODIF = 5    // modified IF over the bit-timesteps -> ternary spike planes
 };
 
 // Destination of the spikes of one column segment of a product.
@@ -128,6 +129,13 @@ struct QbsmArgs {
   int nparts;
   int dense;
   nmdlm_qbsm_stats* stats;
+  // EPI_MODIF: threshold thr_num[m] / thr_den per token; the +1 plane goes
+  // to seg[0], the -1 plane to s_neg_out (same layout); final membrane
+  // (times thr_den) to v_out [M][N] when given
+  const int64_t* thr_num;
+  int64_t thr_den;
+  uint64_t* s_neg_out;
+  int64_t* v_out;
 };
 
 // Scratch used by one product (carved from a workspace).
@@ -180,6 +188,10 @@ struct QbsmCall {
   const uint64_t* u_in;   // partial unions of s_in [u_nparts][ceil(K/64)] or null
   int u_nparts;
   uint64_t* u_out;        // where to write the partial unions of the output
+  const int64_t* thr_num; // EPI_MODIF (see QbsmArgs)
+  int64_t thr_den;
+  uint64_t* s_neg_out;
+  int64_t* v_out;
 };
 
 // Workspace layout helpers -------------------------------------------------

@@ -393,6 +393,37 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
     }
     return;
   }
+  if (a.mode == EPI_MODIF) {
+    // Eqs. (9)-(10): the modified IF neuron over the bit-timesteps t = 0..T-1
+    // of this row block's tokens (input weight 2^t, thresholds +-2^t Vth,
+    // Vth = thr_num[m] / thr_den; the membrane is kept times thr_den, in
+    // int64: integer arithmetic, exact), emitting ternary spike planes
+    const SpikeSeg& so = a.seg[0];
+    for (int ml = wave; ml < a.Mb; ml += NW) {
+      const int m = y * a.Mb + ml;
+      if (m >= a.M) break;
+      const long long num = a.thr_num[m];
+      const bool live = nv && num > 0;  // a zero threshold is silent
+      long long V = 0;
+      for (int t = 0; t < a.T; ++t) {
+        V += (a.thr_den << t) * (long long)sTile[(t * a.Mb + ml) * kTileLd + pc];
+        const long long thr = num << t;
+        const bool up = live && V >= thr;
+        const bool dn = live && !up && V <= -thr;
+        if (up) V -= thr;
+        if (dn) V += thr;
+        const uint64_t wp = __builtin_amdgcn_ballot_w64(up);
+        const uint64_t wn = __builtin_amdgcn_ballot_w64(dn);
+        if (lane == 0) {
+          const int64_t o = t * so.ld_t + (int64_t)m * so.ld_m + x;
+          so.ptr[o] = wp;
+          a.s_neg_out[o] = wn;
+        }
+      }
+      if (a.v_out && nv) a.v_out[(size_t)m * a.N + n] = V;
+    }
+    return;
+  }
   if (a.mode == EPI_HEAD) {
     const float sc = nv ? a.scale[n] : 0.f;
     for (int ml = wave; ml < a.Mb; ml += NW) {
@@ -1632,6 +1663,10 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.nparts = pa.nparts;
   a.dense = dense;
   a.stats = c.stats;
+  a.thr_num = c.thr_num;
+  a.thr_den = c.thr_den;
+  a.s_neg_out = c.s_neg_out;
+  a.v_out = c.v_out;
 
   const dim3 grid(gx, gy, P);
   hipEvent_t e0 = c.ev_begin, e1 = c.ev_end;

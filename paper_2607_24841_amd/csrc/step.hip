@@ -285,6 +285,10 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.u_in = nullptr;
   c.u_nparts = 0;
   c.u_out = nullptr;
+  c.thr_num = nullptr;
+  c.thr_den = 1;
+  c.s_neg_out = nullptr;
+  c.v_out = nullptr;
   return c;
 }
 

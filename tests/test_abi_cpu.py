@@ -186,12 +186,28 @@ def test_ternary_argument_errors(lib):
     assert prod(ldw=500) == B.NMDLM_ERR_INVALID_ARG
     assert prod(ws=None) == B.NMDLM_ERR_WORKSPACE
 
+    def prod_if(**kw):
+        a = dict(sp=FAKE, sn=FAKE, T=8, M=4, K=4096, W=FAKE, N=512, ldw=512, num=FAKE, den=8192,
+                 op=FAKE, on=FAKE, ws=FAKE, ws_bytes=1 << 30)
+        a.update(kw)
+        return lib.nmdlm_qbsm_ternary_if(a["sp"], a["sn"], a["T"], a["M"], a["K"], a["W"], a["N"],
+                                         a["ldw"], a["num"], a["den"], a["op"], a["on"], None,
+                                         None, 0, a["ws"], a["ws_bytes"], None)
+    assert prod_if(num=None) == B.NMDLM_ERR_INVALID_ARG
+    assert prod_if(on=None) == B.NMDLM_ERR_INVALID_ARG
+    assert prod_if(den=0) == B.NMDLM_ERR_INVALID_ARG
+    assert prod_if(den=(1 << 24) + 1) == B.NMDLM_ERR_UNSUPPORTED
+    assert prod_if(K=20000) == B.NMDLM_ERR_UNSUPPORTED
+    assert prod_if(T=9) == B.NMDLM_ERR_UNSUPPORTED
+    assert prod_if(ws_bytes=16) == B.NMDLM_ERR_WORKSPACE
+
 
 def test_binding_constants_match_the_header():
     text = open(HEADER).read()
     for name in ("NMDLM_FORCE_DENSE", "NMDLM_NO_HEAD", "NMDLM_ATTN_FUSED", "NMDLM_SPLIT_SHIFT",
                  "NMDLM_ROWTILE_SHIFT", "NMDLM_MAX_HEAD_M", "NMDLM_MAX_T", "NMDLM_MAX_K",
-                 "NMDLM_MAX_KEYS", "NMDLM_STATUS_TOKEN_CLAMPED"):
+                 "NMDLM_MAX_KEYS", "NMDLM_STATUS_TOKEN_CLAMPED", "NMDLM_MAX_THR_DEN",
+                 "NMDLM_NOALLOC_SCRATCH_BYTES"):
         m = re.search(r"#define\s+%s\s+([0-9xXa-fA-F]+)u?" % name, text)
         assert m, name
         if hasattr(B, name):
