@@ -385,52 +385,72 @@ def generate(model, prompt: np.ndarray, n_blocks: int, B: int, steps: int,
     return np.concatenate(out), log
 
 
+@dataclass
+class E2d2State:
+    """Key/value caches of the encoder layers and of the decoder layers."""
+    kc_enc: list
+    vc_enc: list
+    kc_dec: list
+    vc_dec: list
+
+
+def e2d2_new_state(model, n_enc: int, cap: int) -> E2d2State:
+    kc_e, vc_e = new_caches(n_enc, model.T, cap, model.d)
+    kc_d, vc_d = new_caches(model.n_layers - n_enc, model.T, cap, model.d)
+    return E2d2State(kc_e, vc_e, kc_d, vc_d)
+
+
+def e2d2_encode(model, n_enc: int, tokens: np.ndarray, C: int, state: E2d2State,
+                emb01: np.ndarray) -> np.ndarray:
+    """The encoder pass of Eq. (5) over the tokens at positions [C, C+M),
+    attending to the encoded context [0, C) and to themselves; then every
+    decoder layer writes the keys and values of those positions from the
+    encoder output h (its own projections of h: the decoder attends to the
+    encoder output).  Returns h (bool [T][M][d])."""
+    enc, dec = model.layers[:n_enc], model.layers[n_enc:]
+    X = block_input(np.asarray(tokens, dtype=np.int32), np.arange(C, C + len(tokens)), emb01,
+                    model.pos_ch)
+    h, _ = stack_forward(X, enc, state.kc_enc, state.vc_enc, C)
+    for l, L in enumerate(dec):
+        layer_forward(h, L, state.kc_dec[l], state.vc_dec[l], C)
+    return h
+
+
 def e2d2_generate(model, n_enc: int, prompt: np.ndarray, n_blocks: int, B: int, steps: int,
-                  k_unmask: int, emb01: np.ndarray | None = None):
+                  k_unmask: int, emb01: np.ndarray | None = None, return_state: bool = False):
     """Encoder-decoder block diffusion (Sec. III-A, Eqs. (5)-(6)): the first
     n_enc layers are the encoder f_enc, the others the decoder f_dec.
 
     The encoder gives h^b = f_enc(x^{<b}) (Eq. (5)) block-causally: the prompt
     is encoded once (bidirectional within it), and every finished block is
     encoded over the cached context plus itself, so each token passes the
-    encoder once.  Each decoder layer takes the keys and values of the
-    context positions from h, through its own projections of the encoder
-    output (the decoder attends to the encoder output).  A block starts as B
-    mask tokens; ``steps`` denoising steps z_{s+1} = f_dec(z_s, h^b) (Eq. (6))
-    run the decoder layers and the head over it, revealing ``k_unmask``
-    tokens each.  Returns (generated ids, chosen positions per step)."""
+    encoder once (e2d2_encode).  A block starts as B mask tokens; ``steps``
+    denoising steps z_{s+1} = f_dec(z_s, h^b) (Eq. (6)) run the decoder layers
+    and the head over it, revealing ``k_unmask`` tokens each.  Returns
+    (generated ids, chosen positions per step[, final E2d2State])."""
     import dataclasses
     if emb01 is None:
         emb01 = unpack_model_emb(model)
-    enc, dec = model.layers[:n_enc], model.layers[n_enc:]
+    dec = model.layers[n_enc:]
     dec_model = dataclasses.replace(model, layers=dec, n_layers=len(dec))
     P = len(prompt)
-    cap = P + n_blocks * B
-    kc_e, vc_e = new_caches(len(enc), model.T, cap, model.d)
-    kc_d, vc_d = new_caches(len(dec), model.T, cap, model.d)
-
-    def encode(tokens, C):
-        # the encoder over tokens at positions [C, C+M), then every decoder
-        # layer's keys/values of those positions from its output
-        X = block_input(np.asarray(tokens, dtype=np.int32), np.arange(C, C + len(tokens)), emb01,
-                        model.pos_ch)
-        h, _ = stack_forward(X, enc, kc_e, vc_e, C)
-        for l, L in enumerate(dec):
-            layer_forward(h, L, kc_d[l], vc_d[l], C)
-
-    encode(prompt, 0)
+    state = e2d2_new_state(model, n_enc, P + n_blocks * B)
+    e2d2_encode(model, n_enc, prompt, 0, state, emb01)
     C = P
     out, log = [], []
     for b in range(n_blocks):
         tokens = np.zeros(B, dtype=np.int32)
         masked = np.ones(B, dtype=bool)
         for s in range(steps):
-            r = block_step(dec_model, emb01, tokens, masked, C, C, kc_d, vc_d, k_unmask)
+            r = block_step(dec_model, emb01, tokens, masked, C, C, state.kc_dec, state.vc_dec,
+                           k_unmask)
             tokens, masked = r.tokens, r.masked
             log.append(r.chosen)
         out.append(tokens)
-        encode(tokens, C)
+        e2d2_encode(model, n_enc, tokens, C, state, emb01)
         C += B
+    if return_state:
+        return np.concatenate(out), log, state
     return np.concatenate(out), log
 
 

@@ -1,6 +1,6 @@
 """Write the stored expected values of the full-size MDLM cases.
 
-Usage:  python tests/golden/make_golden.py mdlm12|mdlm24
+Usage:  python tests/golden/make_golden.py mdlm12|mdlm24|e2d2
 
 Calls only the oracle (oracle/) and the seeded generator (workloads/); the
 HIP library is never imported here.  Outputs are JSON files next to this
@@ -92,6 +92,34 @@ def mdlm24():
         json.dump(out, f, indent=1)
 
 
+def e2d2():
+    t0 = time.time()
+    case = synth.e2d2_case()
+    m = case.model
+    P = len(case.prompt)
+    ids, log, st = O.e2d2_generate(m, case.n_enc, case.prompt, case.n_blocks, case.B,
+                                   case.steps, case.k_unmask, return_state=True)
+    J = P + case.n_blocks * case.B
+    kd, vd = cache_digests(st.kc_dec, st.vc_dec, J)
+    ke, ve = cache_digests(st.kc_enc[-1:], st.vc_enc[-1:], J)
+    out = {
+        "case": "encoder-decoder MDLM in the paper's shape: 28 encoder + 4 decoder layers, d=512, "
+                "8 heads x 64, FFN 1536, V=32000, T=8; prompt 64 ids, 4 blocks of 4 tokens, "
+                "4 denoising steps per block, 1 token unmasked per step",
+        "seed": synth.SEEDS["e2d2"],
+        "layout": "caches: packed spike rows uint64 [T][J][d/64], J = prompt + generated tokens",
+        "ids": ids.tolist(),
+        "chosen": [c.tolist() for c in log],
+        "dec_k_cache_sha256": kd,
+        "dec_v_cache_sha256": vd,
+        "last_enc_k_cache_sha256": ke[0],
+        "last_enc_v_cache_sha256": ve[0],
+        "seconds": round(time.time() - t0, 1),
+    }
+    with open(os.path.join(HERE, "e2d2_generation.json"), "w") as f:
+        json.dump(out, f, indent=1)
+
+
 if __name__ == "__main__":
     which = sys.argv[1] if len(sys.argv) > 1 else "mdlm12"
-    {"mdlm12": mdlm12, "mdlm24": mdlm24}[which]()
+    {"mdlm12": mdlm12, "mdlm24": mdlm24, "e2d2": e2d2}[which]()

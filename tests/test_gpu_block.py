@@ -350,3 +350,31 @@ def test_out_of_range_token_ids_are_clamped_and_reported():
     torch.cuda.synchronize()
     assert int(status.item()) == B.NMDLM_STATUS_TOKEN_CLAMPED
     assert_same(synth.unpack_bits(B.from_dev_bits(y), m.d), Yref, "Y")
+
+
+def test_e2d2_decoder_caches_hold_projections_of_the_encoder_output():
+    """The hand-built encoder-decoder model of the oracle pin (encoder output
+    known in closed form, decoder key/value projections that copy their
+    input): after the prompt and one block are encoded on the GPU, every
+    decoder cache row equals the oracle's, which the CPU test pins to the
+    closed form."""
+    torch, B = need_gpu()
+    from paper_2607_24841_amd.e2d2 import E2D2
+    from tests.test_e2d2_oracle import _hand_model
+    m = _hand_model()
+    emb01 = O.unpack_model_emb(m)
+    prompt = np.array([3, 0, 7, 5, 1, 1, 6, 2], dtype=np.int32)
+    blk = np.array([4, 2, 2, 0], dtype=np.int32)
+    st = O.e2d2_new_state(m, 1, 16)
+    O.e2d2_encode(m, 1, prompt, 0, st, emb01)
+    O.e2d2_encode(m, 1, blk, 8, st, emb01)
+    dm = B.DeviceModel.from_mdlm(m, 16)
+    g = E2D2(dm, 1, 8, 1, 4)
+    g.ctx[:12].copy_(torch.from_numpy(np.concatenate([prompt, blk])))
+    g.encode(0, 8)
+    g.encode(8, 4)
+    torch.cuda.synchronize()
+    ks, vs = _caches_to_host(dm, m.T, m.d, 12)
+    assert_same(ks[1], st.kc_dec[0][:, :12], "decoder keys")
+    assert_same(vs[1], st.vc_dec[0][:, :12], "decoder values")
+    assert_same(ks[0], st.kc_enc[0][:, :12], "encoder keys")

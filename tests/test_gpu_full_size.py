@@ -71,15 +71,38 @@ def _load(name):
         return json.load(f)
 
 
-def _chosen_ok(got, want, conf, tol=1e-9):
-    """Identical selections, or a difference confined to confidences that
-    tie (within tol) at the selection boundary."""
-    if list(got) == list(want):
+def _chosen_ok(got, want, conf, masked0=None, tol=1e-9):
+    """The selection is the stored one, or differs from it only where
+    confidences tie (within tol): the same number of positions, all
+    distinct and masked before the step, in order of non-increasing
+    confidence, and none of them less confident than a masked position left
+    out (ties allowed)."""
+    got, want = [int(g) for g in got], [int(w) for w in want]
+    if got == want:
         return True
-    if set(got) == set(want):
-        return all(abs(conf[a] - conf[b]) <= tol * max(conf[a], conf[b])
-                   for a, b in zip(got, want) if a != b)
-    return False
+    if len(got) != len(want) or len(set(got)) != len(got):
+        return False
+    cand = [p for p in range(len(conf)) if masked0 is None or masked0[p]]
+    if not set(got) <= set(cand):
+        return False
+    close = lambda a, b: abs(a - b) <= tol * max(abs(a), abs(b))
+    c = [conf[p] for p in got]
+    if any(c[i + 1] > c[i] and not close(c[i + 1], c[i]) for i in range(len(c) - 1)):
+        return False
+    left = [conf[p] for p in cand if p not in got]
+    return all(x <= min(c) or close(x, min(c)) for x in left)
+
+
+def _tokens_after(chosen, pred, tokens0, masked0):
+    """Tokens and masked flags after revealing `chosen` (Sec. III-A: a chosen
+    position takes its prediction; nothing else changes)."""
+    tok = np.array(tokens0, dtype=np.int64)
+    msk = np.array(masked0, dtype=np.int64)
+    for p in chosen:
+        if p >= 0:
+            tok[p] = pred[p]
+            msk[p] = 0
+    return tok.tolist(), msk.tolist()
 
 
 @pytest.mark.parametrize("flags", [0, 0x4, 4 << 20], ids=["default", "attn-fused", "dma"])
@@ -118,10 +141,14 @@ def test_mdlm12_step_matches_stored_oracle(flags):
     assert _sha(lg) == ref["logits_sha256"]
     assert pred.cpu().numpy().tolist() == ref["pred"]
     assert np.allclose(conf.cpu().numpy(), ref["conf"], rtol=1e-12, atol=0)
-    assert _chosen_ok(chosen.cpu().numpy().tolist(), ref["chosen"], ref["conf"])
-    if chosen.cpu().numpy().tolist() == ref["chosen"]:
-        assert tok.cpu().numpy().tolist() == ref["tokens"]
-        assert msk.cpu().numpy().tolist() == ref["masked"]
+    got = chosen.cpu().numpy().tolist()
+    assert _chosen_ok(got, ref["chosen"], ref["conf"], masked0=[1] * M)
+    # tokens and flags always: those of the stored step, or of a tie-equivalent choice
+    want_tok, want_msk = _tokens_after(got, ref["pred"], [0] * M, [1] * M)
+    if got == ref["chosen"]:
+        assert (want_tok, want_msk) == (ref["tokens"], ref["masked"])
+    assert tok.cpu().numpy().tolist() == want_tok
+    assert msk.cpu().numpy().tolist() == want_msk
     J = C + M
     for l, layer in enumerate(dm.layers):
         kd = _sha(B.from_dev_bits(layer.k_cache)[:, :J])
@@ -143,3 +170,42 @@ def test_mdlm24_generation_matches_stored_oracle():
     ids, log = generate(dm, case.prompt, case.n_blocks, case.B, case.steps, case.k_unmask)
     assert ids.tolist() == ref["ids"]
     assert [c.tolist() for c in log] == ref["chosen"]
+
+
+def _packed_caches(layer, cap, d, J):
+    """(K, V) of a device layer as packed spike rows [T][J][d/64] (the layout
+    the stored digests use)."""
+    from paper_2607_24841_amd import binding as B
+    k = B.from_dev_bits(layer.k_cache)[:, :J]
+    words = np.ascontiguousarray(B.from_dev_bits(layer.vt_cache).transpose(0, 2, 1))  # [T][d][cap/64]
+    vt = synth.unpack_bits(words, cap)
+    return np.ascontiguousarray(k), synth.pack_bits(vt.transpose(0, 2, 1)[:, :J])
+
+
+def test_e2d2_full_shape_matches_stored_oracle():
+    """The paper's own shape (28 encoder + 4 decoder layers, d=512, F=1536,
+    T=8, 64-id prompt, 4 blocks of 4 tokens, one token per step) against the
+    stored oracle generation: ids, every step's choice, the caches of every
+    decoder layer and of the last encoder layer."""
+    torch, B = need_gpu()
+    from paper_2607_24841_amd.e2d2 import E2D2
+    with open(os.path.join(GOLDEN, "e2d2_generation.json")) as f:
+        ref = json.load(f)
+    case = synth.e2d2_case()
+    m = case.model
+    P = len(case.prompt)
+    J = P + case.n_blocks * case.B
+    dm = B.DeviceModel.from_mdlm(m, J)
+    g = E2D2(dm, case.n_enc, P, case.n_blocks, case.B)
+    g.ctx[:P].copy_(torch.from_numpy(np.asarray(case.prompt, dtype=np.int32)))
+    log = []
+    C = g.generate(P, case.n_blocks, case.steps, case.k_unmask, log)
+    torch.cuda.synchronize()
+    assert g.ctx[P:C].cpu().numpy().tolist() == ref["ids"]
+    assert [c.cpu().numpy().tolist() for c in log] == ref["chosen"]
+    for l in range(m.n_layers - case.n_enc):
+        k, v = _packed_caches(dm.layers[case.n_enc + l], dm.cache_cap, m.d, J)
+        assert _sha(k) == ref["dec_k_cache_sha256"][l], f"decoder layer {l} keys"
+        assert _sha(v) == ref["dec_v_cache_sha256"][l], f"decoder layer {l} values"
+    k, v = _packed_caches(dm.layers[case.n_enc - 1], dm.cache_cap, m.d, J)
+    assert _sha(k) == ref["last_enc_k_cache_sha256"] and _sha(v) == ref["last_enc_v_cache_sha256"]

@@ -376,3 +376,20 @@ def test_generation_resume_from_block_snapshot():
         r = O.block_step(m, emb, tokens2, masked2, 14, 14, snap_k, snap_v, 2)
         tokens2, masked2 = r.tokens, r.masked
     assert np.array_equal(np.concatenate([tokens, tokens2]), full)
+
+
+def test_tie_equivalent_selection_checker():
+    """The full-size GPU tests accept a different set of unmasked positions
+    only across exact confidence ties at the boundary; check that rule on
+    hand-made cases (and that it rejects everything else)."""
+    from tests.test_gpu_full_size import _chosen_ok, _tokens_after
+    conf = [0.9, 0.5, 0.7, 0.7, 0.1]
+    assert _chosen_ok([0, 2], [0, 2], conf)
+    assert _chosen_ok([0, 3], [0, 2], conf)                 # 2 and 3 tie at the boundary
+    assert not _chosen_ok([0, 1], [0, 2], conf)             # 1 is less confident than 2, 3
+    assert not _chosen_ok([2, 0], [0, 2], conf)             # order must follow confidence
+    assert not _chosen_ok([0, 0], [0, 2], conf)
+    assert not _chosen_ok([0, 2], [0, 2, 3], conf)
+    assert not _chosen_ok([0, 4], [0, 2], conf, masked0=[1, 1, 1, 1, 1])
+    assert _tokens_after([2, 0], [5, 6, 7, 8, 9], [0, 0, 0, 0, 0], [1, 1, 1, 1, 1]) == \
+        ([5, 0, 7, 0, 0], [0, 1, 0, 1, 1])
