@@ -372,6 +372,114 @@ __device__ bool split_fixup(const QbsmArgs& a, int* sTile, int* sLast, int tid, 
   return true;
 }
 
+// Channel-major output of a row block (the value cache): the tokens' bits of
+// every (step, column) have met in ep.vbits; wave 0 writes them, in plain byte
+// stores when the block's tokens fill whole bytes of the position words (this
+// workgroup owns them), else by clearing and setting its bits with one pair
+// of atomics per word.
+__device__ __forceinline__ void write_channel_major(const QbsmArgs& a, const EpiStage& ep,
+                                                    SpikeSeg seg, int segi, int wave, int col,
+                                                    int n, bool nv, int y) {
+  const bool tr_bytes = (a.Mb & 7) == 0 && (seg.pos0 & 7) == 0;
+  if (wave == 0 && nv) {
+    const int ch = n - segi * a.seg_w;
+    // several sequences: the row block lies within sequence (y Mb) / seq_len
+    const int yb = y * a.Mb;
+    const int sq = seg.seq_len > 0 ? yb / seg.seq_len : 0;
+    const int p0 = seg.pos0 + (seg.seq_len > 0 ? yb - sq * seg.seq_len : yb);
+    seg.ptr += (int64_t)sq * seg.ld_s;
+    const int nvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the block, <= 32
+    if (tr_bytes) {
+      // p0 is a multiple of 8: store the (up to 4) bytes holding a token of
+      // the block; they may straddle two position words
+      const int nb = (nvalid + 7) >> 3;
+      for (int t = 0; t < a.T; ++t) {
+        const uint32_t bits = ep.vbits[t * 64 + col];
+        uint64_t* base = seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m;
+        for (int b = 0; b < nb; ++b) {
+          const int pb = (p0 >> 3) + b;  // byte index along the positions
+          uint8_t* wb = reinterpret_cast<uint8_t*>(base + (int64_t)(pb >> 3) * seg.ld_p);
+          wb[pb & 7] = (uint8_t)(bits >> (8 * b));
+        }
+      }
+    } else {
+      // the block's bits start at bit off of word p0/64 and may run into
+      // the next word
+      const int off = p0 & 63;
+      const uint64_t full = (nvalid >= 32) ? 0xFFFFFFFFull : ((1ull << nvalid) - 1ull);
+      const uint64_t m0 = full << off;
+      const uint64_t m1 = off ? (full >> (64 - off)) : 0ull;
+      for (int t = 0; t < a.T; ++t) {
+        unsigned long long* row = reinterpret_cast<unsigned long long*>(
+            seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + (int64_t)(p0 >> 6) * seg.ld_p);
+        const uint64_t bits = ep.vbits[t * 64 + col];
+        const uint64_t b0 = bits << off;
+        const uint64_t b1 = off ? (bits >> (64 - off)) : 0ull;
+        atomicAnd(row, ~m0);
+        if (b0) atomicOr(row, b0);
+        if (m1) {
+          atomicAnd(row + seg.ld_p, ~m1);
+          if (b1) atomicOr(row + seg.ld_p, b1);
+        }
+      }
+    }
+  }
+}
+
+// Integrate-and-fire of the tokens ml = wave, wave + NW, ... of a row block
+// (one sequence; no currents written), specialised at compile time for the
+// table non-linearity (QNL), a residual input (RES) and a channel-major output
+// (TR): a token's T currents (and residual words) are read, unconditionally,
+// before its membrane steps, so that the reads overlap, and each step is a
+// handful of instructions.  Natural outputs: word (t, m) of the column
+// segment at rowbase[t*ld_t + m*ld_m].
+template <int NW, bool QNL, bool RES, bool TR>
+__device__ __forceinline__ void if_tokens(const QbsmArgs& a, const int* sTile, const EpiStage& ep,
+                                          int lane, int wave, int y, int pc, bool nv, int bias_n,
+                                          int theta, uint64_t* rowbase, int64_t ld_t, int64_t ld_m,
+                                          uint32_t (&vb)[NMDLM_MAX_T], uint64_t& uor) {
+  const int T = a.T, Mb = a.Mb;
+  const int mlim = min(Mb, a.M - y * Mb);
+  for (int ml = wave; ml < mlim; ml += NW) {
+    int I[NMDLM_MAX_T];
+    unsigned long long rw[NMDLM_MAX_T];
+#pragma unroll
+    for (int t = 0; t < NMDLM_MAX_T; ++t) {  // steps past T re-read step T - 1 (unused)
+      const int tc = min(t, T - 1);
+      I[t] = sTile[(tc * Mb + ml) * kTileLd + pc] + bias_n;
+      rw[t] = RES ? ep.resid[tc * Mb + ml] : 0ull;
+    }
+    if constexpr (QNL) {
+#pragma unroll
+      for (int t = 0; t < NMDLM_MAX_T; ++t) {
+        const int q = min(127, max(-128, I[t] >> a.lut_shift));
+        I[t] = (int)ep.lut[q & 0xFF];
+      }
+    }
+    // the membrane is int64: T steps of currents up to 2^31 in magnitude
+    // plus theta stay exact
+    long long V = 0;
+    uint64_t* rp = TR ? nullptr : rowbase + (int64_t)(y * Mb + ml) * ld_m;
+#pragma unroll
+    for (int t = 0; t < NMDLM_MAX_T; ++t) {
+      if (t < T) {
+        long long Iv = I[t];
+        if (RES && ((rw[t] >> lane) & 1ull)) Iv += theta;
+        V += Iv;
+        const bool s = nv && V >= theta;
+        if (s) V -= theta;
+        if constexpr (TR) {
+          vb[t] |= (uint32_t)s << ml;
+        } else {
+          const uint64_t word = __builtin_amdgcn_ballot_w64(s);
+          uor |= word;
+          if (lane == 0) rp[t * ld_t] = word;
+        }
+      }
+    }
+  }
+}
+
 // Epilogue: currents, IF (optionally after the activation table), or head
 // logits, from the reduced tile; emits the partial union of the output.
 template <int NW>
@@ -443,17 +551,30 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   const bool spikes = a.mode != EPI_CUR;
   const bool tr = spikes && seg.transposed;
   // channel-major output (row blocks of at most 32 tokens): the waves' token
-  // bits meet in LDS and one wave writes them, in plain byte stores when the
-  // row block's tokens fill whole bytes of the position words (this workgroup
-  // owns them), else by clearing and setting its bits with one pair of
-  // atomics per word
-  const bool tr_bytes = tr && (a.Mb & 7) == 0 && (seg.pos0 & 7) == 0;
+  // bits meet in LDS and one wave writes them (write_channel_major)
   uint32_t vb[NMDLM_MAX_T];
 #pragma unroll
   for (int t = 0; t < NMDLM_MAX_T; ++t) vb[t] = 0u;
   uint64_t uor = 0ull;  // union of this wave's output words (wave-uniform)
 
-  for (int ml = wave; ml < a.Mb; ml += NW) {
+  // the common case (spikes only, one sequence) takes the specialised loop
+  const bool lean = spikes && !a.cur_out && seg.seq_len == 0;  // workgroup-uniform
+  if (lean) {
+    uint64_t* rb = seg.ptr + wseg;
+    const bool qnl = a.mode == EPI_QNL_IF, res = a.resid != nullptr;
+#define NMDLM_IF_TOKENS(Q, R, X)                                                                   \
+  if_tokens<NW, Q, R, X>(a, sTile, ep, lane, wave, y, pc, nv, bias_n, theta, rb, seg.ld_t, seg.ld_m, \
+                         vb, uor)
+    if (qnl) {
+      if (res) { if (tr) NMDLM_IF_TOKENS(true, true, true); else NMDLM_IF_TOKENS(true, true, false); }
+      else { if (tr) NMDLM_IF_TOKENS(true, false, true); else NMDLM_IF_TOKENS(true, false, false); }
+    } else {
+      if (res) { if (tr) NMDLM_IF_TOKENS(false, true, true); else NMDLM_IF_TOKENS(false, true, false); }
+      else { if (tr) NMDLM_IF_TOKENS(false, false, true); else NMDLM_IF_TOKENS(false, false, false); }
+    }
+#undef NMDLM_IF_TOKENS
+  }
+  for (int ml = wave; ml < a.Mb && !lean; ml += NW) {
     const int m = y * a.Mb + ml;
     if (m >= a.M) break;
     // the membrane (and a current with its residual) is int64: T steps of
@@ -500,49 +621,7 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
     for (int t = 0; t < NMDLM_MAX_T; ++t)
       if (t < a.T && vb[t]) atomicOr(&ep.vbits[t * 64 + col], vb[t]);
     __syncthreads();
-    if (wave == 0 && nv) {
-      const int ch = n - segi * a.seg_w;
-      // several sequences: the row block lies within sequence (y Mb) / seq_len
-      const int yb = y * a.Mb;
-      const int sq = seg.seq_len > 0 ? yb / seg.seq_len : 0;
-      const int p0 = seg.pos0 + (seg.seq_len > 0 ? yb - sq * seg.seq_len : yb);
-      seg.ptr += (int64_t)sq * seg.ld_s;
-      const int nvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the block, <= 32
-      if (tr_bytes) {
-        // p0 is a multiple of 8: store the (up to 4) bytes holding a token of
-        // the block; they may straddle two position words
-        const int nb = (nvalid + 7) >> 3;
-        for (int t = 0; t < a.T; ++t) {
-          const uint32_t bits = ep.vbits[t * 64 + col];
-          uint64_t* base = seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m;
-          for (int b = 0; b < nb; ++b) {
-            const int pb = (p0 >> 3) + b;  // byte index along the positions
-            uint8_t* wb = reinterpret_cast<uint8_t*>(base + (int64_t)(pb >> 3) * seg.ld_p);
-            wb[pb & 7] = (uint8_t)(bits >> (8 * b));
-          }
-        }
-      } else {
-        // the block's bits start at bit off of word p0/64 and may run into
-        // the next word
-        const int off = p0 & 63;
-        const uint64_t full = (nvalid >= 32) ? 0xFFFFFFFFull : ((1ull << nvalid) - 1ull);
-        const uint64_t m0 = full << off;
-        const uint64_t m1 = off ? (full >> (64 - off)) : 0ull;
-        for (int t = 0; t < a.T; ++t) {
-          unsigned long long* row = reinterpret_cast<unsigned long long*>(
-              seg.ptr + t * seg.ld_t + (int64_t)ch * seg.ld_m + (int64_t)(p0 >> 6) * seg.ld_p);
-          const uint64_t bits = ep.vbits[t * 64 + col];
-          const uint64_t b0 = bits << off;
-          const uint64_t b1 = off ? (bits >> (64 - off)) : 0ull;
-          atomicAnd(row, ~m0);
-          if (b0) atomicOr(row, b0);
-          if (m1) {
-            atomicAnd(row + seg.ld_p, ~m1);
-            if (b1) atomicOr(row + seg.ld_p, b1);
-          }
-        }
-      }
-    }
+    write_channel_major(a, ep, seg, segi, wave, col, n, nv, y);
   }
   if (a.u_out && spikes && !tr) {
     // partial union of this row block's output word, for the next product
