@@ -85,7 +85,8 @@ def parse():
 TRAFFIC = {
     "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
               "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "", "bytes_per_launch": None},
+    "mdlm12": {"sources_sha256": "5df81632aad451651882ef1982e3faa4710ecf07bcbba6b9ae45cbe8f518cb6e",
+               "bytes_per_launch": 8728878.1},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
