@@ -58,7 +58,9 @@ typedef enum nmdlm_status {
 /* bits 20..22: product kernel (0 = automatic; 1 = separate pass building the
  * active-row list; 2 = single kernel with an in-kernel list; 3 = single
  * kernel over 64-channel words, loading only active rows into registers;
- * 4 = as 3, gathering the active rows straight into LDS).  Results do not
+ * 4 = as 3, gathering the active rows straight into LDS; 5 = as 3 with a
+ * scalar gather-accumulate product in place of MFMA: per spike of a row,
+ * the active weight row's columns are loaded and added).  Results do not
  * depend on it. */
 #define NMDLM_PATH_SHIFT 20u
 #define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)

@@ -38,6 +38,7 @@ NMDLM_NO_FUSE = 1 << NMDLM_PATH_SHIFT      # separate pass building the active-r
 NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
 NMDLM_PATH_WORDS = 3 << NMDLM_PATH_SHIFT   # single kernel over 64-channel words
 NMDLM_PATH_DMA = 4 << NMDLM_PATH_SHIFT     # as words, active rows gathered into LDS
+NMDLM_PATH_SCALAR = 5 << NMDLM_PATH_SHIFT  # as words, scalar gather-accumulate product
 NMDLM_QNL_S8 = 0
 NMDLM_QNL_U8 = 1
 

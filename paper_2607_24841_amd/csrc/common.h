@@ -136,6 +136,8 @@ struct QbsmArgs {
   int64_t thr_den;
   uint64_t* s_neg_out;
   int64_t* v_out;
+  // word product: 0 = MFMA, 1 = scalar gather-accumulate
+  int accum;
 };
 
 // Scratch used by one product (carved from a workspace).

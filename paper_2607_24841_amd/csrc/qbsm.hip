@@ -723,6 +723,72 @@ __device__ __forceinline__ void stats_write(const QbsmArgs& a, int total) {
   a.stats->weight_bytes = (int64_t)total * (int64_t)a.N;
 }
 
+// ------------------------------------------------- scalar accumulation
+// The gather-accumulate product (path 5; on MI355X it measured no faster than
+// MFMA at any point of the FFN sweep d=4096 -> 14336 -> 4096, density 0.02 to
+// 0.30, so the automatic choice keeps MFMA): each thread takes a
+// task (block row lr, column quad j) and a slice of the words of K (w0 + s,
+// w0 + s + S, ...); for every spike k of the row in its words it loads the
+// four weights W[k][4j .. 4j+3] (one dword) and adds them, sign-extended, to
+// four int32 sums, which meet in the tile (LDS atomics, physical column
+// order).  A row's spikes are taken eight at a time, each group's loads all
+// in flight (lanes past the last spike re-load the group's first row and add
+// nothing).  Integer addition: the sums equal the MFMA path's exactly.  Only
+// the rows of the block's tokens get tasks, and the slices spread the spikes
+// of a row over the threads left.
+constexpr int kScalarGroup = 8;
+
+template <int ROWS, int NT>
+__device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds_row, int* sTile,
+                                  int tid, int x, int y, int w0, int w1) {
+  const int mvalid = min(a.Mb, a.M - y * a.Mb);  // tokens of the row block
+  const int rows = a.T * mvalid;                 // rows with spikes: t * Mb + ml, ml < mvalid
+  const int tasks = rows * 16;
+  if (tasks <= 0) return;
+  const int S = NT >= tasks ? NT / tasks : 1;    // word slices per task
+  const int nwork = NT >= tasks ? tasks * S : NT;
+  if (tid >= nwork) return;
+  const float inv_mv = 1.0f / (float)mvalid;
+  const char* Wb = reinterpret_cast<const char*>(a.W);
+  const uint32_t ldw = (uint32_t)a.ldw;
+  for (int task = NT >= tasks ? tid % tasks : tid; task < tasks; task += NT >= tasks ? tasks : NT) {
+    const int slice = NT >= tasks ? tid / tasks : 0;
+    const int r = task >> 4, j = task & 15;
+    const int t = div_small(r, inv_mv), ml = r - t * mvalid;
+    const int lr = t * a.Mb + ml;
+    const int col = x * 64 + 4 * j;
+    if (col >= a.N) continue;  // ldw is a multiple of 16 >= N: the dword of a valid quad is in the row
+    int s4[4] = {0, 0, 0, 0};
+    for (int w = w0 + slice; w < w1; w += S) {
+      unsigned long long word = (unsigned long long)sS[lr * lds_row + 2 * w] |
+                                ((unsigned long long)sS[lr * lds_row + 2 * w + 1] << 32);
+      while (word) {
+        const int kfirst = w * 64 + (int)__builtin_ctzll(word);
+        uint32_t wv[kScalarGroup];
+        uint32_t valid = 0u;
+#pragma unroll
+        for (int i = 0; i < kScalarGroup; ++i) {
+          const bool v = word != 0ull;
+          const int k = v ? w * 64 + (int)__builtin_ctzll(word) : kfirst;
+          valid |= (uint32_t)v << i;
+          word &= word - 1ull;  // 0 stays 0
+          wv[i] = *reinterpret_cast<const uint32_t*>(Wb + (uint32_t)k * ldw + (uint32_t)col);
+        }
+#pragma unroll
+        for (int i = 0; i < kScalarGroup; ++i) {
+          const int m = -(int)((valid >> i) & 1u);  // all ones for a spike of the group
+          const int q = (int)wv[i] & m;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) s4[b] += (int)(signed char)(q >> (8 * b));
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      if (s4[b]) atomicAdd(&sTile[lr * kTileLd + phys_col(4 * j + b)], s4[b]);
+  }
+}
+
 // ------------------------------------------------- word-granular product
 // k-steps are the original 64-channel words.  The A operand comes straight
 // from the staged spike rows (no list, no compaction).  Within a word, a lane
@@ -969,8 +1035,10 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
         acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
     }
   };
+  // MFMA over the words, or (requested) the scalar gather-accumulate product
+  const bool scalar = !TERN && a.accum == 1 && !a.dense;  // workgroup-uniform
   int jw = w0 + wave;
-  if (first != 0x7fffffff && jw < w1) {  // wave-uniform
+  if (!scalar && first != 0x7fffffff && jw < w1) {  // wave-uniform
     uint32_t xa[16], xb[16];
     load_word(jw, xa);
     while (true) {
@@ -984,9 +1052,10 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       if (jw >= w1) break;
     }
   }
+  if (scalar) scalar_accumulate<ROWS, NT>(a, sS, lds_row, sTile, tid, x, y, w0, w1);
 
   __syncthreads();
-  reduce_tile<RT>(acc, sTile, g, c);
+  if (!scalar) reduce_tile<RT>(acc, sTile, g, c);
   if (stats_wg) stats_count<NT>(a, from_parts ? sLU : sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
   if (stats_wg && tid == 0) stats_write(a, sStatCnt);
@@ -1623,6 +1692,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
     if (words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
   }
+  // 5: the word product with the scalar gather-accumulate product
+  int accum = 0;
+  if (path == 5) {
+    accum = 1;
+    path = 3;
+  }
   if (path == 3 && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
@@ -1746,6 +1821,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.thr_den = c.thr_den;
   a.s_neg_out = c.s_neg_out;
   a.v_out = c.v_out;
+  a.accum = accum;
 
   const dim3 grid(gx, gy, P);
   hipEvent_t e0 = c.ev_begin, e1 = c.ev_end;

@@ -122,9 +122,9 @@ def test_block_step_graph_replays_match_eager():
 
 
 @pytest.mark.parametrize("flags", [1 << 8, 3 << 8, (2 << 8) | (1 << 16), 1 << 20, 2 << 20, 3 << 20,
-                                   4 << 20, 0x4, 2 << 16, 8 << 16],
+                                   4 << 20, 0x4, 2 << 16, 8 << 16, 5 << 20, (5 << 20) | (1 << 16)],
                          ids=["P1", "P3", "P2RT1", "nofuse", "fused", "words", "dma", "attn-fused",
-                              "RT2-bytes", "RT8"])
+                              "RT2-bytes", "RT8", "scalar", "scalar-RT1"])
 def test_block_forced_paths(flags):
     need_gpu()
     _check_block(synth.block_case(), flags=flags)

@@ -56,6 +56,7 @@ def test_tiny_and_ragged_shapes(shape):
 NOFUSE = 1 << 20      # prep pass + list kernel
 FUSED = 2 << 20       # single kernel, in-kernel list
 WORDS = 3 << 20       # single kernel over 64-channel words
+SCALAR = 5 << 20      # words, scalar gather-accumulate product
 DMA = 4 << 20         # as WORDS, active rows gathered into LDS
 
 _FORCED = {
@@ -71,7 +72,28 @@ _FORCED = {
     "dma": DMA, "dma-dense": DMA | 0x1, "dma-P3": DMA | (3 << 8), "dma-RT1": DMA | (1 << 16),
     "dma-RT2": DMA | (2 << 16), "dma-RT4": DMA | (4 << 16), "dma-RT8": DMA | (8 << 16),
     "dma-P2RT2": DMA | (2 << 8) | (2 << 16),
+    "scalar": SCALAR, "scalar-dense": SCALAR | 0x1, "scalar-P3": SCALAR | (3 << 8),
+    "scalar-RT1": SCALAR | (1 << 16), "scalar-RT2": SCALAR | (2 << 16),
+    "scalar-RT4": SCALAR | (4 << 16), "scalar-RT8": SCALAR | (8 << 16),
 }
+
+
+@pytest.mark.parametrize("flags", [SCALAR, SCALAR | (1 << 16), SCALAR | (8 << 16), SCALAR | (2 << 8)],
+                         ids=["scalar", "scalar-RT1", "scalar-RT8", "scalar-P2"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"T{s[0]}M{s[1]}K{s[2]}N{s[3]}" for s in SHAPES])
+def test_scalar_ragged_shapes(shape, flags):
+    need_gpu()
+    T, M, K, N, p = shape
+    _check(synth.make_qbsm_case(100 + K + N, T, M, K, N, p), flags=flags)
+
+
+@pytest.mark.parametrize("density", [0.001, 0.01, 0.05, 0.3])
+def test_scalar_across_densities(density):
+    # the scalar product from nearly empty to dense rows, short and long K
+    need_gpu()
+    for flags in (0, SCALAR):
+        _check(synth.make_qbsm_case(int(1000 * density) + 7, 4, 20, 4096, 300, density), flags=flags)
+        _check(synth.make_qbsm_case(int(1000 * density) + 8, 4, 1, 14336, 256, density), flags=flags)
 
 
 @pytest.mark.parametrize("flags", list(_FORCED.values()), ids=list(_FORCED))
@@ -81,8 +103,8 @@ def test_forced_paths_equal(flags):
     _check(case, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, NOFUSE, FUSED, WORDS, DMA],
-                         ids=["auto", "nofuse", "fused", "words", "dma"])
+@pytest.mark.parametrize("flags", [0, NOFUSE, FUSED, WORDS, DMA, SCALAR],
+                         ids=["auto", "nofuse", "fused", "words", "dma", "scalar"])
 def test_degenerate_inputs(flags):
     need_gpu()
     c = synth.make_qbsm_case(9, 4, 8, 256, 128, 0.1)
@@ -92,7 +114,8 @@ def test_degenerate_inputs(flags):
     _check(c, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS, DMA], ids=["auto", "nofuse", "words", "dma"])
+@pytest.mark.parametrize("flags", [0, NOFUSE, WORDS, DMA, SCALAR],
+                         ids=["auto", "nofuse", "words", "dma", "scalar"])
 def test_large_k_shapes(flags):
     need_gpu()
     # K beyond the in-kernel-list limit, and a long block (many row blocks)
@@ -160,11 +183,11 @@ def test_determinism():
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[3], b[3])
 
 
-LARGE_BIAS_PATHS = [0, NOFUSE, FUSED, WORDS, DMA]
+LARGE_BIAS_PATHS = [0, NOFUSE, FUSED, WORDS, DMA, SCALAR]
 
 
 @pytest.mark.parametrize("T", [4, 8])
-@pytest.mark.parametrize("path", LARGE_BIAS_PATHS, ids=["auto", "list", "fused", "words", "dma"])
+@pytest.mark.parametrize("path", LARGE_BIAS_PATHS, ids=["auto", "list", "fused", "words", "dma", "scalar"])
 def test_membrane_beyond_int32_with_large_bias(T, path):
     """Biases near 2^30 with a threshold near 1.6e9: the membrane passes 2^31
     after two steps, so the fused IF must integrate in 64 bits as the oracle
