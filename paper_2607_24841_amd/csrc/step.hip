@@ -40,41 +40,30 @@ __global__ __launch_bounds__(256) void k_assemble(const uint64_t* __restrict__ e
 }
 
 // Per token: argmax of the logits (ties -> smallest id) and the largest
-// softmax probability 1 / sum_v exp(l_v - l_max) in fp64.
-// Confidence of one token (one workgroup): pred = argmax_v logit (ties ->
-// smallest v), conf = 1 / sum_v exp(logit_v - logit_pred) in float64.
-constexpr int kConfThreads = 1024;
-constexpr int kConfUnroll = 8;
+// softmax probability 1 / sum_v exp(l_v - l_max) in float64, in two passes
+// spread over the chip.  k_conf_part: workgroup (m, c) takes logits
+// [c*kConfChunk, (c+1)*kConfChunk) of token m and records their largest
+// value, its id (ties: the smallest) and sum exp(l_v - that) in float64.
+// k_conf: l_max is the largest chunk maximum (ties: the first chunk, whose
+// ids are the smaller) and sum_v exp(l_v - l_max) = sum_chunks
+// sum_chunk * exp(chunk max - l_max).
+struct ConfPart {
+  float mx;
+  int32_t arg;
+  double sum;
+};
+constexpr int kConfThreads = 256;
+constexpr int kConfPerThread = 8;
+constexpr int kConfChunk = kConfThreads * kConfPerThread;
 
 __device__ __forceinline__ bool conf_better(float a, int ia, float b, int ib) {
   return a > b || (a == b && ia < ib);
 }
 
-__global__ __launch_bounds__(kConfThreads) void k_conf(const float* __restrict__ logits, int V,
-                                                       int32_t* __restrict__ pred,
-                                                       double* __restrict__ conf) {
+// Arg-max over the workgroup (ties -> smaller id); every thread gets it.
+__device__ __forceinline__ void block_argmax(float& best, int& bi, float* sBest, int* sIdx) {
   constexpr int NW = kConfThreads / 64;
-  __shared__ float sBest[NW];
-  __shared__ int sIdx[NW];
-  __shared__ double sSum[NW];
-  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float* row = logits + (size_t)m * V;
-  // pass 1: arg-max; each batch of loads is unconditional (clamped index)
-  float best = -FLT_MAX;
-  int bi = 0x7fffffff;
-  for (int v0 = tid; v0 < V; v0 += kConfThreads * kConfUnroll) {
-    float xs[kConfUnroll];
-#pragma unroll
-    for (int u = 0; u < kConfUnroll; ++u) xs[u] = row[min(v0 + u * kConfThreads, V - 1)];
-#pragma unroll
-    for (int u = 0; u < kConfUnroll; ++u) {
-      const int v = v0 + u * kConfThreads;
-      if (v < V && conf_better(xs[u], v, best, bi)) {
-        best = xs[u];
-        bi = v;
-      }
-    }
-  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int o = 32; o > 0; o >>= 1) {
     const float ob = __shfl_xor(best, o);
     const int oi = __shfl_xor(bi, o);
@@ -95,23 +84,78 @@ __global__ __launch_bounds__(kConfThreads) void k_conf(const float* __restrict__
       best = sBest[w];
       bi = sIdx[w];
     }
-  // pass 2: sum of exp(logit - max) in float64
-  const double mx = (double)best;
-  double acc = 0.0;
-  for (int v0 = tid; v0 < V; v0 += kConfThreads * kConfUnroll) {
-    float xs[kConfUnroll];
-#pragma unroll
-    for (int u = 0; u < kConfUnroll; ++u) xs[u] = row[min(v0 + u * kConfThreads, V - 1)];
-#pragma unroll
-    for (int u = 0; u < kConfUnroll; ++u)
-      if (v0 + u * kConfThreads < V) acc += exp((double)xs[u] - mx);
-  }
+}
+
+// Sum over the workgroup; thread 0 gets it.
+__device__ __forceinline__ double block_sum(double acc, double* sSum) {
+  constexpr int NW = kConfThreads / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
   if (lane == 0) sSum[wave] = acc;
   __syncthreads();
+  double sum = 0.0;
+  for (int w = 0; w < NW; ++w) sum += sSum[w];
+  return sum;
+}
+
+__global__ __launch_bounds__(kConfThreads) void k_conf_part(const float* __restrict__ logits, int V,
+                                                            ConfPart* __restrict__ part) {
+  __shared__ float sBest[kConfThreads / 64];
+  __shared__ int sIdx[kConfThreads / 64];
+  __shared__ double sSum[kConfThreads / 64];
+  const int m = blockIdx.y, ch = blockIdx.x, tid = threadIdx.x;
+  const float* row = logits + (size_t)m * V;
+  const int v0 = ch * kConfChunk + tid;
+  // every load is issued (at a clamped index) before the first is used
+  float xs[kConfPerThread];
+#pragma unroll
+  for (int u = 0; u < kConfPerThread; ++u) xs[u] = row[min(v0 + u * kConfThreads, V - 1)];
+  float best = -FLT_MAX;
+  int bi = 0x7fffffff;
+#pragma unroll
+  for (int u = 0; u < kConfPerThread; ++u) {
+    const int v = v0 + u * kConfThreads;
+    if (v < V && conf_better(xs[u], v, best, bi)) {
+      best = xs[u];
+      bi = v;
+    }
+  }
+  block_argmax(best, bi, sBest, sIdx);
+  const double mx = (double)best;
+  double acc = 0.0;
+#pragma unroll
+  for (int u = 0; u < kConfPerThread; ++u)
+    if (v0 + u * kConfThreads < V) acc += exp((double)xs[u] - mx);
+  const double sum = block_sum(acc, sSum);
+  if (tid == 0) part[(size_t)m * gridDim.x + ch] = ConfPart{best, bi, sum};
+}
+
+__global__ __launch_bounds__(kConfThreads) void k_conf(const ConfPart* __restrict__ part, int nch,
+                                                       int32_t* __restrict__ pred,
+                                                       double* __restrict__ conf) {
+  __shared__ float sBest[kConfThreads / 64];
+  __shared__ int sIdx[kConfThreads / 64];
+  __shared__ double sSum[kConfThreads / 64];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const ConfPart* row = part + (size_t)m * nch;
+  float best = -FLT_MAX;
+  int bi = 0x7fffffff;
+  for (int i = tid; i < nch; i += kConfThreads) {
+    const ConfPart p = row[i];
+    if (conf_better(p.mx, p.arg, best, bi)) {
+      best = p.mx;
+      bi = p.arg;
+    }
+  }
+  block_argmax(best, bi, sBest, sIdx);
+  const double mx = (double)best;
+  double acc = 0.0;
+  for (int i = tid; i < nch; i += kConfThreads) {
+    const ConfPart p = row[i];
+    acc += p.sum * exp((double)p.mx - mx);
+  }
+  const double sum = block_sum(acc, sSum);
   if (tid == 0) {
-    double sum = 0.0;
-    for (int w = 0; w < NW; ++w) sum += sSum[w];
     pred[m] = bi;
     conf[m] = 1.0 / sum;
   }
@@ -137,6 +181,35 @@ __global__ __launch_bounds__(64) void k_unmask(int32_t* __restrict__ tokens,
   pred += so;
   conf += so;
   if (chosen) chosen += (size_t)blockIdx.x * k;
+  if (M <= 64) {
+    // one position per lane: its rank among the masked positions (higher
+    // confidence first, ties to the lower position) decides it in one pass;
+    // the r-th chosen position is the one of rank r (the order the
+    // one-at-a-time selection takes them in)
+    const bool mv = lane < M && masked[lane];
+    const double cm = mv ? conf[lane] : 0.0;
+    const uint64_t mm = __builtin_amdgcn_ballot_w64(mv);
+    int rank = 0;
+    const unsigned long long cbits = __double_as_longlong(cm);
+    for (uint64_t rest = mm; rest; rest &= rest - 1) {
+      const int j = (int)__builtin_ctzll(rest);  // wave-uniform
+      const unsigned long long bj =
+          ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(cbits >> 32), j) << 32) |
+          (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)cbits, j);
+      const double cj = __longlong_as_double((long long)bj);
+      rank += (cj > cm || (cj == cm && j < lane)) ? 1 : 0;
+    }
+    if (mv && rank < k) {
+      tokens[lane] = pred[lane];
+      masked[lane] = 0;
+      if (chosen) chosen[rank] = lane;
+    }
+    const int nm = __popcll(mm);
+    if (chosen)
+      for (int r = lane; r < k; r += 64)
+        if (r >= nm) chosen[r] = -1;  // fewer masked positions than k
+    return;
+  }
   uint64_t mine = 0ull;
   for (int jj = 0, m = lane; m < M; ++jj, m += 64)
     if (masked[m]) mine |= 1ull << jj;
@@ -185,7 +258,8 @@ struct StepBuffers {
   uint64_t* uX1;    // partial unions of X1 [M][dw] (at most one per token)
   uint64_t* uH;     // partial unions of H  [M][Fw]
   uint64_t* uY[2];  // partial unions of Y  [M][dw]
-  float* logits;    // [M][V]
+  float* logits;    // [M][V] (when the caller gives none)
+  ConfPart* cpart;  // [M][ceil(V/kConfChunk)] confidence partials
   int32_t* pred;
   double* conf;
   QbsmScratch qs;
@@ -225,6 +299,7 @@ static void carve_step(Carver& cv, const nmdlm_model* md, int M, unsigned flags,
   b->uY[1] = cv.take<uint64_t>((size_t)M * dw);
   const bool head = !(flags & NMDLM_NO_HEAD);
   b->logits = (head && need_logits) ? cv.take<float>((size_t)M * md->V) : nullptr;
+  b->cpart = head ? cv.take<ConfPart>((size_t)M * ((md->V + kConfChunk - 1) / kConfChunk)) : nullptr;
   b->pred = (head && need_pred) ? cv.take<int32_t>(M) : nullptr;
   b->conf = (head && need_conf) ? cv.take<double>(M) : nullptr;
   carve_qbsm_scratch(cv, step_limits(md, M, flags), &b->qs);
@@ -431,7 +506,10 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
   hc.u_nparts = uX_parts;
   attach_events(hc, io, 4 * md->n_layers);
   if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
-  hipLaunchKernelGGL(k_conf, dim3(M), dim3(kConfThreads), 0, st, logits, md->V, pred, conf);
+  const int nch = (md->V + kConfChunk - 1) / kConfChunk;
+  hipLaunchKernelGGL(k_conf_part, dim3(nch, M), dim3(kConfThreads), 0, st, logits, md->V, b.cpart);
+  if ((rc = hip_status()) != NMDLM_OK) return rc;
+  hipLaunchKernelGGL(k_conf, dim3(M), dim3(kConfThreads), 0, st, b.cpart, nch, pred, conf);
   if ((rc = hip_status()) != NMDLM_OK) return rc;
   hipLaunchKernelGGL(k_unmask, dim3(n_seq), dim3(64), 0, st, io->tokens, io->masked, pred, conf,
                      Ms, io->k_unmask, io->unmasked_pos);
