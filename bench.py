@@ -85,8 +85,8 @@ def parse():
 TRAFFIC = {
     "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
               "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "5df81632aad451651882ef1982e3faa4710ecf07bcbba6b9ae45cbe8f518cb6e",
-               "bytes_per_launch": 8728878.1},
+    "mdlm12": {"sources_sha256": "029e59b1e72c13e081e52d2726f0fdc5e26a39a2cd2959e6bbceef9651aa9dd9",
+               "bytes_per_launch": 8745116.9},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
