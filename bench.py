@@ -61,6 +61,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--copies", type=int, default=32, help="rotating layer copies (>= 256 MB total)")
     p.add_argument("--eager", action="store_true", help="issue kernels directly, no HIP graph")
+    p.add_argument("--weights", choices=("rows", "blocked"), default="rows",
+                   help="rows: row-major weights only; blocked: also the blocked copies, read by "
+                        "products over dense unions")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="host seconds of oracle steps for cpu_baseline")
@@ -441,7 +444,7 @@ def bench_mdlm12_step(args):
     case = synth.mdlm12_step_case()
     m = case.model
     C, M, k = case.C, case.B, case.k_unmask
-    dm = B.DeviceModel.from_mdlm(m, C + M)
+    dm = B.DeviceModel.from_mdlm(m, C + M, blocked=args.weights == "blocked")
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
                          B.nmdlm_block_step_workspace_size(dm, M, 0)))
     ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()
@@ -531,7 +534,8 @@ def bench_mdlm12_step(args):
                                "tokens over 1024 context tokens (prefilled, untimed), head + "
                                "confidence + top-8 unmasking",
                    "block_tokens": M, "context_tokens": C, "layers": m.n_layers,
-                   "issue": "eager" if args.eager else "hip_graph (one step per replay)"},
+                   "issue": "eager" if args.eager else "hip_graph (one step per replay)",
+                   "weights": args.weights},
         "step_ms_percentiles": pct,
         "timing_check": {"ms_per_step_over_replay_p50": ms_per_step / pct["p50"]},
         "unmasked_tokens_per_s": k / (ms_per_step * 1e-3),
@@ -567,7 +571,7 @@ def bench_mdlm24_generate(args):
     case = synth.mdlm24_generation_case()
     m = case.model
     P = len(case.prompt)
-    dm = B.DeviceModel.from_mdlm(m, P + case.n_blocks * case.B)
+    dm = B.DeviceModel.from_mdlm(m, P + case.n_blocks * case.B, blocked=args.weights == "blocked")
     gen = Generator(dm, P, case.B)
     ids = torch.from_numpy(np.asarray(case.prompt, dtype=np.int32)).cuda()
     # warm run (fills the caches, loads code), then the timed one
@@ -592,7 +596,8 @@ def bench_mdlm24_generate(args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": "24-layer spiking MDLM generation: prompt 2048 ids, 8 blocks x 32 "
-                               "tokens, 8 denoising steps per block, 4 unmasked per step"},
+                               "tokens, 8 denoising steps per block, 4 unmasked per step",
+                   "weights": args.weights},
         "generated_tokens_per_s": n_tok / (t_gen * 1e-3),
         "generated_tokens_per_s_with_prefill": n_tok / ((t_pre + t_gen) * 1e-3),
         "prefill_ms": t_pre, "generation_ms": t_gen, "issue": "eager",
@@ -695,7 +700,7 @@ def bench_e2d2_generate(args):
     case = synth.e2d2_case()
     m = case.model
     P, nb, Bk = len(case.prompt), case.n_blocks, case.B
-    dm = B.DeviceModel.from_mdlm(m, P + nb * Bk)
+    dm = B.DeviceModel.from_mdlm(m, P + nb * Bk, blocked=args.weights == "blocked")
     g = E2D2(dm, case.n_enc, P, nb, Bk)
     g.ctx[:P].copy_(torch.from_numpy(np.asarray(case.prompt, dtype=np.int32)))
 
@@ -828,7 +833,8 @@ def bench_block(args):
     T, C_ctx, M, d, H, F = case.T, case.C, case.M, L.d, L.H, L.F
 
     # --- device state (untimed): layer copies, prefilled caches ----------------
-    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F) for _ in range(args.copies)]
+    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F, blocked=args.weights == "blocked")
+           for _ in range(args.copies)]
     nb = max(B.nmdlm_block_step_workspace_size(dms[0], C_ctx, B.NMDLM_NO_HEAD),
              B.nmdlm_block_step_workspace_size(dms[0], M, B.NMDLM_NO_HEAD))
     ws = B.workspace(nb)
@@ -971,6 +977,7 @@ def bench_block(args):
                         "context tokens, input spike rate 0.10, int8 weights",
             "block_tokens": M, "context_tokens": C_ctx, "timesteps": T,
             "layer_copies_rotated": args.copies, "issue": "eager" if args.eager else "hip_graph",
+            "weights": args.weights,
         },
         "step_us_percentiles": pct,
         "weight_skip_fraction": skip,
@@ -1016,7 +1023,8 @@ def bench_block_batch(args):
     L = base.layer
     T, C_ctx, M, d, H, F = base.T, base.C, base.M, L.d, L.H, L.F
     inputs = [synth.block_inputs(args.seed + 1000 * s, C_ctx, M, d, T) for s in range(nmax)]
-    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F, max_seq=nmax) for _ in range(args.copies)]
+    dms = [B.DeviceModel([L], T, C_ctx + M, d, H, F, max_seq=nmax, blocked=args.weights == "blocked")
+           for _ in range(args.copies)]
     nb = max(B.nmdlm_block_step_workspace_size(dms[0], nmax * C_ctx, B.NMDLM_NO_HEAD),
              B.nmdlm_block_step_workspace_size(dms[0], nmax * M, B.NMDLM_NO_HEAD))
     ws = B.workspace(nb)
@@ -1080,7 +1088,7 @@ def bench_block_batch(args):
                         "sequences at once: d=1024, 16 heads x 64, FFN 4096, T=4, per sequence a "
                         "block of 16 masked tokens over 512 context tokens, input spike rate "
                         "0.10, int8 weights",
-            "layer_copies_rotated": len(dms), "issue": "hip_graph",
+            "layer_copies_rotated": len(dms), "issue": "hip_graph", "weights": args.weights,
         },
         "points": points,
     }

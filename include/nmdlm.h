@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define NMDLM_ABI_VERSION 4
+#define NMDLM_ABI_VERSION 5
 
 typedef enum nmdlm_status {
   NMDLM_OK = 0,
@@ -60,7 +60,8 @@ typedef enum nmdlm_status {
  * kernel over 64-channel words, loading only active rows into registers;
  * 4 = as 3, gathering the active rows straight into LDS; 5 = as 3 with a
  * scalar gather-accumulate product in place of MFMA: per spike of a row,
- * the active weight row's columns are loaded and added).  Results do not
+ * the active weight row's columns are loaded and added; 6 = as 3 over the
+ * blocked copy of the weights, nmdlm_qbsm_blocked only).  Results do not
  * depend on it. */
 #define NMDLM_PATH_SHIFT 20u
 #define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)
@@ -128,6 +129,50 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K,
                         unsigned flags, void* ws, size_t ws_bytes, void* stream);
 
 size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
+
+/* ------------------------------------------------------------------------
+ * Blocked weights — a second layout of a weight matrix for products over
+ * many rows (prefills, steps over many sequences), where the block union is
+ * dense and the products are plain int8 contractions.
+ *
+ * Sec. IV-A (Eqs. (12)-(13)): the row-load rule reads row k of W only if
+ * input neuron k spikes in the block.  Over the blocked copy the rule is
+ * applied per 64-row word: a word with no active row is skipped, every row
+ * of an active word is read (rows that do not spike meet zero inputs, so the
+ * result is unchanged).  At dense unions the bytes read are those of the
+ * row-major path; the copy's bytes sit in MFMA operand order, so a 64-row
+ * word of a 64-column tile is four 16-byte loads per lane with no byte
+ * transposes.
+ *
+ * Layout: for word w (rows 64w..64w+63) and column tile x (columns
+ * 64x..64x+63), 4096 bytes at offset (w * ceil(N/64) + x) * 4096; within
+ * them, operand v (0..3), lane l = 16g + c (0..63), byte j (0..15) at
+ * v*1024 + l*16 + j holds W[64w + 16g + j][64x + 4c + v], zero past K or N.
+ *
+ * nmdlm_weight_blocked_bytes: size of the copy (0 for invalid sizes).
+ * nmdlm_weight_block: writes the copy Wb (device, 16-byte aligned, of
+ *   nmdlm_weight_blocked_bytes) from W (as for nmdlm_qbsm); asynchronous on
+ *   the stream.  The copy must be rebuilt whenever W changes.
+ * nmdlm_qbsm_blocked: nmdlm_qbsm (same arguments, results and errors) with
+ *   the blocked copy Wb of W also given.  With path 6 in the flags every
+ *   word is read from the copy; unforced, each wave of the product reads it
+ *   when its words' union is dense (on average at least
+ *   NMDLM_BLOCKED_MIN_ROWS of the 64 rows of its active words active, so
+ *   whole words cost at most twice the active rows' bytes), else the
+ *   row-major rows of W.  Results do not depend on which is used.
+ *   NMDLM_ERR_UNSUPPORTED when the copy would exceed 2^31 bytes.
+ * ------------------------------------------------------------------------ */
+#define NMDLM_BLOCKED_MIN_ROWS 32
+size_t nmdlm_weight_blocked_bytes(int K, int N);
+nmdlm_status nmdlm_weight_block(const int8_t* W, int K, int N, int64_t ldw,
+                                int8_t* Wb, void* stream);
+nmdlm_status nmdlm_qbsm_blocked(const uint64_t* s_in, int T, int M, int K,
+                                const int8_t* W, const int8_t* Wb, int N,
+                                int64_t ldw, const int32_t* bias,
+                                int32_t* cur_out, int32_t theta,
+                                const int32_t* theta_vec, uint64_t* s_out,
+                                nmdlm_qbsm_stats* stats, unsigned flags,
+                                void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * nmdlm_qbsm_noalloc — nmdlm_qbsm without a workspace argument, for callers
@@ -368,6 +413,14 @@ typedef struct nmdlm_layer {
   uint64_t* k_cache;     /* device [T][cache_cap][d/64]      */
   uint64_t* vt_cache;    /* device [T][cache_cap/64][d]: bit j%64 of word
                             (t, j/64, c) is value channel c of position j */
+  /* Blocked copies (nmdlm_weight_block, ldw = N) of the four weights, or
+   * NULL.  With a copy, each wave of a product reads it when its words'
+   * union is dense (at least half the rows of its active words active),
+   * else the row-major rows.  Results do not depend on it. */
+  const int8_t* w_qkv_b;
+  const int8_t* w_o_b;
+  const int8_t* w_up_b;
+  const int8_t* w_dn_b;
 } nmdlm_layer;
 
 typedef struct nmdlm_model {
@@ -383,6 +436,7 @@ typedef struct nmdlm_model {
   int max_seq;                /* sequences the caches hold (0 counts as 1):
                                  k_cache [max_seq][T][cache_cap][d/64],
                                  vt_cache [max_seq][T][cache_cap/64][d]     */
+  const int8_t* w_head_b;     /* blocked copy of w_head (ldw = V) or NULL   */
 } nmdlm_model;
 
 typedef struct nmdlm_step_io {

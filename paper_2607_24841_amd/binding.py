@@ -39,6 +39,8 @@ NMDLM_PATH_FUSED = 2 << NMDLM_PATH_SHIFT   # single kernel, in-kernel list
 NMDLM_PATH_WORDS = 3 << NMDLM_PATH_SHIFT   # single kernel over 64-channel words
 NMDLM_PATH_DMA = 4 << NMDLM_PATH_SHIFT     # as words, active rows gathered into LDS
 NMDLM_PATH_SCALAR = 5 << NMDLM_PATH_SHIFT  # as words, scalar gather-accumulate product
+NMDLM_PATH_BLOCKED = 6 << NMDLM_PATH_SHIFT  # as words, over the blocked weight copy
+NMDLM_BLOCKED_MIN_ROWS = 32
 NMDLM_QNL_S8 = 0
 NMDLM_QNL_U8 = 1
 
@@ -47,6 +49,7 @@ EXPORTS = (
     "nmdlm_bbm_attn", "nmdlm_bbm_attn_workspace_size", "nmdlm_block_step",
     "nmdlm_block_step_workspace_size", "nmdlm_workspace_clear", "nmdlm_status_string",
     "nmdlm_abi_version", "nmdlm_ternary_encode", "nmdlm_qbsm_ternary", "nmdlm_qbsm_ternary_if",
+    "nmdlm_qbsm_blocked", "nmdlm_weight_blocked_bytes", "nmdlm_weight_block",
 )
 
 
@@ -69,6 +72,8 @@ class Layer(C.Structure):
         ("theta_dn", C.c_int32), ("s_up", C.c_int32),
         ("lut_att", C.c_void_p), ("lut_act", C.c_void_p),
         ("k_cache", C.c_void_p), ("vt_cache", C.c_void_p),
+        ("w_qkv_b", C.c_void_p), ("w_o_b", C.c_void_p), ("w_up_b", C.c_void_p),
+        ("w_dn_b", C.c_void_p),
     ]
 
 
@@ -78,6 +83,7 @@ class Model(C.Structure):
         ("T", C.c_int), ("cache_cap", C.c_int64), ("max_pos", C.c_int),
         ("layers", C.POINTER(Layer)), ("emb", C.c_void_p), ("pos_ch", C.c_void_p),
         ("w_head", C.c_void_p), ("head_scale", C.c_void_p), ("max_seq", C.c_int),
+        ("w_head_b", C.c_void_p),
     ]
 
 
@@ -120,6 +126,11 @@ def load(path: str = LIB_PATH):
                                vp, vp, u, vp, sz, vp]
     lib.nmdlm_qbsm_noalloc.argtypes = [vp, C.c_int, C.c_int, C.c_int, vp, C.c_int, i64, vp, vp,
                                        i32, vp, vp, vp, u, vp]
+    lib.nmdlm_qbsm_blocked.argtypes = [vp, C.c_int, C.c_int, C.c_int, vp, vp, C.c_int, i64, vp,
+                                       vp, i32, vp, vp, vp, u, vp, sz, vp]
+    lib.nmdlm_weight_blocked_bytes.argtypes = [C.c_int, C.c_int]
+    lib.nmdlm_weight_blocked_bytes.restype = sz
+    lib.nmdlm_weight_block.argtypes = [vp, C.c_int, C.c_int, i64, vp, vp]
     lib.nmdlm_qbsm_workspace_size.argtypes = [C.c_int] * 4
     lib.nmdlm_qbsm_workspace_size.restype = sz
     lib.nmdlm_if_neuron.argtypes = [vp, C.c_int, C.c_int, C.c_int, i32, vp, vp, vp, vp, vp]
@@ -198,6 +209,35 @@ def nmdlm_qbsm(s_in, T, M, K, W, N, ldw, bias=None, cur_out=None, theta=0, theta
                         ptr(theta_vec), ptr(s_out), ptr(stats), flags, ptr(ws),
                         0 if ws is None else ws.numel() * ws.element_size(), stream_handle(stream))
     check(st, "nmdlm_qbsm")
+
+
+def nmdlm_qbsm_blocked(s_in, T, M, K, W, Wb, N, ldw, bias=None, cur_out=None, theta=0,
+                       theta_vec=None, s_out=None, stats=None, flags=0, ws=None,
+                       stream=None) -> None:
+    """nmdlm_qbsm with the blocked copy Wb of W (see nmdlm_weight_block)."""
+    st = load().nmdlm_qbsm_blocked(ptr(s_in), T, M, K, ptr(W), ptr(Wb), N, ldw, ptr(bias),
+                                   ptr(cur_out), theta, ptr(theta_vec), ptr(s_out), ptr(stats),
+                                   flags, ptr(ws),
+                                   0 if ws is None else ws.numel() * ws.element_size(),
+                                   stream_handle(stream))
+    check(st, "nmdlm_qbsm_blocked")
+
+
+def nmdlm_weight_blocked_bytes(K, N) -> int:
+    return load().nmdlm_weight_blocked_bytes(K, N)
+
+
+def nmdlm_weight_block(W, K, N, ldw, Wb, stream=None) -> None:
+    check(load().nmdlm_weight_block(ptr(W), K, N, ldw, ptr(Wb), stream_handle(stream)),
+          "nmdlm_weight_block")
+
+
+def blocked_weights(W, K, N, ldw, stream=None):
+    """A device uint8 tensor holding the blocked copy of the int8 weights W."""
+    import torch
+    Wb = torch.empty(nmdlm_weight_blocked_bytes(K, N), dtype=torch.int8, device=W.device)
+    nmdlm_weight_block(W, K, N, ldw, Wb, stream)
+    return Wb
 
 
 def nmdlm_qbsm_noalloc(s_in, T, M, K, W, N, ldw, bias=None, cur_out=None, theta=0,
@@ -293,12 +333,20 @@ class DeviceLayer:
     max_seq sequences: k_seq [max_seq][T][cap][d/64], vt_seq
     [max_seq][T][cap/64][d]; k_cache / vt_cache are sequence 0's."""
 
-    def __init__(self, L, T: int, cache_cap: int, device="cuda", max_seq: int = 1):
+    def __init__(self, L, T: int, cache_cap: int, device="cuda", max_seq: int = 1,
+                 blocked: bool = False):
         d = L.d
         self.w_qkv = _dev(L.W_qkv, device)
         self.w_o = _dev(L.W_o, device)
         self.w_up = _dev(L.W_up, device)
         self.w_dn = _dev(L.W_dn, device)
+        # blocked copies (nmdlm_weight_block) for products over dense unions
+        self.blk = {}
+        if blocked:
+            for name in ("w_qkv", "w_o", "w_up", "w_dn"):
+                w = getattr(self, name)
+                K, N = w.shape
+                self.blk[name] = blocked_weights(w, K, N, N)
         self.lut_att = _dev(L.lut_att, device)
         self.lut_act = _dev(L.lut_act, device)
         self.k_seq = torch.zeros((max_seq, T, cache_cap, d // 64), dtype=torch.int64, device=device)
@@ -307,32 +355,40 @@ class DeviceLayer:
         th = L.theta
         self.c = Layer(ptr(self.w_qkv), ptr(self.w_o), ptr(self.w_up), ptr(self.w_dn),
                        th["q"], th["k"], th["v"], th["a"], th["o"], th["up"], th["dn"], L.s_up,
-                       ptr(self.lut_att), ptr(self.lut_act), ptr(self.k_cache), ptr(self.vt_cache))
+                       ptr(self.lut_att), ptr(self.lut_act), ptr(self.k_cache), ptr(self.vt_cache),
+                       *[ptr(self.blk.get(n)) for n in ("w_qkv", "w_o", "w_up", "w_dn")])
 
 
 class DeviceModel:
     """A stack of layers (and optionally token tables and a head) on the GPU."""
 
     def __init__(self, layers, T: int, cache_cap: int, d: int, H: int, F: int, V: int = 1,
-                 emb=None, pos_ch=None, W_head=None, scale=None, device="cuda", max_seq: int = 1):
+                 emb=None, pos_ch=None, W_head=None, scale=None, device="cuda", max_seq: int = 1,
+                 blocked: bool = False):
+        """blocked: also hold blocked copies of every weight (twice the weight
+        bytes), which products over dense unions read."""
         cache_cap = (cache_cap + 63) // 64 * 64
         self.T, self.d, self.H, self.F, self.V, self.cache_cap = T, d, H, F, V, cache_cap
         self.max_seq = max(1, int(max_seq))
-        self.layers = [DeviceLayer(L, T, cache_cap, device, self.max_seq) for L in layers]
+        self.layers = [DeviceLayer(L, T, cache_cap, device, self.max_seq, blocked) for L in layers]
         self._c_layers = (Layer * max(1, len(self.layers)))(*[l.c for l in self.layers])
         self.emb = _dev(emb, device) if emb is not None else None
         self.pos_ch = _dev(pos_ch.astype(np.int32), device) if pos_ch is not None else None
         self.w_head = _dev(W_head, device) if W_head is not None else None
         self.scale = _dev(scale.astype(np.float32), device) if scale is not None else None
         self.max_pos = 0 if pos_ch is None else int(pos_ch.shape[0])
+        self.w_head_b = None
+        if blocked and self.w_head is not None:
+            self.w_head_b = blocked_weights(self.w_head, d, V, V)
         self.c = Model(len(self.layers), d, H, F, V, T, cache_cap, self.max_pos, self._c_layers,
                        ptr(self.emb), ptr(self.pos_ch), ptr(self.w_head), ptr(self.scale),
-                       self.max_seq)
+                       self.max_seq, ptr(self.w_head_b))
 
     @classmethod
-    def from_mdlm(cls, m, cache_cap: int, device="cuda", max_seq: int = 1):
+    def from_mdlm(cls, m, cache_cap: int, device="cuda", max_seq: int = 1, blocked: bool = False):
         return cls(m.layers, m.T, cache_cap, m.d, m.H, m.F, m.V, emb=m.emb, pos_ch=m.pos_ch,
-                   W_head=m.W_head, scale=m.scale, device=device, max_seq=max_seq)
+                   W_head=m.W_head, scale=m.scale, device=device, max_seq=max_seq,
+                   blocked=blocked)
 
     def reset_caches(self):
         for l in self.layers:
@@ -357,7 +413,8 @@ class ModelView:
         p = parent.c
         self.c = Model(len(self.layers), p.d, p.H, p.F, p.V, p.T, p.cache_cap, p.max_pos,
                        self._c_layers, p.emb, p.pos_ch, p.w_head if head else None,
-                       p.head_scale if head else None, p.max_seq)
+                       p.head_scale if head else None, p.max_seq,
+                       p.w_head_b if head else None)
 
 
 def step_io(M, C_, pos0=0, flags=0, x_in=None, tokens=None, masked=None, k_unmask=0, y_out=None,

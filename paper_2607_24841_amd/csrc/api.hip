@@ -24,6 +24,12 @@ size_t qbsm_ws(int T, int M, int K, int N) {
   return align_up(cv.off, 256);
 }
 
+// an optional blocked copy: NULL, or 16-byte aligned with a size below 2^31
+bool blocked_ok(const int8_t* Wb, int K, int N) {
+  return !Wb || (((reinterpret_cast<uintptr_t>(Wb) & 15) == 0) &&
+                 weight_blocked_bytes(K, N) < ((size_t)1 << 31));
+}
+
 bool weights_ok(const int8_t* W, int K, int N, int64_t ldw) {
   if (!W || !aligned(W, 16)) return false;
   if (ldw < N || (ldw % 16) != 0) return false;
@@ -53,10 +59,15 @@ size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N) {
   return qbsm_ws(T, M, K, N);
 }
 
-nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t* W, int N,
-                        int64_t ldw, const int32_t* bias, int32_t* cur_out, int32_t theta,
-                        const int32_t* theta_vec, uint64_t* s_out, nmdlm_qbsm_stats* stats,
-                        unsigned flags, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+nmdlm_status qbsm_entry(const uint64_t* s_in, int T, int M, int K, const int8_t* W,
+                        const int8_t* Wb, int N, int64_t ldw, const int32_t* bias,
+                        int32_t* cur_out, int32_t theta, const int32_t* theta_vec,
+                        uint64_t* s_out, nmdlm_qbsm_stats* stats, unsigned flags, void* ws,
+                        size_t ws_bytes, void* stream) {
   if (!s_in || T < 1 || M < 1 || K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
   if (T > NMDLM_MAX_T || K > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
   if (!weights_ok(W, K, N, ldw)) return NMDLM_ERR_INVALID_ARG;
@@ -110,12 +121,50 @@ nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t*
   c.thr_den = 1;
   c.s_neg_out = nullptr;
   c.v_out = nullptr;
+  c.Wb = Wb;
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
   QbsmScratch scr;
   carve_qbsm_scratch(cv, qbsm_limits_single(T, M, K, N), &scr);
   if (!cv.ok) return NMDLM_ERR_WORKSPACE;
   return launch_qbsm(c, scr, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+nmdlm_status nmdlm_qbsm(const uint64_t* s_in, int T, int M, int K, const int8_t* W, int N,
+                        int64_t ldw, const int32_t* bias, int32_t* cur_out, int32_t theta,
+                        const int32_t* theta_vec, uint64_t* s_out, nmdlm_qbsm_stats* stats,
+                        unsigned flags, void* ws, size_t ws_bytes, void* stream) {
+  return qbsm_entry(s_in, T, M, K, W, nullptr, N, ldw, bias, cur_out, theta, theta_vec, s_out,
+                    stats, flags, ws, ws_bytes, stream);
+}
+
+size_t nmdlm_weight_blocked_bytes(int K, int N) {
+  if (K < 1 || K > NMDLM_MAX_K || N < 1) return 0;
+  return weight_blocked_bytes(K, N);
+}
+
+nmdlm_status nmdlm_weight_block(const int8_t* W, int K, int N, int64_t ldw, int8_t* Wb,
+                                void* stream) {
+  if (K < 1 || N < 1) return NMDLM_ERR_INVALID_ARG;
+  if (K > NMDLM_MAX_K) return NMDLM_ERR_UNSUPPORTED;
+  if (!weights_ok(W, K, N, ldw) || !Wb || !aligned(Wb, 16)) return NMDLM_ERR_INVALID_ARG;
+  if (weight_blocked_bytes(K, N) >= ((size_t)1 << 31)) return NMDLM_ERR_UNSUPPORTED;
+  return launch_weight_block(W, K, N, ldw, Wb, static_cast<hipStream_t>(stream));
+}
+
+nmdlm_status nmdlm_qbsm_blocked(const uint64_t* s_in, int T, int M, int K, const int8_t* W,
+                                const int8_t* Wb, int N, int64_t ldw, const int32_t* bias,
+                                int32_t* cur_out, int32_t theta, const int32_t* theta_vec,
+                                uint64_t* s_out, nmdlm_qbsm_stats* stats, unsigned flags, void* ws,
+                                size_t ws_bytes, void* stream) {
+  if (!Wb || !aligned(Wb, 16)) return NMDLM_ERR_INVALID_ARG;
+  if (weight_blocked_bytes(K, N) >= ((size_t)1 << 31)) return NMDLM_ERR_UNSUPPORTED;
+  return qbsm_entry(s_in, T, M, K, W, Wb, N, ldw, bias, cur_out, theta, theta_vec, s_out, stats,
+                    flags, ws, ws_bytes, stream);
 }
 
 nmdlm_status nmdlm_ternary_encode(const int32_t* a, int M, int D, int K, int T, uint64_t* s_pos,
@@ -182,6 +231,7 @@ nmdlm_status ternary_product(const uint64_t* s_pos, const uint64_t* s_neg, int T
   c.thr_den = thr_den;
   c.s_neg_out = out_neg;
   c.v_out = v_out;
+  c.Wb = nullptr;
 
   Carver cv{static_cast<char*>(ws), 0, ws_bytes, true};
   QbsmScratch scr;
@@ -323,6 +373,9 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
         !weights_ok(L.w_dn, md->F, md->d, md->d))
       return NMDLM_ERR_INVALID_ARG;
     if (!L.lut_att || !L.lut_act || !L.k_cache || !L.vt_cache) return NMDLM_ERR_INVALID_ARG;
+    if (!blocked_ok(L.w_qkv_b, md->d, 3 * md->d) || !blocked_ok(L.w_o_b, md->d, md->d) ||
+        !blocked_ok(L.w_up_b, md->d, md->F) || !blocked_ok(L.w_dn_b, md->F, md->d))
+      return NMDLM_ERR_INVALID_ARG;
     if (L.theta_q <= 0 || L.theta_k <= 0 || L.theta_v <= 0 || L.theta_a <= 0 || L.theta_o <= 0 ||
         L.theta_up <= 0 || L.theta_dn <= 0)
       return NMDLM_ERR_INVALID_ARG;
@@ -335,7 +388,8 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   }
   const bool head = !(io->flags & NMDLM_NO_HEAD);
   if (head) {
-    if (!weights_ok(md->w_head, md->d, md->V, md->V) || !md->head_scale)
+    if (!weights_ok(md->w_head, md->d, md->V, md->V) || !md->head_scale ||
+        !blocked_ok(md->w_head_b, md->d, md->V))
       return NMDLM_ERR_INVALID_ARG;
     if (!io->tokens || !io->masked || io->k_unmask < 0) return NMDLM_ERR_INVALID_ARG;
     if (io->M > NMDLM_MAX_HEAD_M) return NMDLM_ERR_UNSUPPORTED;

@@ -138,6 +138,10 @@ struct QbsmArgs {
   int64_t* v_out;
   // word product: 0 = MFMA, 1 = scalar gather-accumulate
   int accum;
+  // blocked weights (operand order, see launch_weight_block) or null, and
+  // the active rows per active word from which a wave reads them
+  const int8_t* Wb;
+  int blk_min;
 };
 
 // Scratch used by one product (carved from a workspace).
@@ -194,7 +198,19 @@ struct QbsmCall {
   int64_t thr_den;
   uint64_t* s_neg_out;
   int64_t* v_out;
+  const int8_t* Wb;       // the weights in blocked operand order, or null
 };
+
+// Blocked weight layout: for word w (rows 64w..64w+63) and column tile x
+// (columns 64x..64x+63), 4096 bytes at (w * ceil(N/64) + x) * 4096; within
+// them operand v (v = 0..3), lane l = 16g + c, byte j holds
+// W[64w + 16g + j][64x + 4c + v] (zero past K or N): the B operand of
+// v_mfma_i32_16x16x64_i8 for the tile's columns 4c + v, one 16-byte load.
+inline size_t weight_blocked_bytes(int K, int N) {
+  return (size_t)((K + 63) / 64) * (size_t)((N + 63) / 64) * 4096;
+}
+nmdlm_status launch_weight_block(const int8_t* W, int K, int N, int64_t ldw, int8_t* Wb,
+                                 hipStream_t st);
 
 // Workspace layout helpers -------------------------------------------------
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

@@ -216,7 +216,10 @@ constexpr size_t kLdsBudget = 65536;    // LDS per workgroup used by the product
 constexpr int kMaxEpiTokens = 128;      // row-block tokens whose residual words are staged
 constexpr int kUpLoads = 2;             // partial-union loads per thread staged in registers
 constexpr int kRowLoads = 2;            // spike-row words per thread staged in registers
-constexpr int kStageBatch = 8;          // further spike-row words per thread per staging batch
+constexpr int kStageBatch = 8;
+// a wave reads the blocked weight copy when its active words have at least
+// this many active rows of 64 on average (at most twice the row bytes)
+constexpr int kBlockedMinRows = NMDLM_BLOCKED_MIN_ROWS;          // further spike-row words per thread per staging batch
 static_assert(kMaxEpiTokens >= 8 * 16, "every tile's residual words are staged (RT <= 8)");
 
 __device__ __forceinline__ uint32_t expand4(uint32_t nib) {
@@ -797,7 +800,12 @@ __device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds
 // slot (left stale) is multiplied by zero.  Across row blocks the rows read
 // are the block union; repeated reads hit the cache.  Words with no active
 // row are skipped.
-template <int RT, int NW, bool TERN = false>
+// BLK: a blocked copy of the weights (a.Wb, operand order) is also given: a
+// word is then four 16-byte loads per lane, already B operands, with every
+// row of an active word read (rows outside the local union meet zero spikes)
+// and a word with no active row skipped.  Each wave takes the copy or the
+// row-major rows by the density of its words' union (a.blk_min).
+template <int RT, int NW, bool TERN = false, bool BLK = false>
 __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
@@ -1008,7 +1016,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   // next word's loads can be in flight while the current one is multiplied.
   const uint32_t first_off = (uint32_t)first * ldw + colb;
   const int stride = NW;
-  auto load_word = [&](int w, uint32_t (&xg)[16]) {
+  auto load_rows = [&](int w, uint32_t (&xg)[16]) {
     const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
     const uint32_t m16 = (uint32_t)(u >> (16 * g)) & 0xFFFFu;
     const uint32_t wbase = (uint32_t)w * 64u * ldw + lane_base;
@@ -1018,11 +1026,22 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
       xg[s2] = *reinterpret_cast<const uint32_t*>(Wb + off);
     }
   };
-  auto mul_word = [&](int w, const uint32_t (&xg)[16]) {
+  // blocked copy: a word of the tile is four 16-byte operand loads; an
+  // inactive word (or one past the range) re-reads the first active word
+  const int gxb = (a.N + 63) >> 6;
+  const char* Wbb = reinterpret_cast<const char*>(a.Wb) + (size_t)x * 4096 + (size_t)lane * 16;
+  auto load_blocked = [&](int w, uint32_t (&xg)[16]) {
     const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
-    if (u == 0ull) return;  // wave-uniform
-    v4i b[4];
-    b_operands(xg, b);
+    const int ws = u ? w : (first >> 6);
+    const char* p = Wbb + (size_t)ws * gxb * 4096;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const v4i q = *reinterpret_cast<const v4i*>(p + v * 1024);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) xg[4 * v + e] = (uint32_t)q[e];
+    }
+  };
+  auto mul_b = [&](int w, const v4i (&b)[4]) {
 #pragma unroll
     for (int q = 0; q < RT; ++q) {
       const int sidx = (q * 16 + c) * lds_row + 2 * w + (g >> 1);
@@ -1035,22 +1054,61 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
         acc[q][v] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, b[v], acc[q][v], 0, 0, 0);
     }
   };
-  // MFMA over the words, or (requested) the scalar gather-accumulate product
-  const bool scalar = !TERN && a.accum == 1 && !a.dense;  // workgroup-uniform
-  int jw = w0 + wave;
-  if (!scalar && first != 0x7fffffff && jw < w1) {  // wave-uniform
+  auto mul_rows = [&](int w, const uint32_t (&xg)[16]) {
+    const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
+    if (u == 0ull) return;  // wave-uniform
+    v4i b[4];
+    b_operands(xg, b);
+    mul_b(w, b);
+  };
+  auto mul_blocked = [&](int w, const uint32_t (&xg)[16]) {
+    const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
+    if (u == 0ull) return;  // wave-uniform
+    v4i b[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      b[v] = v4i{(int)xg[4 * v], (int)xg[4 * v + 1], (int)xg[4 * v + 2], (int)xg[4 * v + 3]};
+    mul_b(w, b);
+  };
+  // the words of this wave, the next one's loads in flight while the
+  // current one is multiplied
+  auto loop = [&](auto&& load, auto&& mul) {
+    int jw = w0 + wave;
     uint32_t xa[16], xb[16];
-    load_word(jw, xa);
+    load(jw, xa);
     while (true) {
-      load_word(jw + stride, xb);
-      mul_word(jw, xa);
+      load(jw + stride, xb);
+      mul(jw, xa);
       jw += stride;
       if (jw >= w1) break;
-      load_word(jw + stride, xa);
-      mul_word(jw, xb);
+      load(jw + stride, xa);
+      mul(jw, xb);
       jw += stride;
       if (jw >= w1) break;
     }
+  };
+  // MFMA over the words, or (requested) the scalar gather-accumulate product
+  const bool scalar = !TERN && !BLK && a.accum == 1 && !a.dense;  // workgroup-uniform
+  if (!scalar && first != 0x7fffffff && w0 + wave < w1) {  // wave-uniform
+    // with a blocked copy, each wave reads it when at least a.blk_min of
+    // the 64 rows of its active words are active on average (whole words
+    // then cost at most 64 / blk_min times the rows), else the rows
+    bool blocked = false;
+    if constexpr (BLK) {
+      int rows = 0, words = 0;
+      for (int w = w0 + wave + lane * stride; w < w1; w += 64 * stride) {
+        const unsigned long long u = sLU[w];
+        rows += __popcll(u);
+        words += u != 0ull;
+      }
+      for (int o = kWave / 2; o > 0; o >>= 1) {
+        rows += __shfl_xor(rows, o);
+        words += __shfl_xor(words, o);
+      }
+      blocked = rows >= words * a.blk_min;
+    }
+    if (BLK && blocked) loop(load_blocked, mul_blocked);
+    else loop(load_rows, mul_rows);
   }
   if (scalar) scalar_accumulate<ROWS, NT>(a, sS, lds_row, sTile, tid, x, y, w0, w1);
 
@@ -1556,6 +1614,16 @@ static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
 template <int RT, int NW>
 static nmdlm_status launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
                                  hipEvent_t e0, hipEvent_t e1) {
+  // blocked weights: the variant loading operand-order words
+  if (a.Wb) {
+    if (dyn > 65536 &&
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_words<RT, NW, false, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+      return NMDLM_ERR_HIP;
+    hipExtLaunchKernelGGL((k_qbsm_words<RT, NW, false, true>), grid, dim3(NW * 64), (uint32_t)dyn,
+                          st, e0, e1, 0, a);
+    return NMDLM_OK;
+  }
   // ternary input (-1 spikes given): the variant staging both spike planes
   if (a.Sn) {
     if (dyn > 65536 &&
@@ -1598,6 +1666,44 @@ static void launch_list(const dim3& grid, const QbsmArgs& a, hipStream_t st, hip
   hipExtLaunchKernelGGL((k_qbsm_list<RT, NW>), grid, dim3(NW * 64), 0u, st, e0, e1, 0, a);
 }
 
+// Blocked weight layout (see weight_blocked_bytes): thread i writes the
+// 16-byte operand lane i % 64 of operand (i / 64) % 4 of block i / 256, each
+// byte read from the row-major weights (zero past K or N).
+__global__ __launch_bounds__(256) void k_weight_block(const int8_t* __restrict__ W, int K, int N,
+                                                      int64_t ldw, int8_t* __restrict__ Wb,
+                                                      long long n_lanes) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_lanes) return;
+  const int gx = (N + 63) / 64;
+  const int lane = (int)(i & 63), v = (int)((i >> 6) & 3);
+  const long long blk = i >> 8;
+  const int x = (int)(blk % gx), w = (int)(blk / gx);
+  const int g = lane >> 4, c = lane & 15;
+  const int col = x * 64 + 4 * c + v;
+  uint32_t q[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint32_t d = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int row = w * 64 + 16 * g + 4 * e + b;
+      const uint32_t byte = (row < K && col < N) ? (uint8_t)W[(int64_t)row * ldw + col] : 0u;
+      d |= byte << (8 * b);
+    }
+    q[e] = d;
+  }
+  *reinterpret_cast<uint4*>(Wb + i * 16) = uint4{q[0], q[1], q[2], q[3]};
+}
+
+nmdlm_status launch_weight_block(const int8_t* W, int K, int N, int64_t ldw, int8_t* Wb,
+                                 hipStream_t st) {
+  const long long n_lanes = (long long)(weight_blocked_bytes(K, N) / 16);
+  if (n_lanes == 0) return NMDLM_OK;
+  hipLaunchKernelGGL(k_weight_block, dim3((unsigned)((n_lanes + 255) / 256)), dim3(256), 0, st, W, K,
+                     N, ldw, Wb, n_lanes);
+  return hip_status();
+}
+
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
 static size_t words_lds(int RT, int NW, int Kw, bool tern = false) {
   return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
@@ -1624,6 +1730,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   // product path: 1 = prep pass + list kernel, 2 = single kernel with a
   // compacted list, 3 = word-granular single kernel, 0 = automatic
   int path = (int)((c.flags >> NMDLM_PATH_SHIFT) & 0x7u);
+  const bool path_auto = path == 0;
   const int rt_full = pick_rt(R);
   int RT = (int)((c.flags >> NMDLM_ROWTILE_SHIFT) & 0xFu);
   const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
@@ -1698,11 +1805,28 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     accum = 1;
     path = 3;
   }
+  // 6: the word product over blocked weights (requested: every wave reads
+  // the copy; unrequested, with a copy: each wave chooses by its union)
+  bool blk = false;
+  int blk_min = kBlockedMinRows;
+  if (path == 6) {
+    if (!c.Wb || tern) return NMDLM_ERR_UNSUPPORTED;
+    blk = true;
+    blk_min = 0;
+    path = 3;
+    while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
+    if (words_lds(RT, 4, Kw) > kWordsLdsBudget) return NMDLM_ERR_UNSUPPORTED;
+  } else if (path_auto && path == 3 && c.Wb && !tern) {
+    blk = true;
+  }
   if (path == 3 && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
   const int Mb = (16 * RT) / c.T;
+  // the tile heights lowered for LDS above keep a channel-major segment's
+  // row blocks within one sequence, or the call is refused
+  if (has_tr && c.seq_len > 0 && c.seq_len % Mb != 0) return NMDLM_ERR_UNSUPPORTED;
   const int gy = (c.M + Mb - 1) / Mb;
   const int tiles = gx * gy;
   if ((size_t)tiles > scr.n_counters) return NMDLM_ERR_WORKSPACE;
@@ -1822,6 +1946,8 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.s_neg_out = c.s_neg_out;
   a.v_out = c.v_out;
   a.accum = accum;
+  a.Wb = blk ? c.Wb : nullptr;
+  a.blk_min = blk_min;
 
   const dim3 grid(gx, gy, P);
   hipEvent_t e0 = c.ev_begin, e1 = c.ev_end;

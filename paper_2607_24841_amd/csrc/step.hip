@@ -364,6 +364,7 @@ static QbsmCall base_call(const uint64_t* s_in, int T, int M, int K, const int8_
   c.thr_den = 1;
   c.s_neg_out = nullptr;
   c.v_out = nullptr;
+  c.Wb = nullptr;
   return c;
 }
 
@@ -432,6 +433,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     }
     qkv.u_in = uX;
     qkv.u_nparts = uX_parts;
+    qkv.Wb = ly.w_qkv_b;
     attach_events(qkv, io, 4 * l + 0);
     if ((rc = launch_qbsm(qkv, b.qs, st)) != NMDLM_OK) return rc;
 
@@ -455,6 +457,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     o.u_in = b.uA;
     o.u_nparts = M;
     o.u_out = b.uX1;
+    o.Wb = ly.w_o_b;
     attach_events(o, io, 4 * l + 1);
     if ((rc = launch_qbsm(o, b.qs, st, &gy)) != NMDLM_OK) return rc;
     const int uX1_parts = gy;
@@ -467,6 +470,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     up.u_in = b.uX1;
     up.u_nparts = uX1_parts;
     up.u_out = b.uH;
+    up.Wb = ly.w_up_b;
     attach_events(up, io, 4 * l + 2);
     if ((rc = launch_qbsm(up, b.qs, st, &gy)) != NMDLM_OK) return rc;
     const int uH_parts = gy;
@@ -481,6 +485,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
     dn.u_in = b.uH;
     dn.u_nparts = uH_parts;
     dn.u_out = b.uY[l & 1];
+    dn.Wb = ly.w_dn_b;
     attach_events(dn, io, 4 * l + 3);
     if ((rc = launch_qbsm(dn, b.qs, st, &gy)) != NMDLM_OK) return rc;
     X = Yl;
@@ -504,6 +509,7 @@ nmdlm_status block_step_impl(const nmdlm_model* md, nmdlm_step_io* io, void* ws,
   hc.scale = md->head_scale;
   hc.u_in = uX;
   hc.u_nparts = uX_parts;
+  hc.Wb = md->w_head_b;
   attach_events(hc, io, 4 * md->n_layers);
   if ((rc = launch_qbsm(hc, b.qs, st)) != NMDLM_OK) return rc;
   const int nch = (md->V + kConfChunk - 1) / kConfChunk;

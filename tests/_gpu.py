@@ -23,9 +23,10 @@ def pad_weights(W: np.ndarray) -> tuple[np.ndarray, int]:
     return Wp, ldw
 
 
-def run_qbsm(S, W, bias=None, theta=None, theta_vec=None, flags=0, want_cur=True):
-    """Run nmdlm_qbsm; returns (currents int64 or None, spikes bool or None,
-    stats dict, raw spike words)."""
+def run_qbsm(S, W, bias=None, theta=None, theta_vec=None, flags=0, want_cur=True, blocked=False):
+    """Run nmdlm_qbsm (nmdlm_qbsm_blocked with a blocked copy of the weights
+    when blocked); returns (currents int64 or None, spikes bool or None, stats
+    dict, raw spike words)."""
     torch, B = need_gpu()
     T, M, K = S.shape
     N = W.shape[1]
@@ -42,8 +43,14 @@ def run_qbsm(S, W, bias=None, theta=None, theta_vec=None, flags=0, want_cur=True
         spk = torch.full((T, M, Nw), -1, dtype=torch.int64, device=dev)
     stats = torch.zeros(4, dtype=torch.int64, device=dev)
     ws = B.workspace(B.nmdlm_qbsm_workspace_size(T, M, K, N), dev)
-    B.nmdlm_qbsm(s_in, T, M, K, Wd, N, ldw, bias=bd, cur_out=cur, theta=int(theta or 0),
-                 theta_vec=tv, s_out=spk, stats=stats, flags=flags, ws=ws)
+    if blocked:
+        Wb = B.blocked_weights(Wd, K, N, ldw)
+        B.nmdlm_qbsm_blocked(s_in, T, M, K, Wd, Wb, N, ldw, bias=bd, cur_out=cur,
+                             theta=int(theta or 0), theta_vec=tv, s_out=spk, stats=stats,
+                             flags=flags, ws=ws)
+    else:
+        B.nmdlm_qbsm(s_in, T, M, K, Wd, N, ldw, bias=bd, cur_out=cur, theta=int(theta or 0),
+                     theta_vec=tv, s_out=spk, stats=stats, flags=flags, ws=ws)
     torch.cuda.synchronize()
     st = stats.cpu().numpy()
     out_cur = cur.cpu().numpy().astype(np.int64) if cur is not None else None

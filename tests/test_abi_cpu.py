@@ -31,7 +31,7 @@ def test_exports_every_declared_function(lib):
     assert set(B.EXPORTS) <= set(names)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.nmdlm_abi_version() == 4
+    assert lib.nmdlm_abi_version() == 5
     assert lib.nmdlm_status_string(0) == b"ok"
     assert lib.nmdlm_status_string(3).startswith(b"workspace")
 
@@ -140,6 +140,14 @@ def test_block_step_argument_errors(lib):
     big = B.step_io(4097, 0, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
     nb = lib.nmdlm_block_step_workspace_size(C.byref(mh), 4097, 0)
     assert nb > 0 and call(mh, big, nb=nb) == B.NMDLM_ERR_UNSUPPORTED
+    # blocked weight copies must be 16-byte aligned
+    Lb = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 200, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE,
+                 FAKE, FAKE, FAKE + 8, None, None)
+    mb = B.Model(1, 1024, 16, 4096, 32000, 4, 576, 0, (B.Layer * 1)(Lb), None, None, None, None)
+    assert call(mb, io) == B.NMDLM_ERR_INVALID_ARG
+    mhb = B.Model(1, 1024, 16, 4096, 32000, 4, 8192, 0, layers, None, None, FAKE, FAKE, 1, FAKE + 4)
+    head16 = B.step_io(16, 512, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
+    assert call(mhb, head16) == B.NMDLM_ERR_INVALID_ARG
 
 
 def test_batched_step_argument_errors(lib):
@@ -207,8 +215,31 @@ def test_binding_constants_match_the_header():
     for name in ("NMDLM_FORCE_DENSE", "NMDLM_NO_HEAD", "NMDLM_ATTN_FUSED", "NMDLM_SPLIT_SHIFT",
                  "NMDLM_ROWTILE_SHIFT", "NMDLM_MAX_HEAD_M", "NMDLM_MAX_T", "NMDLM_MAX_K",
                  "NMDLM_MAX_KEYS", "NMDLM_STATUS_TOKEN_CLAMPED", "NMDLM_MAX_THR_DEN",
-                 "NMDLM_NOALLOC_SCRATCH_BYTES"):
+                 "NMDLM_NOALLOC_SCRATCH_BYTES", "NMDLM_BLOCKED_MIN_ROWS"):
         m = re.search(r"#define\s+%s\s+([0-9xXa-fA-F]+)u?" % name, text)
         assert m, name
         if hasattr(B, name):
             assert getattr(B, name) == int(m.group(1).rstrip("u"), 0), name
+
+
+def test_blocked_weight_sizes_and_errors(lib):
+    # 4096 bytes per (64-row word, 64-column tile), ragged K and N rounded up
+    assert lib.nmdlm_weight_blocked_bytes(64, 64) == 4096
+    assert lib.nmdlm_weight_blocked_bytes(700, 300) == 11 * 5 * 4096
+    assert lib.nmdlm_weight_blocked_bytes(0, 64) == 0
+    assert lib.nmdlm_weight_blocked_bytes(70000, 64) == 0
+    # validation before any HIP call
+    assert lib.nmdlm_weight_block(FAKE, 0, 64, 64, FAKE, None) == B.NMDLM_ERR_INVALID_ARG
+    assert lib.nmdlm_weight_block(FAKE, 64, 64, 64, None, None) == B.NMDLM_ERR_INVALID_ARG
+    assert lib.nmdlm_weight_block(FAKE, 64, 64, 64, FAKE + 8, None) == B.NMDLM_ERR_INVALID_ARG
+    assert lib.nmdlm_weight_block(FAKE, 64, 64, 60, FAKE, None) == B.NMDLM_ERR_INVALID_ARG
+    assert lib.nmdlm_weight_block(FAKE, 70000, 64, 64, FAKE, None) == B.NMDLM_ERR_UNSUPPORTED
+
+    def blk(Wb=FAKE, K=512, N=512, ldw=512, ws_bytes=1 << 30):
+        return lib.nmdlm_qbsm_blocked(FAKE, 4, 8, K, FAKE, Wb, N, ldw, None, FAKE, 256, None, None,
+                                      None, 0, FAKE, ws_bytes, None)
+    assert blk(Wb=None) == B.NMDLM_ERR_INVALID_ARG
+    assert blk(Wb=FAKE + 4) == B.NMDLM_ERR_INVALID_ARG
+    assert blk(K=65536, N=40000, ldw=40000) == B.NMDLM_ERR_UNSUPPORTED  # copy beyond 2^31 bytes
+    assert blk(ldw=500) == B.NMDLM_ERR_INVALID_ARG
+    assert blk(ws_bytes=16) == B.NMDLM_ERR_WORKSPACE

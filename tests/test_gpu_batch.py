@@ -50,10 +50,23 @@ def _cases(n, C, M, d, H, F, seed, T=4):
 ], ids=["straddle", "bytes", "rt2-ragged", "dense", "full-4seq", "16seq", "T8", "T3", "dh128",
         "attn-fused-flag", "128seq"])
 def test_batched_block_step_matches_independent_sequences(n, C, M, d, H, F, flags, T):
+    _batched_matches_independent(n, C, M, d, H, F, flags, T)
+
+
+@pytest.mark.parametrize("n,C,M,d,H,F,flags,T", [
+    (4, 512, 16, 1024, 16, 4096, 0, 4),     # full-size layer, four sequences
+    (128, 40, 16, 128, 2, 256, 0, 4),       # 128 sequences: 8192 rows per product
+    (3, 62, 6, 128, 2, 256, 6 << 20, 8),    # every word from the copies, T = 8
+], ids=["full-4seq", "128seq", "T8-forced"])
+def test_batched_step_with_blocked_weights(n, C, M, d, H, F, flags, T):
+    _batched_matches_independent(n, C, M, d, H, F, flags, T, blocked=True)
+
+
+def _batched_matches_independent(n, C, M, d, H, F, flags, T, blocked=False):
     torch, B = need_gpu()
     cases = _cases(n, C, M, d, H, F, seed=71, T=T)
     L, T = cases[0].layer, cases[0].T
-    dm = B.DeviceModel([L], T, C + M, d, H, F, max_seq=n)
+    dm = B.DeviceModel([L], T, C + M, d, H, F, max_seq=n, blocked=blocked)
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, n * C, B.NMDLM_NO_HEAD),
                          B.nmdlm_block_step_workspace_size(dm, n * M, B.NMDLM_NO_HEAD)))
     # batched prefill of the n contexts, then the batched block step

@@ -23,11 +23,11 @@ def _caches_to_host(dm, T, d, J):
     return ks, vs
 
 
-def _run_block_case(case, flags=0):
+def _run_block_case(case, flags=0, blocked=False):
     torch, B = need_gpu()
     L = case.layer
     T, C, M, d = case.T, case.C, case.M, L.d
-    dm = B.DeviceModel([L], T, C + M, d, L.H, L.F)
+    dm = B.DeviceModel([L], T, C + M, d, L.H, L.F, blocked=blocked)
     nb = max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
              B.nmdlm_block_step_workspace_size(dm, M, B.NMDLM_NO_HEAD))
     ws = B.workspace(nb)
@@ -50,8 +50,8 @@ def _oracle_block_case(case):
     return tr, kc[0], vc[0]
 
 
-def _check_block(case, flags=0):
-    dm, Y, stats = _run_block_case(case, flags)
+def _check_block(case, flags=0, blocked=False):
+    dm, Y, stats = _run_block_case(case, flags, blocked)
     tr, kref, vref = _oracle_block_case(case)
     assert_same(Y, tr.Y, 'Y')
     ks, vs = _caches_to_host(dm, case.T, case.layer.d, case.C + case.M)
@@ -128,6 +128,18 @@ def test_block_step_graph_replays_match_eager():
 def test_block_forced_paths(flags):
     need_gpu()
     _check_block(synth.block_case(), flags=flags)
+
+
+@pytest.mark.parametrize("flags", [0, 6 << 20, (6 << 20) | (1 << 16), (6 << 20) | (2 << 8), 0x1,
+                                   3 << 20],
+                         ids=["auto", "blocked", "blocked-RT1", "blocked-P2", "dense", "rows"])
+def test_block_with_blocked_weights(flags):
+    # the layer also holds blocked weight copies: waves choose by their
+    # union (auto), every word from the copies (path 6), or the rows only
+    need_gpu()
+    _check_block(synth.block_case(), flags=flags, blocked=True)
+    _check_block(synth.block_case(seed=23, C=70, M=37, d=192, H=3, F=320), flags=flags,
+                 blocked=True)
 
 
 # ----------------------------------------------------------------------------

@@ -105,14 +105,16 @@ def _tokens_after(chosen, pred, tokens0, masked0):
     return tok.tolist(), msk.tolist()
 
 
-@pytest.mark.parametrize("flags", [0, 0x4, 4 << 20], ids=["default", "attn-fused", "dma"])
-def test_mdlm12_step_matches_stored_oracle(flags):
+@pytest.mark.parametrize("flags,blocked", [(0, False), (0x4, False), (4 << 20, False), (0, True),
+                                           (6 << 20, True)],
+                         ids=["default", "attn-fused", "dma", "blocked-copies", "blocked-forced"])
+def test_mdlm12_step_matches_stored_oracle(flags, blocked):
     torch, B = need_gpu()
     ref = _load("mdlm12_block_step.json")
     case = synth.mdlm12_step_case()
     m = case.model
     C, M, k = case.C, case.B, case.k_unmask
-    dm = B.DeviceModel.from_mdlm(m, C + M)
+    dm = B.DeviceModel.from_mdlm(m, C + M, blocked=blocked)
     ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
                          B.nmdlm_block_step_workspace_size(dm, M, 0)))
     ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()

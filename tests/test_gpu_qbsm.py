@@ -26,12 +26,12 @@ SHAPES = [  # T, M, K, N, density
 ]
 
 
-def _check(case, flags=0, theta_vec=None):
+def _check(case, flags=0, theta_vec=None, blocked=False):
     I_ref = O.qbsm(case.S, case.W, case.bias)
     th = case.theta if theta_vec is None else np.asarray(theta_vec)
     s_ref, _ = O.if_neuron(I_ref, th)
     cur, spk, st, words, _ = run_qbsm(case.S, case.W, case.bias, theta=case.theta,
-                                      theta_vec=theta_vec, flags=flags)
+                                      theta_vec=theta_vec, flags=flags, blocked=blocked)
     assert_same(cur, I_ref)
     assert_same(spk, s_ref)
     assert padding_bits_zero(words, case.N)
@@ -58,6 +58,7 @@ FUSED = 2 << 20       # single kernel, in-kernel list
 WORDS = 3 << 20       # single kernel over 64-channel words
 SCALAR = 5 << 20      # words, scalar gather-accumulate product
 DMA = 4 << 20         # as WORDS, active rows gathered into LDS
+BLOCKED = 6 << 20     # as WORDS, over the blocked weight copy
 
 _FORCED = {
     "dense": 0x1, "P1": 1 << 8, "P2": 2 << 8, "P7": 7 << 8, "RT1": 1 << 16, "RT2": 2 << 16,
@@ -206,3 +207,69 @@ def test_membrane_beyond_int32_with_large_bias(T, path):
     cur, spk, _, _, _ = run_qbsm(S, W, bias, theta=theta, flags=path)
     assert_same(cur, I_ref)
     assert_same(spk, s_ref)
+
+
+# ----------------------------------------------------------------------------
+# blocked weight copy (nmdlm_weight_block, nmdlm_qbsm_blocked)
+# ----------------------------------------------------------------------------
+def _blocked_layout(W, K, N):
+    """The blocked copy as the header defines it, built on the host."""
+    Kw, gx = (K + 63) // 64, (N + 63) // 64
+    Wp = np.zeros((Kw * 64, gx * 64), dtype=np.int8)
+    Wp[:K, :N] = W[:K, :N]
+    out = np.zeros((Kw, gx, 4, 64, 16), dtype=np.int8)
+    for v in range(4):
+        for lane in range(64):
+            g, c = lane // 16, lane % 16
+            # [w][j][x]: W[64w + 16g + j][64x + 4c + v]
+            blk = Wp.reshape(Kw, 64, gx, 64)[:, 16 * g:16 * g + 16, :, 4 * c + v]
+            out[:, :, v, lane, :] = blk.transpose(0, 2, 1)
+    return out.reshape(-1)
+
+
+@pytest.mark.parametrize("K,N,ldw", [(64, 64, 64), (130, 70, 80), (1, 1, 16), (200, 300, 320)])
+def test_blocked_layout(K, N, ldw):
+    torch, B = need_gpu()
+    rng = np.random.default_rng(K * 7 + N)
+    W = rng.integers(-128, 128, size=(K, ldw), dtype=np.int8)
+    Wd = torch.from_numpy(W).cuda()
+    Wb = B.blocked_weights(Wd, K, N, ldw)
+    torch.cuda.synchronize()
+    assert Wb.numel() == B.nmdlm_weight_blocked_bytes(K, N)
+    assert_same(Wb.cpu().numpy(), _blocked_layout(W, K, N), "blocked copy")
+
+
+@pytest.mark.parametrize("flags", [BLOCKED, BLOCKED | (1 << 16), BLOCKED | (2 << 16),
+                                   BLOCKED | (8 << 16), BLOCKED | (2 << 8), BLOCKED | 0x1],
+                         ids=["blocked", "blocked-RT1", "blocked-RT2", "blocked-RT8", "blocked-P2",
+                              "blocked-dense"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"T{s[0]}M{s[1]}K{s[2]}N{s[3]}" for s in SHAPES])
+def test_blocked_ragged_shapes(shape, flags):
+    need_gpu()
+    T, M, K, N, p = shape
+    _check(synth.make_qbsm_case(100 + K + N, T, M, K, N, p), flags=flags, blocked=True)
+
+
+@pytest.mark.parametrize("T,M,K,N,p", [
+    (4, 256, 1024, 384, 0.05),      # 1024 rows: the blocked copy by default
+    (4, 300, 700, 200, 0.02),       # ragged K and N, many row blocks
+    (1, 1100, 130, 90, 0.3),        # T = 1
+    (8, 200, 4096, 128, 0.01),      # long K, sparse words skipped
+])
+def test_blocked_automatic_at_many_rows(T, M, K, N, p):
+    need_gpu()
+    case = synth.make_qbsm_case(T * M + K, T, M, K, N, p)
+    _check(case, blocked=True)
+    case.S[:, :, 64:192] = False     # two words with no active row
+    _check(case, blocked=True)
+
+
+def test_blocked_degenerate_inputs():
+    need_gpu()
+    c = synth.make_qbsm_case(19, 4, 300, 256, 128, 0.1)
+    c.S[:] = False
+    _check(c, flags=BLOCKED, blocked=True)
+    _check(c, blocked=True)
+    c.S[:] = True
+    _check(c, flags=BLOCKED, blocked=True)
+    _check(c, blocked=True)
