@@ -7,7 +7,10 @@ dequantised to fp32 logits, T=4) at one block-denoising step: 32 masked
 tokens over 1024 context tokens, head, confidence and top-8 unmasking.  The
 context prefill runs once, untimed.  Weights are seeded int8 uniforms
 (workloads/synth.py); 640 MB of weights per step, more than the 256 MB
-last-level cache, so every step streams its weights from HBM.
+last-level cache, so every step streams its weights from HBM.  The model
+also holds the blocked copies of its weights (--weights blocked, the
+default): each wave of a product reads them when its words' union is dense;
+--weights rows keeps the row-major weights only.
 
 A "step" is one nmdlm_block_step (block input, per layer the QKV product,
 attention, O, up and down products with their neurons, then the head,
@@ -61,7 +64,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--copies", type=int, default=32, help="rotating layer copies (>= 256 MB total)")
     p.add_argument("--eager", action="store_true", help="issue kernels directly, no HIP graph")
-    p.add_argument("--weights", choices=("rows", "blocked"), default="rows",
+    p.add_argument("--weights", choices=("rows", "blocked"), default="blocked",
                    help="rows: row-major weights only; blocked: also the blocked copies, read by "
                         "products over dense unions")
     p.add_argument("--no-cpu-baseline", action="store_true")
