@@ -805,7 +805,9 @@ __device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds
 // row of an active word read (rows outside the local union meet zero spikes)
 // and a word with no active row skipped.  Each wave takes the copy or the
 // row-major rows by the density of its words' union (a.blk_min).
-template <int RT, int NW, bool TERN = false, bool BLK = false>
+// SCA: the variant with the scalar gather-accumulate product (a.accum == 1);
+// kept out of the others, whose registers it would raise.
+template <int RT, int NW, bool TERN = false, bool BLK = false, bool SCA = false>
 __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
@@ -1088,7 +1090,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
     }
   };
   // MFMA over the words, or (requested) the scalar gather-accumulate product
-  const bool scalar = !TERN && !BLK && a.accum == 1 && !a.dense;  // workgroup-uniform
+  const bool scalar = SCA && !TERN && !BLK && a.accum == 1 && !a.dense;  // workgroup-uniform
   if (!scalar && first != 0x7fffffff && w0 + wave < w1) {  // wave-uniform
     // with a blocked copy, each wave reads it when at least a.blk_min of
     // the 64 rows of its active words are active on average (whole words
@@ -1632,6 +1634,16 @@ static nmdlm_status launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn
       return NMDLM_ERR_HIP;
     hipExtLaunchKernelGGL((k_qbsm_words<RT, NW, true>), grid, dim3(NW * 64), (uint32_t)dyn, st, e0,
                           e1, 0, a);
+    return NMDLM_OK;
+  }
+  // the scalar gather-accumulate product (requested path 5)
+  if (a.accum == 1) {
+    if (dyn > 65536 &&
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&k_qbsm_words<RT, NW, false, false, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+      return NMDLM_ERR_HIP;
+    hipExtLaunchKernelGGL((k_qbsm_words<RT, NW, false, false, true>), grid, dim3(NW * 64),
+                          (uint32_t)dyn, st, e0, e1, 0, a);
     return NMDLM_OK;
   }
   if (dyn > 65536 &&
