@@ -211,3 +211,57 @@ def test_e2d2_full_shape_matches_stored_oracle():
         assert _sha(v) == ref["dec_v_cache_sha256"][l], f"decoder layer {l} values"
     k, v = _packed_caches(dm.layers[case.n_enc - 1], dm.cache_cap, m.d, J)
     assert _sha(k) == ref["last_enc_k_cache_sha256"] and _sha(v) == ref["last_enc_v_cache_sha256"]
+
+
+# ----------------------------------------------------------------------------
+# full-size head on diverse inputs: ordering, not ties
+# ----------------------------------------------------------------------------
+@pytest.fixture(scope="module")
+def head_case():
+    # the 12-layer model's head shape (d=2048, V=32000, T=4) with no layers,
+    # fed with per-token Bernoulli(0.05) spikes: the masked positions predict
+    # many different ids, with distinct confidences
+    m = synth.make_mdlm(synth.SEEDS["mdlm12"] + 50, 0, max_pos=64)
+    T, M, k = m.T, 32, 8
+    X = synth.bernoulli(synth.stream(synth.SEEDS["mdlm12"] + 50, 9), 0.05, (T, M, m.d))
+    tok0 = synth.random_tokens(synth.SEEDS["mdlm12"] + 51, M, m.V).astype(np.int32)
+    msk0 = np.ones(M, dtype=bool)
+    msk0[::4] = False                                 # 24 masked positions
+    logits = O.head_logits(X, m.W_head, m.scale)
+    pred, conf = O.confidence(logits)
+    tok_ref, msk_ref, chosen = O.unmask(tok0, msk0, pred, conf, k)
+    return m, X, tok0, msk0, k, logits, pred, conf, tok_ref, msk_ref, chosen
+
+
+def test_full_size_head_case_is_not_tied(head_case):
+    m, X, tok0, msk0, k, logits, pred, conf, tok_ref, msk_ref, chosen = head_case
+    cm = np.sort(conf[msk0])[::-1]
+    assert len(set(pred[msk0].tolist())) >= 16        # many different predictions
+    assert len(np.unique(cm)) == cm.size              # no two masked confidences equal
+    assert cm[k - 1] > cm[k]                          # the top-k boundary is not a tie
+    assert len(chosen) == k and not msk_ref[chosen].any()
+
+
+@pytest.mark.parametrize("blocked", [False, True], ids=["rows", "blocked-copy"])
+def test_full_size_head_matches_oracle(head_case, blocked):
+    torch, B = need_gpu()
+    m, X, tok0, msk0, k, logits_ref, pred_ref, conf_ref, tok_ref, msk_ref, chosen_ref = head_case
+    T, M = X.shape[0], X.shape[1]
+    dm = B.DeviceModel.from_mdlm(m, 64, blocked=blocked)
+    ws = B.workspace(B.nmdlm_block_step_workspace_size(dm, M, 0))
+    tok = torch.from_numpy(tok0).cuda()
+    msk = torch.from_numpy(msk0.astype(np.uint8)).cuda()
+    logits = torch.empty((M, m.V), dtype=torch.float32, device="cuda")
+    pred = torch.empty(M, dtype=torch.int32, device="cuda")
+    conf = torch.empty(M, dtype=torch.float64, device="cuda")
+    chosen = torch.full((k,), -7, dtype=torch.int32, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, 0, x_in=B.to_dev_bits(synth.pack_bits(X)), tokens=tok,
+                                     masked=msk, k_unmask=k, logits=logits, pred=pred, conf=conf,
+                                     unmasked_pos=chosen), ws)
+    torch.cuda.synchronize()
+    assert_same(logits.cpu().numpy(), logits_ref, "logits")
+    assert_same(pred.cpu().numpy(), pred_ref, "pred")
+    assert np.allclose(conf.cpu().numpy(), conf_ref, rtol=1e-12, atol=0)
+    assert np.array_equal(chosen.cpu().numpy(), np.asarray(chosen_ref))
+    assert np.array_equal(tok.cpu().numpy(), tok_ref)
+    assert np.array_equal(msk.cpu().numpy().astype(bool), msk_ref)
