@@ -807,8 +807,14 @@ __device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds
 // row-major rows by the density of its words' union (a.blk_min).
 // SCA: the variant with the scalar gather-accumulate product (a.accum == 1);
 // kept out of the others, whose registers it would raise.
+// The 64-row blocked variant is held to four waves per SIMD (the head's
+// 1000 workgroups then run in one round instead of two: 29.7 -> 22.5 us at
+// the 12-layer shape); the compiler then keeps a dozen values that live
+// across the word loop in scratch, stored once before it and reloaded once
+// after it.
 template <int RT, int NW, bool TERN = false, bool BLK = false, bool SCA = false>
-__global__ __launch_bounds__(NW * 64) void k_qbsm_words(QbsmArgs a) {
+__global__ __launch_bounds__(NW * 64, (BLK && RT == 4 && NW == 4) ? 4 : 1)
+void k_qbsm_words(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
   __shared__ int sTile[ROWS * kTileLd];
