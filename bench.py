@@ -91,8 +91,8 @@ def parse():
 TRAFFIC = {
     "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
               "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "029e59b1e72c13e081e52d2726f0fdc5e26a39a2cd2959e6bbceef9651aa9dd9",
-               "bytes_per_launch": 8745116.9},
+    "mdlm12": {"sources_sha256": "a9968029a92816cfd10c6a1cfe2f589094e5a4420b5147ca59195a08619c2e44",
+               "bytes_per_launch": 10931732.1},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
