@@ -91,8 +91,8 @@ def parse():
 TRAFFIC = {
     "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
               "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "a9968029a92816cfd10c6a1cfe2f589094e5a4420b5147ca59195a08619c2e44",
-               "bytes_per_launch": 10931732.1},
+    "mdlm12": {"sources_sha256": "004c7d5332778a6b39eee7a8a2318b6ca538d102b7f9d30e6172aaf49b60d1d2",
+               "bytes_per_launch": 10939147.4},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
