@@ -152,8 +152,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   }
 }
 
-// waves per workgroup: 16 for dh = 64; 8 for dh = 128 (its 16 keys of two
-// words per lane need more than the 128 registers of a 1024-thread group);
+// waves per workgroup: 16 for dh = 64; 8 or 12 for dh = 128 (its 16 keys of
+// two words per lane need more than the 128 registers of a 1024-thread group);
 // halved while the grid would not fit the chip in one round (many sequences:
 // fewer waves per workgroup take more key chunks each, the workgroups of all
 // sequences run at once)
@@ -161,6 +161,7 @@ constexpr int kAttnWaves64 = 16, kAttnWaves128 = 8;
 // waves resident at once: 256 CUs x 16 (the kernels' registers allow 4-5
 // waves per SIMD)
 constexpr long long kAttnResidentWaves = 256LL * 16;
+constexpr long long kAttnCus = 256;
 
 struct AttnLaunch {
   const uint64_t* q;
@@ -187,12 +188,18 @@ nmdlm_status launch_attn(const uint64_t* q, const uint64_t* k_cache, const uint6
   const dim3 grid(H, n_seq * ((M + 15) / 16), T);
   const long long wgs = (long long)grid.x * grid.y * grid.z;
   int nw = (dh == 64) ? kAttnWaves64 : kAttnWaves128;
-  while (nw > 4 && wgs * nw > kAttnResidentWaves) nw >>= 1;
+  // dh = 128: 12 waves (168 registers: three waves per SIMD, one workgroup
+  // per CU) when every workgroup has a CU of its own, so that 1024 + 32 keys
+  // take at most two chunks per wave instead of three (12-layer step 0.843
+  // -> 0.839 ms)
+  if (dh == 128 && wgs <= kAttnCus) nw = 12;
+  else while (nw > 4 && wgs * nw > kAttnResidentWaves) nw >>= 1;
   const AttnLaunch l{q, k_cache, vt_cache, cap, T, M, C, H, lut, a_out, n_seq, seq_words};
   switch (dh / 64 * 100 + nw) {
     case 116: attn_launch<1, 16>(grid, l, st); break;
     case 108: attn_launch<1, 8>(grid, l, st); break;
     case 104: attn_launch<1, 4>(grid, l, st); break;
+    case 212: attn_launch<2, 12>(grid, l, st); break;
     case 208: attn_launch<2, 8>(grid, l, st); break;
     case 204: attn_launch<2, 4>(grid, l, st); break;
     default:
