@@ -1098,9 +1098,11 @@ void k_qbsm_words(QbsmArgs a) {
   // MFMA over the words, or (requested) the scalar gather-accumulate product
   const bool scalar = SCA && !TERN && !BLK && a.accum == 1 && !a.dense;  // workgroup-uniform
   if (!scalar && first != 0x7fffffff && w0 + wave < w1) {  // wave-uniform
-    // with a blocked copy, each wave reads it when at least a.blk_min of
-    // the 64 rows of its active words are active on average (whole words
-    // then cost at most 64 / blk_min times the rows), else the rows
+    // with a blocked copy, each wave reads it when its active words have
+    // on average at least a.blk_min active rows of 64 counted over the row
+    // blocks that read the same words (whole words, shared in L2 by the row
+    // blocks, then cost at most 64 / blk_min times the rows' HBM bytes; the
+    // rows cost about 128 vector instructions per word), else the rows
     bool blocked = false;
     if constexpr (BLK) {
       int rows = 0, words = 0;
@@ -1113,7 +1115,7 @@ void k_qbsm_words(QbsmArgs a) {
         rows += __shfl_xor(rows, o);
         words += __shfl_xor(words, o);
       }
-      blocked = rows >= words * a.blk_min;
+      blocked = rows * (int)gridDim.y >= words * a.blk_min;
     }
     if (BLK && blocked) loop(load_blocked, mul_blocked);
     else loop(load_rows, mul_rows);
