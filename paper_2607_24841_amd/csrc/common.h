@@ -61,6 +61,25 @@ __device__ __forceinline__ void tile_coords(int& x, int& y, int& z) {
   x = (l / gy) % gx;
   z = l / (gy * gx);
 }
+// With inv_gy = 1/gy and inv_gxy = 1/(gx gy) the quotients of grids of
+// fewer than 2^21 workgroups are taken in float (exact, see div_small), in
+// place of the integer divisions the scalar unit emulates with some forty
+// instructions each.
+__device__ __forceinline__ void tile_coords_inv(int& x, int& y, int& z, float inv_gy,
+                                                float inv_gxy) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int n = gx * gy * gridDim.z;
+  if (n >= (1 << 21)) {  // uniform
+    tile_coords(x, y, z);
+    return;
+  }
+  const int d = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int l = xcd_order(d, n);
+  const int q = __builtin_amdgcn_readfirstlane(div_small(l, inv_gy));  // l / gy
+  z = __builtin_amdgcn_readfirstlane(div_small(l, inv_gxy));           // l / (gx gy)
+  y = l - q * gy;
+  x = q - z * gx;
+}
 constexpr int kMaxSeg = 3;
 constexpr int kChunkSteps = 16;   // k-steps (of 64 active rows) staged per LDS chunk
 constexpr int kTileLd = 68;       // LDS row stride (ints) of the 64-column output tile
@@ -142,6 +161,9 @@ struct QbsmArgs {
   // the active rows per active word from which a wave reads them
   const int8_t* Wb;
   int blk_min;
+  // 1.0f / gridDim.y and 1.0f / (gridDim.x * gridDim.y) (IEEE, from the
+  // host): the workgroup's tile coordinates without integer divisions
+  float inv_gy, inv_gxy;
 };
 
 // Scratch used by one product (carved from a workspace).

@@ -831,7 +831,7 @@ void k_qbsm_words(QbsmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   int x, y, z;
-  tile_coords(x, y, z);
+  tile_coords_inv(x, y, z, a.inv_gy, a.inv_gxy);
   const int Kw = (a.K + 63) >> 6;
   const int lds_row = 2 * Kw + 1;
   unsigned long long* sLU = sDyn;
@@ -1006,8 +1006,9 @@ void k_qbsm_words(QbsmArgs a) {
   }
   for (int o = kWave / 2; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o));
 
-  const int w0 = (int)(((long long)Kw * z) / a.P);
-  const int w1 = (int)(((long long)Kw * (z + 1)) / a.P);
+  // the K split's words (Kw <= 1024, z < P <= 255: 32-bit products)
+  const int w0 = a.P > 1 ? (Kw * z) / a.P : 0;
+  const int w1 = a.P > 1 ? (Kw * (z + 1)) / a.P : Kw;
   const uint32_t colb = (x * 64 + 4 * c < a.N) ? (uint32_t)(x * 64 + 4 * c) : (uint32_t)(x * 64);
   const uint32_t ldw = (uint32_t)a.ldw;
   const uint32_t lane_base = (uint32_t)(16 * g) * ldw + colb;   // row 16g of word 0
@@ -1955,6 +1956,8 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.counters = scr.counters;
   a.u_out = c.u_out;
   a.u_ld = gx;
+  a.inv_gy = 1.0f / (float)gy;
+  a.inv_gxy = 1.0f / (float)((long long)gx * gy);
   a.S = c.s_in;
   a.Sn = c.s_neg;
   a.upart = pa.upart;
