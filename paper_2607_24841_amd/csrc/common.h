@@ -164,6 +164,9 @@ struct QbsmArgs {
   // 1.0f / gridDim.y and 1.0f / (gridDim.x * gridDim.y) (IEEE, from the
   // host): the workgroup's tile coordinates without integer divisions
   float inv_gy, inv_gxy;
+  // 1.0f / ceil(K/64), 1.0f / Mb and 1.0f / seg_w (several segments): the
+  // in-kernel quotients by div_small
+  float inv_kw, inv_mb, inv_segw;
 };
 
 // Scratch used by one product (carved from a workspace).

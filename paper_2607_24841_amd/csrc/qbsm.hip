@@ -294,10 +294,11 @@ __device__ __forceinline__ EpiRegs epi_load(const QbsmArgs& a, int tid, int x, i
     if (a.bias) r.bias = a.bias[nc];
     if (a.theta_vec) r.theta_ch = a.theta_vec[nc];
   }
-  if (a.mode == EPI_IF || a.mode == EPI_QNL_IF) r.theta_seg = a.seg[(x * 64) / a.seg_w].theta;
+  if (a.mode == EPI_IF || a.mode == EPI_QNL_IF)
+    r.theta_seg = a.seg[a.nseg > 1 ? div_small(x * 64, a.inv_segw) : 0].theta;
   if (a.resid && wv * 64 < a.T * a.Mb) {  // T * Mb <= 16 * RT <= kMaxEpiTokens
     const int i = min(tid, a.T * a.Mb - 1);
-    const int t = div_small(i, 1.0f / (float)a.Mb), m = min(y * a.Mb + (i - t * a.Mb), a.M - 1);
+    const int t = div_small(i, a.inv_mb), m = min(y * a.Mb + (i - t * a.Mb), a.M - 1);
     r.resid = a.resid[t * a.rld_t + (int64_t)m * a.rld_m + x];
   }
   if (a.mode == EPI_QNL_IF && wv < 4) r.lut = (int)(signed char)a.lut[tid & 255];
@@ -314,7 +315,7 @@ __device__ __forceinline__ void epi_store(const QbsmArgs& a, EpiStage& ep, const
     ep.theta[tid] = a.theta_vec ? (nv ? r.theta_ch : 1) : r.theta_seg;
   }
   if (a.resid && tid < a.T * a.Mb) {
-    const int t = div_small(tid, 1.0f / (float)a.Mb), m = y * a.Mb + (tid - t * a.Mb);
+    const int t = div_small(tid, a.inv_mb), m = y * a.Mb + (tid - t * a.Mb);
     ep.resid[tid] = m < a.M ? r.resid : 0ull;
   }
   if (a.mode == EPI_QNL_IF && tid < 256) ep.lut[tid] = (signed char)r.lut;
@@ -546,7 +547,7 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
     }
     return;
   }
-  const int segi = (a.mode == EPI_CUR) ? 0 : n0 / a.seg_w;
+  const int segi = (a.mode == EPI_CUR || a.nseg == 1) ? 0 : div_small(n0, a.inv_segw);
   SpikeSeg seg = a.seg[segi];
   const int wseg = (n0 - segi * a.seg_w) >> 6;
   const int bias_n = ep.bias[col];
@@ -658,7 +659,8 @@ __device__ __forceinline__ unsigned long long or_slice(const uint64_t* src, int 
                                                        int tid) {
   unsigned long long u = 0ull;
   if (NT < Kw) return u;
-  const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
+  const float inv_kw = 1.0f / (float)Kw;
+  const int slices = div_small(NT, inv_kw), s0 = div_small(tid, inv_kw), w = tid - s0 * Kw;
   if (s0 >= slices) return u;
   int r = s0;
   for (; r + 3 * slices < nsrc; r += 4 * slices)
@@ -675,7 +677,8 @@ __device__ __forceinline__ void or_merge(unsigned long long* dst, const uint64_t
                                          int Kw, int tid, unsigned long long u,
                                          unsigned long long last_mask) {
   if (NT >= Kw) {
-    const int slices = NT / Kw, s0 = tid / Kw, w = tid - s0 * Kw;
+    const float inv_kw = 1.0f / (float)Kw;
+    const int slices = div_small(NT, inv_kw), s0 = div_small(tid, inv_kw), w = tid - s0 * Kw;
     if (w == Kw - 1) u &= last_mask;
     if (s0 < slices && u) atomicOr(&dst[w], u);
   } else {
@@ -854,7 +857,7 @@ void k_qbsm_words(QbsmArgs a) {
   const EpiRegs er = epi_load<NT>(a, tid, x, y);
   // thread tid takes word wq = tid % Kw and rows r0 = tid / Kw, + rpp, ...
   // (rpp = NT / Kw rows per pass; none when the words outnumber the threads)
-  const float inv_kw = 1.0f / (float)Kw, inv_mb = 1.0f / (float)a.Mb;
+  const float inv_kw = a.inv_kw, inv_mb = a.inv_mb;
   const int r0 = div_small(tid, inv_kw), wq = tid - r0 * Kw;
   const int rpp = div_small(NT, inv_kw);
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1957,6 +1960,9 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.u_out = c.u_out;
   a.u_ld = gx;
   a.inv_gy = 1.0f / (float)gy;
+  a.inv_kw = 1.0f / (float)Kw;
+  a.inv_mb = 1.0f / (float)Mb;
+  a.inv_segw = 1.0f / (float)std::max(1, std::min(c.seg_w, 1 << 22));
   a.inv_gxy = 1.0f / (float)((long long)gx * gy);
   a.S = c.s_in;
   a.Sn = c.s_neg;
