@@ -156,9 +156,10 @@ size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
  * nmdlm_qbsm_blocked: nmdlm_qbsm (same arguments, results and errors) with
  *   the blocked copy Wb of W also given.  With path 6 in the flags every
  *   word is read from the copy; unforced, each wave of the product reads it
- *   when its words' union is dense (on average at least
- *   NMDLM_BLOCKED_MIN_ROWS of the 64 rows of its active words active, so
- *   whole words cost at most twice the active rows' bytes), else the
+ *   when its words' union is dense: on average at least
+ *   NMDLM_BLOCKED_MIN_ROWS active rows of 64 per active word, counted over
+ *   the row blocks of the product that read the same words (the whole words
+ *   then cost at most twice the active rows' bytes from HBM); else the
  *   row-major rows of W.  Results do not depend on which is used.
  *   NMDLM_ERR_UNSUPPORTED when the copy would exceed 2^31 bytes.
  * ------------------------------------------------------------------------ */
@@ -415,8 +416,11 @@ typedef struct nmdlm_layer {
                             (t, j/64, c) is value channel c of position j */
   /* Blocked copies (nmdlm_weight_block, ldw = N) of the four weights, or
    * NULL.  With a copy, each wave of a product reads it when its words'
-   * union is dense (at least half the rows of its active words active),
-   * else the row-major rows.  Results do not depend on it. */
+   * union, counted over the row blocks that share the words, is dense
+   * (NMDLM_BLOCKED_MIN_ROWS), else the row-major rows.  Path 6 in the flags
+   * (every word from the copies) requires every copy, and the head's when
+   * the step runs the head (NMDLM_ERR_INVALID_ARG otherwise).  Results do
+   * not depend on it. */
   const int8_t* w_qkv_b;
   const int8_t* w_o_b;
   const int8_t* w_up_b;

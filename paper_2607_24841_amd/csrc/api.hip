@@ -366,6 +366,7 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   if ((int64_t)io->C + io->M > NMDLM_MAX_KEYS || md->cache_cap / 64 > INT_MAX)
     return NMDLM_ERR_UNSUPPORTED;
   if (md->n_layers > 0 && !md->layers) return NMDLM_ERR_INVALID_ARG;
+  const bool forced_blocked = ((io->flags >> NMDLM_PATH_SHIFT) & 0x7u) == 6u;
   for (int l = 0; l < md->n_layers; ++l) {
     const nmdlm_layer& L = md->layers[l];
     if (!weights_ok(L.w_qkv, md->d, 3 * md->d, 3 * (int64_t)md->d) ||
@@ -375,6 +376,9 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
     if (!L.lut_att || !L.lut_act || !L.k_cache || !L.vt_cache) return NMDLM_ERR_INVALID_ARG;
     if (!blocked_ok(L.w_qkv_b, md->d, 3 * md->d) || !blocked_ok(L.w_o_b, md->d, md->d) ||
         !blocked_ok(L.w_up_b, md->d, md->F) || !blocked_ok(L.w_dn_b, md->F, md->d))
+      return NMDLM_ERR_INVALID_ARG;
+    // path 6 (every word from the blocked copies) needs every copy
+    if (forced_blocked && (!L.w_qkv_b || !L.w_o_b || !L.w_up_b || !L.w_dn_b))
       return NMDLM_ERR_INVALID_ARG;
     if (L.theta_q <= 0 || L.theta_k <= 0 || L.theta_v <= 0 || L.theta_a <= 0 || L.theta_o <= 0 ||
         L.theta_up <= 0 || L.theta_dn <= 0)
@@ -389,7 +393,7 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   const bool head = !(io->flags & NMDLM_NO_HEAD);
   if (head) {
     if (!weights_ok(md->w_head, md->d, md->V, md->V) || !md->head_scale ||
-        !blocked_ok(md->w_head_b, md->d, md->V))
+        !blocked_ok(md->w_head_b, md->d, md->V) || (forced_blocked && !md->w_head_b))
       return NMDLM_ERR_INVALID_ARG;
     if (!io->tokens || !io->masked || io->k_unmask < 0) return NMDLM_ERR_INVALID_ARG;
     if (io->M > NMDLM_MAX_HEAD_M) return NMDLM_ERR_UNSUPPORTED;

@@ -148,6 +148,15 @@ def test_block_step_argument_errors(lib):
     mhb = B.Model(1, 1024, 16, 4096, 32000, 4, 8192, 0, layers, None, None, FAKE, FAKE, 1, FAKE + 4)
     head16 = B.step_io(16, 512, flags=0, x_in=FAKE, tokens=FAKE, masked=FAKE, k_unmask=4)
     assert call(mhb, head16) == B.NMDLM_ERR_INVALID_ARG
+    # path 6 forced: every layer (and the head) needs its blocked copies
+    forced = B.step_io(16, 512, flags=B.NMDLM_NO_HEAD | B.NMDLM_PATH_BLOCKED, x_in=FAKE)
+    assert call(m, forced) == B.NMDLM_ERR_INVALID_ARG
+    Lc = B.Layer(FAKE, FAKE, FAKE, FAKE, 200, 200, 200, 200, 200, 200, 200, 4, FAKE, FAKE, FAKE,
+                 FAKE, FAKE, FAKE, FAKE, FAKE)
+    mc = B.Model(1, 1024, 16, 4096, 32000, 4, 8192, 0, (B.Layer * 1)(Lc), None, None, FAKE, FAKE)
+    forced_head = B.step_io(16, 512, flags=B.NMDLM_PATH_BLOCKED, x_in=FAKE, tokens=FAKE,
+                            masked=FAKE, k_unmask=4)
+    assert call(mc, forced_head) == B.NMDLM_ERR_INVALID_ARG       # head copy missing
 
 
 def test_batched_step_argument_errors(lib):
