@@ -872,7 +872,7 @@ void k_qbsm_words(QbsmArgs a) {
     upv[k] = 0ull;
     // waves with a part to load (uniform); other lanes load a valid word
     if (up_regs && wr0 + k * slices < a.nparts)
-      upv[k] = a.upart[(size_t)min(s0 + k * slices, a.nparts - 1) * Kw + wq];
+      upv[k] = a.upart[(uint32_t)(min(s0 + k * slices, a.nparts - 1) * Kw + wq)];
   }
   // this row block's spike rows: tile row lr = r0 + k * rpp, word wq; rows
   // past the tile or the block load a valid word and drop it
@@ -888,7 +888,8 @@ void k_qbsm_words(QbsmArgs a) {
     if (wr0 < rpp && wr0 + k * rpp < ROWS) {  // wave-uniform
       const int lc = min(lr, ROWS - 1);
       const int t = div_small(lc, inv_mb), m = y * a.Mb + (lc - t * a.Mb);
-      const size_t src = (size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + wq;
+      // T*M <= 2^19 rows of at most 1024 words: 32-bit offsets
+      const uint32_t src = (uint32_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * (uint32_t)Kw + wq;
       rv[k] = a.S[src];
       if constexpr (TERN) rvn[k] = a.Sn[src];
       rdst[k] = (r0 < rpp && lr < ROWS) ? lr * lds_row + 2 * wq : -1;
@@ -937,7 +938,7 @@ void k_qbsm_words(QbsmArgs a) {
       const int i = i0 + j * NT, ic = min(i, items - 1);
       const int lr = div_small(ic, inv_kw), w = ic - lr * Kw;
       const int t = div_small(lr, inv_mb), m = y * a.Mb + (lr - t * a.Mb);
-      const size_t src = (size_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * Kw + w;
+      const uint32_t src = (uint32_t)(min(t, a.T - 1) * a.M + min(m, a.M - 1)) * (uint32_t)Kw + w;
       v[j] = a.S[src];
       if constexpr (TERN) vn[j] = a.Sn[src];
       kp |= (uint32_t)(i < items && t < a.T && m < a.M) << j;
