@@ -91,8 +91,8 @@ def parse():
 TRAFFIC = {
     "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
               "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "9dad4e51f25546b422233490da8ed557778c09da737244612aa6fa0757e3626d",
-               "bytes_per_launch": 14233812.2},
+    "mdlm12": {"sources_sha256": "03343e123121d74e91761a9229d6bff32a85f2108d08dcd102dbfc831c5ff904",
+               "bytes_per_launch": 14220054.2},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
