@@ -61,8 +61,10 @@ typedef enum nmdlm_status {
  * 4 = as 3, gathering the active rows straight into LDS; 5 = as 3 with a
  * scalar gather-accumulate product in place of MFMA: per spike of a row,
  * the active weight row's columns are loaded and added; 6 = as 3 over the
- * blocked copy of the weights, nmdlm_qbsm_blocked only).  Results do not
- * depend on it. */
+ * blocked copy of the weights, nmdlm_qbsm_blocked only; 7 = as 6 with wide
+ * tiles where the row tile is 64 rows: a workgroup takes four 64-column
+ * tiles, each wave one of them over all of K).  Results do not depend on
+ * it. */
 #define NMDLM_PATH_SHIFT 20u
 #define NMDLM_NO_FUSE (1u << NMDLM_PATH_SHIFT)
 
@@ -160,7 +162,10 @@ size_t nmdlm_qbsm_workspace_size(int T, int M, int K, int N);
  *   NMDLM_BLOCKED_MIN_ROWS active rows of 64 per active word, counted over
  *   the row blocks of the product that read the same words (the whole words
  *   then cost at most twice the active rows' bytes from HBM); else the
- *   row-major rows of W.  Results do not depend on which is used.
+ *   row-major rows of W.  Products of 64-row tiles over at least 1536 output
+ *   tiles of 64 x 64 (and path 7 in the flags) take wide tiles: four column
+ *   tiles per workgroup, each read from the copy over all of K.  Results do
+ *   not depend on which is used.
  *   NMDLM_ERR_UNSUPPORTED when the copy would exceed 2^31 bytes.
  * ------------------------------------------------------------------------ */
 #define NMDLM_BLOCKED_MIN_ROWS 32

@@ -40,6 +40,7 @@ NMDLM_PATH_WORDS = 3 << NMDLM_PATH_SHIFT   # single kernel over 64-channel words
 NMDLM_PATH_DMA = 4 << NMDLM_PATH_SHIFT     # as words, active rows gathered into LDS
 NMDLM_PATH_SCALAR = 5 << NMDLM_PATH_SHIFT  # as words, scalar gather-accumulate product
 NMDLM_PATH_BLOCKED = 6 << NMDLM_PATH_SHIFT  # as words, over the blocked weight copy
+NMDLM_PATH_WIDE = 7 << NMDLM_PATH_SHIFT     # as blocked, four column tiles per workgroup
 NMDLM_BLOCKED_MIN_ROWS = 32
 NMDLM_QNL_S8 = 0
 NMDLM_QNL_U8 = 1

@@ -366,7 +366,8 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
   if ((int64_t)io->C + io->M > NMDLM_MAX_KEYS || md->cache_cap / 64 > INT_MAX)
     return NMDLM_ERR_UNSUPPORTED;
   if (md->n_layers > 0 && !md->layers) return NMDLM_ERR_INVALID_ARG;
-  const bool forced_blocked = ((io->flags >> NMDLM_PATH_SHIFT) & 0x7u) == 6u;
+  const unsigned path_req = (io->flags >> NMDLM_PATH_SHIFT) & 0x7u;
+  const bool forced_blocked = path_req == 6u || path_req == 7u;
   for (int l = 0; l < md->n_layers; ++l) {
     const nmdlm_layer& L = md->layers[l];
     if (!weights_ok(L.w_qkv, md->d, 3 * md->d, 3 * (int64_t)md->d) ||
@@ -377,7 +378,7 @@ nmdlm_status nmdlm_block_step(const nmdlm_model* md, nmdlm_step_io* io, void* ws
     if (!blocked_ok(L.w_qkv_b, md->d, 3 * md->d) || !blocked_ok(L.w_o_b, md->d, md->d) ||
         !blocked_ok(L.w_up_b, md->d, md->F) || !blocked_ok(L.w_dn_b, md->F, md->d))
       return NMDLM_ERR_INVALID_ARG;
-    // path 6 (every word from the blocked copies) needs every copy
+    // paths 6 and 7 (every word from the blocked copies) need every copy
     if (forced_blocked && (!L.w_qkv_b || !L.w_o_b || !L.w_up_b || !L.w_dn_b))
       return NMDLM_ERR_INVALID_ARG;
     if (L.theta_q <= 0 || L.theta_k <= 0 || L.theta_v <= 0 || L.theta_a <= 0 || L.theta_o <= 0 ||

@@ -639,6 +639,139 @@ __device__ void epilogue(const QbsmArgs& a, const int* sTile, EpiStage& ep,
   }
 }
 
+// Epilogue of a wide tile (one wave, one 64-column tile, 64 rows), from the
+// wave's accumulators: acc[q][v][e] of lane (g, c) is tile row 16q + 4g + e,
+// column 4c + v.  With row blocks of Mb = 64 / T tokens (T = 1, 2, 4), row
+// t Mb + m lies in q = t Mb / 16 + m / 16 with 4g + e = m % 16, so a lane
+// holds all T currents of its 16 neurons (tokens 16k + 4g + e, k < Mb / 16;
+// columns 4c + v) and integrates them in registers.  Spike words (t, m) of
+// the tile's 64 columns are assembled in the wave's 256 LDS dwords: each
+// lane writes the nibble of its four columns as a byte, lane i then packs
+// the 16 nibbles of word i.  Channel-major output meets in ep.vbits as in
+// the workgroup epilogue.  Modes: currents, IF, table + IF, head logits.
+template <int T>
+__device__ __forceinline__ void wide_epilogue(const QbsmArgs& a, const v4i (&acc)[4][4], EpiStage& ep,
+                                              uint32_t* nib, int lane, int x, int y) {
+  constexpr int KB = 4 / T;       // 16-token groups of a row block
+  constexpr int Mb = 16 * KB;     // tokens of the row block
+  const int g = lane >> 4, c = lane & 15;
+  const int n0 = x * 64;
+  if (a.mode == EPI_HEAD) {
+    // logits: the sum over the steps, dequantised per column
+    float sc[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sc[v] = n0 + 4 * c + v < a.N ? a.scale[n0 + 4 * c + v] : 0.f;
+#pragma unroll
+    for (int k = 0; k < KB; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = y * Mb + 16 * k + 4 * g + e;
+        if (m >= a.M) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          int sum = 0;
+#pragma unroll
+          for (int t = 0; t < T; ++t) sum += acc[t * KB + k][v][e];
+          const int n = n0 + 4 * c + v;
+          if (n < a.N) a.logits[(size_t)m * a.N + n] = (float)sum * sc[v];
+        }
+      }
+    return;
+  }
+  const bool spikes = a.mode != EPI_CUR;
+  const int segi = (a.mode == EPI_CUR || a.nseg == 1) ? 0 : div_small(n0, a.inv_segw);
+  SpikeSeg seg = a.seg[segi];
+  const int wseg = (n0 - segi * a.seg_w) >> 6;
+  const bool tr = spikes && seg.transposed;
+  const bool qnl = a.mode == EPI_QNL_IF, res = a.resid != nullptr;
+  // spike bits: byte (t, k, e) of this lane holds columns 4c..4c+3
+  uint32_t sb[T * KB];
+#pragma unroll
+  for (int i = 0; i < T * KB; ++i) sb[i] = 0u;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int col = 4 * c + v, n = n0 + col;
+    const bool nv = n < a.N;
+    const int bias_n = ep.bias[col], theta = ep.theta[col];
+#pragma unroll
+    for (int k = 0; k < KB; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ml = 16 * k + 4 * g + e, m = y * Mb + ml;
+        long long V = 0;  // int64: T currents up to 2^31 in magnitude plus theta
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          int I = acc[t * KB + k][v][e] + bias_n;
+          if (a.cur_out && nv && m < a.M) a.cur_out[((size_t)t * a.M + m) * a.N + n] = I;
+          if (!spikes) continue;
+          if (qnl) I = (int)ep.lut[min(127, max(-128, I >> a.lut_shift)) & 0xFF];
+          long long Iv = I;
+          if (res && ((ep.resid[t * Mb + ml] >> col) & 1ull)) Iv += theta;
+          V += Iv;
+          const bool s = nv && V >= theta;
+          if (s) V -= theta;
+          sb[t * KB + k] |= (uint32_t)s << (8 * e + v);
+        }
+      }
+  }
+  if (!spikes) return;
+  if (tr) {
+    // channel-major: the row block's token bits of each (step, column)
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        uint32_t bits = 0u;
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            bits |= ((sb[t * KB + k] >> (8 * e + v)) & 1u) << (16 * k + 4 * g + e);
+        if (bits) atomicOr(&ep.vbits[t * 64 + 4 * c + v], bits);
+      }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    write_channel_major(a, ep, seg, segi, 0, lane, n0 + lane, n0 + lane < a.N, y);
+    return;
+  }
+  // natural words: byte c of word (t, ml) at nib[(t Mb + ml) * 4 + c / 4]
+  uint8_t* nb = reinterpret_cast<uint8_t*>(nib);
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int k = 0; k < KB; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        nb[(t * Mb + 16 * k + 4 * g + e) * 16 + c] = (uint8_t)((sb[t * KB + k] >> (8 * e)) & 0xFu);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // lane i: word i = (t, ml) (64 = T * Mb words), the low nibbles of its 16 bytes
+  const int t = lane / Mb, ml = lane - t * Mb, m = y * Mb + ml;
+  uint32_t h[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    uint32_t w = nib[lane * 4 + d] & 0x0F0F0F0Fu;
+    w = (w | (w >> 4)) & 0x00FF00FFu;
+    h[d] = (w | (w >> 8)) & 0x0000FFFFu;
+  }
+  const uint64_t word = (uint64_t)(h[0] | (h[1] << 16)) | ((uint64_t)(h[2] | (h[3] << 16)) << 32);
+  const bool mv = m < a.M;
+  if (mv) {
+    const int64_t mo = seg.seq_len > 0
+                           ? (int64_t)(m / seg.seq_len) * seg.ld_s + (int64_t)(m % seg.seq_len) * seg.ld_m
+                           : (int64_t)m * seg.ld_m;
+    seg.ptr[t * seg.ld_t + mo + wseg] = word;
+  }
+  if (a.u_out) {
+    // partial union of the tile's output word over the row block
+    uint64_t u = mv ? word : 0ull;
+    for (int o = kWave / 2; o > 0; o >>= 1) u |= __shfl_xor(u, o);
+    if (lane == 0) a.u_out[(size_t)y * a.u_ld + x] = u;
+  }
+}
+
 // ------------------------------------------------- weight-skip statistics
 // The statistics of a product are those of the whole block: the number of
 // input rows (channels) active in the union of all its spike rows.  Workgroup
@@ -815,14 +948,22 @@ __device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds
 // the 12-layer shape); the compiler then keeps a dozen values that live
 // across the word loop in scratch, stored once before it and reloaded once
 // after it.
-template <int RT, int NW, bool TERN = false, bool BLK = false, bool SCA = false>
+// WIDE: a workgroup takes NW adjacent 64-column tiles of one row block, wave
+// j the tile NW x + j over every word of K (blocked copy only): the spike
+// staging, the union and the epilogue operands are shared by NW tiles, the
+// waves' accumulators need no reduction, and the tiles' epilogues run one
+// after the other over the LDS tile.
+template <int RT, int NW, bool TERN = false, bool BLK = false, bool SCA = false, bool WIDE = false>
 __global__ __launch_bounds__(NW * 64, (BLK && RT == 4 && NW == 4) ? 4 : 1)
 void k_qbsm_words(QbsmArgs a) {
+  static_assert(!WIDE || (BLK && !TERN && !SCA && RT == 4 && NW == 4), "wide tiles: blocked, 64 rows");
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
-  __shared__ int sTile[ROWS * kTileLd];
+  constexpr int NE = WIDE ? NW : 1;  // column tiles (epilogue stages) per workgroup
+  // WIDE: the waves' 1 KB spike-word exchanges in place of the LDS tile
+  __shared__ int sTile[WIDE ? NW * 256 : ROWS * kTileLd];
   __shared__ unsigned long long sUn[NW];
-  __shared__ EpiStage ep;
+  __shared__ EpiStage ep[NE];
   __shared__ int sLast;
   __shared__ int sStatCnt;
   // dynamic: local union [Kw] (u64), the block union of the statistics [Kw]
@@ -843,6 +984,9 @@ void k_qbsm_words(QbsmArgs a) {
   // ternary input: the -1 spike rows follow the +1 rows, same layout
   uint32_t* sSn = sS + ROWS * lds_row;
   const bool stats_wg = a.stats && x == 0 && y == 0 && z == 0;  // workgroup-uniform
+  const int gx = WIDE ? (a.N + 63) >> 6 : 0;  // column tiles (WIDE)
+  // this wave's column tile (WIDE), else the workgroup's
+  const int xs = WIDE ? x * NW + wave : x;
 
   const unsigned long long last_mask = (a.K & 63) ? (1ull << (a.K & 63)) - 1ull : ~0ull;
   // With the producer's partial unions, the union is their OR over the whole
@@ -854,7 +998,12 @@ void k_qbsm_words(QbsmArgs a) {
   const bool stats_rows = stats_wg && !from_parts && !a.dense;  // block union from the rows
 
   // ---- staging, load phase: every load goes out before the first is used
-  const EpiRegs er = epi_load<NT>(a, tid, x, y);
+  const EpiRegs er = epi_load<NT>(a, tid, WIDE ? min(x * NW, gx - 1) : x, y);
+  EpiRegs erw[NE > 1 ? NE - 1 : 1];  // WIDE: the other column tiles' operands
+  if constexpr (WIDE) {
+#pragma unroll
+    for (int j = 1; j < NE; ++j) erw[j - 1] = epi_load<NT>(a, tid, min(x * NW + j, gx - 1), y);
+  }
   // thread tid takes word wq = tid % Kw and rows r0 = tid / Kw, + rpp, ...
   // (rpp = NT / Kw rows per pass; none when the words outnumber the threads)
   const float inv_kw = a.inv_kw, inv_mb = a.inv_mb;
@@ -907,8 +1056,13 @@ void k_qbsm_words(QbsmArgs a) {
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- staging, store phase
-  for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
-  epi_store<NT>(a, ep, er, tid, x, y);
+  if constexpr (!WIDE)
+    for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
+  epi_store<NT>(a, ep[0], er, tid, WIDE ? min(x * NW, gx - 1) : x, y);
+  if constexpr (WIDE) {
+#pragma unroll
+    for (int j = 1; j < NE; ++j) epi_store<NT>(a, ep[j], erw[j - 1], tid, min(x * NW + j, gx - 1), y);
+  }
   if (from_parts || (ROWS > 32 && !a.dense && NT >= Kw))
     for (int w = tid; w < Kw; w += NT) sLU[w] = 0ull;
   if (stats_wg && tid == 0) sStatCnt = 0;
@@ -1028,7 +1182,7 @@ void k_qbsm_words(QbsmArgs a) {
   // line is read anyway.  Every word then issues the same 16 loads, so the
   // next word's loads can be in flight while the current one is multiplied.
   const uint32_t first_off = (uint32_t)first * ldw + colb;
-  const int stride = NW;
+  const int stride = WIDE ? 1 : NW;
   auto load_rows = [&](int w, uint32_t (&xg)[16]) {
     const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
     const uint32_t m16 = (uint32_t)(u >> (16 * g)) & 0xFFFFu;
@@ -1042,7 +1196,8 @@ void k_qbsm_words(QbsmArgs a) {
   // blocked copy: a word of the tile is four 16-byte operand loads; an
   // inactive word (or one past the range) re-reads the first active word
   const int gxb = (a.N + 63) >> 6;
-  const char* Wbb = reinterpret_cast<const char*>(a.Wb) + (size_t)x * 4096 + (size_t)lane * 16;
+  const char* Wbb = reinterpret_cast<const char*>(a.Wb) + (size_t)(WIDE ? min(xs, gxb - 1) : x) * 4096 +
+                    (size_t)lane * 16;
   auto load_blocked = [&](int w, uint32_t (&xg)[16]) {
     const unsigned long long u = (w < w1) ? sLU[w] : 0ull;
     const int ws = u ? w : (first >> 6);
@@ -1086,7 +1241,7 @@ void k_qbsm_words(QbsmArgs a) {
   // the words of this wave, the next one's loads in flight while the
   // current one is multiplied
   auto loop = [&](auto&& load, auto&& mul) {
-    int jw = w0 + wave;
+    int jw = WIDE ? w0 : w0 + wave;
     uint32_t xa[16], xb[16];
     load(jw, xa);
     while (true) {
@@ -1102,14 +1257,14 @@ void k_qbsm_words(QbsmArgs a) {
   };
   // MFMA over the words, or (requested) the scalar gather-accumulate product
   const bool scalar = SCA && !TERN && !BLK && a.accum == 1 && !a.dense;  // workgroup-uniform
-  if (!scalar && first != 0x7fffffff && w0 + wave < w1) {  // wave-uniform
+  if (!scalar && first != 0x7fffffff && (WIDE ? xs < gx : w0 + wave < w1)) {  // wave-uniform
     // with a blocked copy, each wave reads it when its active words have
     // on average at least a.blk_min active rows of 64 counted over the row
     // blocks that read the same words (whole words, shared in L2 by the row
     // blocks, then cost at most 64 / blk_min times the rows' HBM bytes; the
     // rows cost about 128 vector instructions per word), else the rows
-    bool blocked = false;
-    if constexpr (BLK) {
+    bool blocked = WIDE;
+    if constexpr (BLK && !WIDE) {
       int rows = 0, words = 0;
       for (int w = w0 + wave + lane * stride; w < w1; w += 64 * stride) {
         const unsigned long long u = sLU[w];
@@ -1128,12 +1283,22 @@ void k_qbsm_words(QbsmArgs a) {
   if (scalar) scalar_accumulate<ROWS, NT>(a, sS, lds_row, sTile, tid, x, y, w0, w1);
 
   __syncthreads();
-  if (!scalar) reduce_tile<RT>(acc, sTile, g, c);
+  if (!scalar && !WIDE) reduce_tile<RT>(acc, sTile, g, c);
   if (stats_wg) stats_count<NT>(a, from_parts ? sLU : sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
   if (stats_wg && tid == 0) stats_write(a, sStatCnt);
+  if constexpr (WIDE) {
+    // each wave finishes its own tile from its accumulators (no barrier)
+    if (xs < gx) {
+      uint32_t* nib = reinterpret_cast<uint32_t*>(sTile) + wave * 256;
+      if (a.T == 4) wide_epilogue<4>(a, acc, ep[wave], nib, lane, xs, y);
+      else if (a.T == 2) wide_epilogue<2>(a, acc, ep[wave], nib, lane, xs, y);
+      else wide_epilogue<1>(a, acc, ep[wave], nib, lane, xs, y);
+    }
+    return;
+  }
   const bool last = !(a.P > 1) || split_fixup<ROWS, NT>(a, sTile, &sLast, tid, x, y, z);
-  if (last) epilogue<NW>(a, sTile, ep, sUn, tid, lane, wave, x, y);
+  if (last) epilogue<NW>(a, sTile, ep[0], sUn, tid, lane, wave, x, y);
 }
 
 // ------------------------------------------------- LDS-streamed product
@@ -1575,6 +1740,7 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_list(QbsmArgs a) {
 // host side
 // ---------------------------------------------------------------------------
 constexpr size_t kWordsLdsBudget = 81920;  // word product: two workgroups per CU fit in LDS
+constexpr int kWideMinTiles = 1536;  // output tiles (64 x 64) from which blocked products go wide
 constexpr int kCus = 256;            // compute units of the device
 constexpr int kThreadsPerCu = 2048;  // resident threads per compute unit
 
@@ -1628,7 +1794,19 @@ static void launch_fused(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStr
 
 template <int RT, int NW>
 static nmdlm_status launch_words(const dim3& grid, const QbsmArgs& a, size_t dyn, hipStream_t st,
-                                 hipEvent_t e0, hipEvent_t e1) {
+                                 hipEvent_t e0, hipEvent_t e1, bool wide = false) {
+  // wide tiles: NW column tiles per workgroup over the blocked weights
+  if constexpr (RT == 4 && NW == 4) {
+    if (wide) {
+      const void* fn = reinterpret_cast<const void*>(&k_qbsm_words<4, 4, false, true, false, true>);
+      if (dyn > 65536 &&
+          hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn) != hipSuccess)
+        return NMDLM_ERR_HIP;
+      hipExtLaunchKernelGGL((k_qbsm_words<4, 4, false, true, false, true>), grid, dim3(256),
+                            (uint32_t)dyn, st, e0, e1, 0, a);
+      return NMDLM_OK;
+    }
+  }
   // blocked weights: the variant loading operand-order words
   if (a.Wb) {
     if (dyn > 65536 &&
@@ -1730,8 +1908,9 @@ nmdlm_status launch_weight_block(const int8_t* W, int K, int N, int64_t ldw, int
 }
 
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
-static size_t words_lds(int RT, int NW, int Kw, bool tern = false) {
-  return (size_t)RT * 16 * kTileLd * 4 + (size_t)NW * 12 + sizeof(EpiStage) + 64 +
+static size_t words_lds(int RT, int NW, int Kw, bool tern = false, bool wide = false) {
+  return (wide ? (size_t)NW * 1024 : (size_t)RT * 16 * kTileLd * 4) + (size_t)NW * 12 +
+         sizeof(EpiStage) * (wide ? NW : 1) + 64 +
          (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
 }
 
@@ -1831,9 +2010,12 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     path = 3;
   }
   // 6: the word product over blocked weights (requested: every wave reads
-  // the copy; unrequested, with a copy: each wave chooses by its union)
+  // the copy; unrequested, with a copy: each wave chooses by its union);
+  // 7: as 6 with wide tiles where the row tile is 64 rows
   bool blk = false;
   int blk_min = kBlockedMinRows;
+  const bool wide_req = path == 7;
+  if (path == 7) path = 6;
   if (path == 6) {
     if (!c.Wb || tern) return NMDLM_ERR_UNSUPPORTED;
     blk = true;
@@ -1896,6 +2078,18 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     if (fused && fused_static_lds(RT, NW) + dyn > kLdsBudget) fused = false;
     if (fused && !c.u_in && !dense && (long long)R * Kw > kUnionDirect) fused = false;
   }
+
+  // wide tiles (a workgroup takes four 64-column tiles of a 64-row block,
+  // each wave one tile over all of K): requested, or for blocked products of
+  // many output tiles, where the per-tile staging, union and reduction of
+  // the word kernel would be repeated by every column tile
+  bool wide = false;
+  if (words && blk && accum == 0 && P == 1 && RT == 4 && (c.T == 1 || c.T == 2 || c.T == 4) &&
+      (c.mode == EPI_CUR || c.mode == EPI_IF || c.mode == EPI_QNL_IF || c.mode == EPI_HEAD) &&
+      words_lds(4, 4, Kw, false, true) <= kWordsLdsBudget)
+    wide = wide_req || (path_auto && tiles >= kWideMinTiles);
+  const int gxl = wide ? (gx + 3) / 4 : gx;  // grid columns
+  if (wide) NW = 4;
 
   nmdlm_status rc0 = NMDLM_OK;
   PrepArgs pa;
@@ -1964,7 +2158,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.inv_kw = 1.0f / (float)Kw;
   a.inv_mb = 1.0f / (float)Mb;
   a.inv_segw = 1.0f / (float)std::max(1, std::min(c.seg_w, 1 << 22));
-  a.inv_gxy = 1.0f / (float)((long long)gx * gy);
+  a.inv_gxy = 1.0f / (float)((long long)gxl * gy);
   a.S = c.s_in;
   a.Sn = c.s_neg;
   a.upart = pa.upart;
@@ -1979,7 +2173,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   a.Wb = blk ? c.Wb : nullptr;
   a.blk_min = blk_min;
 
-  const dim3 grid(gx, gy, P);
+  const dim3 grid(gxl, gy, P);
   hipEvent_t e0 = c.ev_begin, e1 = c.ev_end;
   if (dma) {
     nmdlm_status rd = NMDLM_OK;
@@ -2009,7 +2203,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
       switch (RT) {
         case 1: rw = launch_words<1, 4>(grid, a, dyn, st, e0, e1); break;
         case 2: rw = launch_words<2, 4>(grid, a, dyn, st, e0, e1); break;
-        case 4: rw = launch_words<4, 4>(grid, a, dyn, st, e0, e1); break;
+        case 4: rw = launch_words<4, 4>(grid, a, dyn, st, e0, e1, wide); break;
         default: rw = launch_words<8, 4>(grid, a, dyn, st, e0, e1); break;
       }
     }

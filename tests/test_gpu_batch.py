@@ -57,7 +57,9 @@ def test_batched_block_step_matches_independent_sequences(n, C, M, d, H, F, flag
     (4, 512, 16, 1024, 16, 4096, 0, 4),     # full-size layer, four sequences
     (128, 40, 16, 128, 2, 256, 0, 4),       # 128 sequences: 8192 rows per product
     (3, 62, 6, 128, 2, 256, 6 << 20, 8),    # every word from the copies, T = 8
-], ids=["full-4seq", "128seq", "T8-forced"])
+    (128, 40, 16, 128, 2, 256, (7 << 20) | (4 << 16), 4),  # wide tiles, 8192 rows
+    (8, 64, 32, 192, 3, 320, (7 << 20) | (4 << 16), 2),    # wide tiles, T = 2 (32-token blocks)
+], ids=["full-4seq", "128seq", "T8-forced", "128seq-wide", "T2-wide"])
 def test_batched_step_with_blocked_weights(n, C, M, d, H, F, flags, T):
     _batched_matches_independent(n, C, M, d, H, F, flags, T, blocked=True)
 

@@ -131,11 +131,12 @@ def test_block_forced_paths(flags):
 
 
 @pytest.mark.parametrize("flags", [0, 6 << 20, (6 << 20) | (1 << 16), (6 << 20) | (2 << 8), 0x1,
-                                   3 << 20],
-                         ids=["auto", "blocked", "blocked-RT1", "blocked-P2", "dense", "rows"])
+                                   3 << 20, (7 << 20) | (4 << 16)],
+                         ids=["auto", "blocked", "blocked-RT1", "blocked-P2", "dense", "rows", "wide"])
 def test_block_with_blocked_weights(flags):
     # the layer also holds blocked weight copies: waves choose by their
-    # union (auto), every word from the copies (path 6), or the rows only
+    # union (auto), every word from the copies (path 6), wide tiles over the
+    # copies (path 7 with 64-row tiles), or the rows only
     need_gpu()
     _check_block(synth.block_case(), flags=flags, blocked=True)
     _check_block(synth.block_case(seed=23, C=70, M=37, d=192, H=3, F=320), flags=flags,

@@ -59,6 +59,7 @@ WORDS = 3 << 20       # single kernel over 64-channel words
 SCALAR = 5 << 20      # words, scalar gather-accumulate product
 DMA = 4 << 20         # as WORDS, active rows gathered into LDS
 BLOCKED = 6 << 20     # as WORDS, over the blocked weight copy
+WIDE = 7 << 20        # as BLOCKED, four column tiles per workgroup (64-row tiles)
 
 _FORCED = {
     "dense": 0x1, "P1": 1 << 8, "P2": 2 << 8, "P7": 7 << 8, "RT1": 1 << 16, "RT2": 2 << 16,
@@ -264,12 +265,44 @@ def test_blocked_automatic_at_many_rows(T, M, K, N, p):
     _check(case, blocked=True)
 
 
+WIDE_SHAPES = [  # T, M, K, N, density: 64-row tiles, column groups of four tiles
+    (4, 16, 64, 64, 0.2),        # one tile: three waves without a tile
+    (4, 40, 300, 70, 0.1),       # two row blocks (the second ragged), ragged K
+    (4, 33, 1000, 333, 0.05),    # six column tiles: one group and a ragged one
+    (2, 70, 129, 520, 0.1),      # T = 2: 32-token row blocks, nine column tiles
+    (1, 130, 65, 260, 0.3),      # T = 1: 64-token row blocks
+    (8, 20, 4096, 200, 0.02),    # T = 8, long K, sparse words skipped
+    (3, 50, 200, 1000, 0.1),     # T = 3: 21-token row blocks (one row unused)
+    (4, 64, 2048, 1024, 0.1),    # sixteen column tiles, 32 words
+]
+
+
+@pytest.mark.parametrize("flags", [WIDE, WIDE | (4 << 16), WIDE | 0x1],
+                         ids=["wide", "wide-RT4", "wide-dense"])
+@pytest.mark.parametrize("shape", WIDE_SHAPES, ids=[f"T{s[0]}M{s[1]}K{s[2]}N{s[3]}" for s in WIDE_SHAPES])
+def test_wide_ragged_shapes(shape, flags):
+    need_gpu()
+    T, M, K, N, p = shape
+    _check(synth.make_qbsm_case(300 + K + N, T, M, K, N, p), flags=flags, blocked=True)
+
+
+def test_wide_automatic_at_many_tiles():
+    # 8192 rows x 1024 columns: 2048 output tiles of 64 x 64 (wide from 1536)
+    need_gpu()
+    case = synth.make_qbsm_case(4242, 4, 2048, 200, 1024, 0.1)
+    _check(case, blocked=True)
+    case.S[:, :, 64:128] = False     # a word with no active row
+    _check(case, blocked=True)
+
+
 def test_blocked_degenerate_inputs():
     need_gpu()
     c = synth.make_qbsm_case(19, 4, 300, 256, 128, 0.1)
     c.S[:] = False
     _check(c, flags=BLOCKED, blocked=True)
     _check(c, blocked=True)
+    _check(c, flags=WIDE, blocked=True)
     c.S[:] = True
     _check(c, flags=BLOCKED, blocked=True)
     _check(c, blocked=True)
+    _check(c, flags=WIDE, blocked=True)
