@@ -950,11 +950,13 @@ __device__ void scalar_accumulate(const QbsmArgs& a, const uint32_t* sS, int lds
 // after it.
 // WIDE: a workgroup takes NW adjacent 64-column tiles of one row block, wave
 // j the tile NW x + j over every word of K (blocked copy only): the spike
-// staging, the union and the epilogue operands are shared by NW tiles, the
-// waves' accumulators need no reduction, and the tiles' epilogues run one
-// after the other over the LDS tile.
+// staging, the union and the epilogue operands are shared by NW tiles, and
+// each wave finishes its own tile from its accumulators (wide_epilogue).
+// Entry points aligned to 1 KB: with the default 256-byte placement the
+// twelve-layer step measured 0.8-1.5% slower, depending on where the code
+// object's other contents happened to put the kernels.
 template <int RT, int NW, bool TERN = false, bool BLK = false, bool SCA = false, bool WIDE = false>
-__global__ __launch_bounds__(NW * 64, (BLK && RT == 4 && NW == 4) ? 4 : 1)
+__global__ __launch_bounds__(NW * 64, (BLK && RT == 4 && NW == 4) ? 4 : 1) __attribute__((aligned(1024)))
 void k_qbsm_words(QbsmArgs a) {
   static_assert(!WIDE || (BLK && !TERN && !SCA && RT == 4 && NW == 4), "wide tiles: blocked, 64 rows");
   constexpr int ROWS = RT * 16;
@@ -1992,13 +1994,29 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     if (16 * RT < c.T || c.seq_len % ((16 * RT) / c.T) != 0) return NMDLM_ERR_UNSUPPORTED;
   }
   const bool tern = c.s_neg != nullptr;
+  // wide tiles (a workgroup takes four 64-column tiles of a 64-row block,
+  // each wave one tile over all of K, the IF in registers): requested by
+  // path 7, or unrequested for blocked products of many output tiles, where
+  // the one-tile kernel would repeat the staging, union and reduction of a
+  // row block for every column tile.  Decided before the LDS limits of the
+  // one-tile kernel: the wide variant holds no LDS tile and may take all of
+  // a CU's LDS.
+  bool wide = false;
+  if (c.Wb && !tern && (path == 0 || path == 7) && RT == 4 &&
+      ((c.flags >> NMDLM_SPLIT_SHIFT) & 0xFFu) <= 1u && (c.T == 1 || c.T == 2 || c.T == 4) &&
+      (c.mode == EPI_CUR || c.mode == EPI_IF || c.mode == EPI_QNL_IF || c.mode == EPI_HEAD) &&
+      words_lds(4, 4, Kw, false, true) <= kDmaLdsMax) {
+    const int mb4 = 64 / c.T;
+    const long long tiles4 = (long long)gx * ((c.M + mb4 - 1) / mb4);
+    wide = path == 7 || tiles4 >= kWideMinTiles;
+  }
   if (tern) {
     // ternary input: the word product only (both spike planes staged)
     path = 3;
     while (RT > 1 && words_lds(RT, 4, Kw, true) > kWordsLdsBudget && !rt_forced) RT >>= 1;
     if (words_lds(RT, 4, Kw, true) > kWordsLdsBudget || Kw > 256) return NMDLM_ERR_UNSUPPORTED;
   }
-  if (path == 0) {
+  if (path == 0 && !wide) {
     path = 3;
     while (RT > 1 && words_lds(RT, 4, Kw) > kWordsLdsBudget && !rt_forced) RT >>= 1;
     if (words_lds(RT, 4, Kw) > kWordsLdsBudget) path = 1;
@@ -2014,8 +2032,13 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   // 7: as 6 with wide tiles where the row tile is 64 rows
   bool blk = false;
   int blk_min = kBlockedMinRows;
-  const bool wide_req = path == 7;
-  if (path == 7) path = 6;
+  if (wide) {
+    blk = true;
+    blk_min = 0;
+    path = 3;
+  } else if (path == 7) {
+    path = 6;
+  }
   if (path == 6) {
     if (!c.Wb || tern) return NMDLM_ERR_UNSUPPORTED;
     blk = true;
@@ -2026,7 +2049,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   } else if (path_auto && path == 3 && c.Wb && !tern) {
     blk = true;
   }
-  if (path == 3 && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
+  if (path == 3 && !wide && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
@@ -2044,7 +2067,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   // 256 workgroups then share the weight rows instead of 64).  Elsewhere the
   // atomic accumulation costs more round trips than the split saves.
   int P = (int)((c.flags >> NMDLM_SPLIT_SHIFT) & 0xFFu);
-  if (P == 0 && path == 3 && !tern && tiles <= 64 && Kw >= 128) P = 4;
+  if (P == 0 && path == 3 && !tern && !wide && tiles <= 64 && Kw >= 128) P = 4;
   P = std::max(1, std::min(P, Kw));
   const size_t acc_elems = (size_t)16 * RT * 64 * (size_t)tiles;  // one accumulator tile per output tile
   if (P > 1 && (!scr.part || scr.part_elems < acc_elems)) P = 1;
@@ -2079,15 +2102,6 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     if (fused && !c.u_in && !dense && (long long)R * Kw > kUnionDirect) fused = false;
   }
 
-  // wide tiles (a workgroup takes four 64-column tiles of a 64-row block,
-  // each wave one tile over all of K): requested, or for blocked products of
-  // many output tiles, where the per-tile staging, union and reduction of
-  // the word kernel would be repeated by every column tile
-  bool wide = false;
-  if (words && blk && accum == 0 && P == 1 && RT == 4 && (c.T == 1 || c.T == 2 || c.T == 4) &&
-      (c.mode == EPI_CUR || c.mode == EPI_IF || c.mode == EPI_QNL_IF || c.mode == EPI_HEAD) &&
-      words_lds(4, 4, Kw, false, true) <= kWordsLdsBudget)
-    wide = wide_req || (path_auto && tiles >= kWideMinTiles);
   const int gxl = wide ? (gx + 3) / 4 : gx;  // grid columns
   if (wide) NW = 4;
 
