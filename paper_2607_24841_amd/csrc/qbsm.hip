@@ -340,6 +340,17 @@ __device__ __forceinline__ void reduce_tile(const v4i (&acc)[RT][4], int* sTile,
       }
 }
 
+// One wave's accumulators stored into the LDS tile (every entry of it).
+template <int RT>
+__device__ __forceinline__ void store_tile(const v4i (&acc)[RT][4], int* sTile, int g, int c) {
+#pragma unroll
+  for (int q = 0; q < RT; ++q)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sTile[(q * 16 + g * 4 + e) * kTileLd + v * 16 + c] = acc[q][v][e];
+}
+
 // K split across workgroups: every split adds its tile into the tile's
 // accumulator (int32, zero between products) with device-scope atomic adds
 // whose returned values are waited for, so that each add has been performed
@@ -962,8 +973,12 @@ void k_qbsm_words(QbsmArgs a) {
   constexpr int ROWS = RT * 16;
   constexpr int NT = NW * 64;
   constexpr int NE = WIDE ? NW : 1;  // column tiles (epilogue stages) per workgroup
+  // ALIAS (64-row tiles): the reduction tile takes the place of the spike
+  // rows, which are dead once the word loop is done, so that long-K tiles
+  // keep four workgroups per CU (the host sizes the dynamic LDS for both)
+  constexpr bool ALIAS = RT == 4 && !WIDE && !SCA;
   // WIDE: the waves' 1 KB spike-word exchanges in place of the LDS tile
-  __shared__ int sTile[WIDE ? NW * 256 : ROWS * kTileLd];
+  __shared__ int sTileS[WIDE ? NW * 256 : (ALIAS ? 1 : ROWS * kTileLd)];
   __shared__ unsigned long long sUn[NW];
   __shared__ EpiStage ep[NE];
   __shared__ int sLast;
@@ -983,6 +998,7 @@ void k_qbsm_words(QbsmArgs a) {
   unsigned long long* sLU = sDyn;
   unsigned long long* sStat = sDyn + Kw;
   uint32_t* sS = reinterpret_cast<uint32_t*>(sDyn + 2 * Kw);
+  int* const sTile = ALIAS ? reinterpret_cast<int*>(sDyn + 2 * Kw) : sTileS;
   // ternary input: the -1 spike rows follow the +1 rows, same layout
   uint32_t* sSn = sS + ROWS * lds_row;
   const bool stats_wg = a.stats && x == 0 && y == 0 && z == 0;  // workgroup-uniform
@@ -1058,7 +1074,7 @@ void k_qbsm_words(QbsmArgs a) {
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- staging, store phase
-  if constexpr (!WIDE)
+  if constexpr (!WIDE && !ALIAS)
     for (int i = tid; i < ROWS * kTileLd; i += NT) sTile[i] = 0;
   epi_store<NT>(a, ep[0], er, tid, WIDE ? min(x * NW, gx - 1) : x, y);
   if constexpr (WIDE) {
@@ -1285,7 +1301,14 @@ void k_qbsm_words(QbsmArgs a) {
   if (scalar) scalar_accumulate<ROWS, NT>(a, sS, lds_row, sTile, tid, x, y, w0, w1);
 
   __syncthreads();
-  if (!scalar && !WIDE) reduce_tile<RT>(acc, sTile, g, c);
+  if constexpr (ALIAS) {
+    // the tile over the spike rows: wave 0 stores its sums, the others add
+    if (wave == 0) store_tile<RT>(acc, sTile, g, c);
+    __syncthreads();
+    if (wave != 0) reduce_tile<RT>(acc, sTile, g, c);
+  } else if (!scalar && !WIDE) {
+    reduce_tile<RT>(acc, sTile, g, c);
+  }
   if (stats_wg) stats_count<NT>(a, from_parts ? sLU : sStat, &sStatCnt, Kw, tid, lane);
   __syncthreads();
   if (stats_wg && tid == 0) stats_write(a, sStatCnt);
@@ -1910,10 +1933,20 @@ nmdlm_status launch_weight_block(const int8_t* W, int K, int N, int64_t ldw, int
 }
 
 // Static LDS of k_qbsm_words<RT, NW> and its dynamic part (mirror the declarations).
-static size_t words_lds(int RT, int NW, int Kw, bool tern = false, bool wide = false) {
-  return (wide ? (size_t)NW * 1024 : (size_t)RT * 16 * kTileLd * 4) + (size_t)NW * 12 +
-         sizeof(EpiStage) * (wide ? NW : 1) + 64 +
-         (size_t)Kw * 16 + (size_t)RT * 16 * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
+// 64-row tiles of the one-tile kernel (not the scalar variant) keep the
+// reduction tile in the dynamic part, over the spike rows.
+static bool words_alias(int RT, bool wide, bool sca) { return RT == 4 && !wide && !sca; }
+static size_t words_dyn(int RT, int Kw, bool tern = false, bool wide = false, bool sca = false) {
+  const size_t rows = (size_t)RT * 16 * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
+  const size_t tile = (size_t)RT * 16 * kTileLd * 4;
+  return (size_t)Kw * 16 + (words_alias(RT, wide, sca) ? std::max(rows, tile) : rows);
+}
+static size_t words_lds(int RT, int NW, int Kw, bool tern = false, bool wide = false,
+                        bool sca = false) {
+  const size_t tile = wide ? (size_t)NW * 1024
+                           : (words_alias(RT, wide, sca) ? 4 : (size_t)RT * 16 * kTileLd * 4);
+  return tile + (size_t)NW * 12 + sizeof(EpiStage) * (wide ? NW : 1) + 64 +
+         words_dyn(RT, Kw, tern, wide, sca);
 }
 
 // Static LDS of k_qbsm_fused<RT, NW> (mirrors its declarations).
@@ -2049,7 +2082,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   } else if (path_auto && path == 3 && c.Wb && !tern) {
     blk = true;
   }
-  if (path == 3 && !wide && words_lds(RT, 4, Kw, tern) > kWordsLdsBudget) path = 1;
+  if (path == 3 && !wide && words_lds(RT, 4, Kw, tern, false, accum == 1) > kWordsLdsBudget) path = 1;
   if (path == 4 && dma_lds(RT, 4, 4, Kw) > kDmaLdsMax) path = 1;
   if (path > 4) path = 1;
   if (16 * RT < c.T) return NMDLM_ERR_UNSUPPORTED;
@@ -2090,7 +2123,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
     NW = words_waves(RT, ks_per_wg);
     if (words_lds(RT, NW, Kw) > kWordsLdsBudget) NW = 4;
     if (words_lds(RT, NW, Kw, tern) > kWordsLdsBudget) NW = 4;
-    dyn = (size_t)Kw * 16 + (size_t)16 * RT * (2 * Kw + 1) * 4 * (tern ? 2 : 1);
+    dyn = words_dyn(RT, Kw, tern, wide, accum == 1);
   } else if (path == 2) {
     // one kernel (union, list and spike compaction in LDS) when the tile's
     // spike rows fit; else the prep pass builds them in global memory
