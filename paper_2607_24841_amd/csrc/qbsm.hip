@@ -1767,7 +1767,9 @@ __global__ __launch_bounds__(NW * 64) void k_qbsm_list(QbsmArgs a) {
 constexpr size_t kWordsLdsBudget = 81920;  // word product: two workgroups per CU fit in LDS
 constexpr int kWideMinTiles = 1536;  // output tiles (64 x 64) from which blocked products go wide
 constexpr int kCus = 256;            // compute units of the device
-constexpr int kThreadsPerCu = 2048;  // resident threads per compute unit
+// resident threads per compute unit of the word kernel: its variants take
+// 74-128 registers, four or five waves per SIMD, 16-20 waves per CU
+constexpr int kThreadsPerCu = 1024;
 
 // Waves per workgroup of the word product: 16 for one row group with more
 // than 32 words of K, 8 for up to two row groups with 8 or more, else 4.
@@ -1975,7 +1977,7 @@ nmdlm_status launch_qbsm(const QbsmCall& c, const QbsmScratch& scr, hipStream_t 
   const bool rt_forced = (RT == 1 || RT == 2 || RT == 4 || RT == 8);
   if (!rt_forced) {
     // rows per tile group (at most 4): the largest that gives >= 512
-    // workgroups all resident at once (256 CUs x 2048 threads), else >= 256
+    // workgroups all resident at once (256 CUs x 1024 threads), else >= 256
     // resident, else 1 (the most row blocks; they re-read weights from L2)
     RT = 1;
     bool found = false;
