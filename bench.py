@@ -89,10 +89,10 @@ def parse():
 # A value holds only for the product-kernel sources with the recorded digest:
 # any change to them reports null until the counters are taken again.
 TRAFFIC = {
-    "block": {"sources_sha256": "67b91cd72428097db4653d7a6d62c3e739ca8cb2e56092b7957c2c57403459d5",
-              "bytes_per_launch": 2631235.6},
-    "mdlm12": {"sources_sha256": "03343e123121d74e91761a9229d6bff32a85f2108d08dcd102dbfc831c5ff904",
-               "bytes_per_launch": 14220054.2},
+    "block": {"sources_sha256": "09ea33426a5d079863fa361ea3ac0d4a094c0fcad9a1c38eb0c59c4d6999a299",
+              "bytes_per_launch": 2773553.6},
+    "mdlm12": {"sources_sha256": "09ea33426a5d079863fa361ea3ac0d4a094c0fcad9a1c38eb0c59c4d6999a299",
+               "bytes_per_launch": 14211565.7},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 
@@ -248,6 +248,11 @@ def bench_ffn_sweep(args):
     n_copies = 4                       # 4 x (58.7 + 58.7) MB > 256 MB last-level cache
     W_up = [torch.from_numpy(ffn.W_up).cuda() for _ in range(n_copies)]
     W_dn = [torch.from_numpy(ffn.W_dn).cuda() for _ in range(n_copies)]
+    blocked = args.weights == "blocked"
+    # blocked operand-order copies beside the row-major weights (each wave of
+    # a product reads the copy or the rows by its union)
+    Wb_up = [B.blocked_weights(w, d, F, F) for w in W_up] if blocked else None
+    Wb_dn = [B.blocked_weights(w, F, d, d) for w in W_dn] if blocked else None
     th_up, th_dn = int(ffn.theta_up), int(ffn.theta_dn)
     points = []
     for iB in range(len(synth.FFN_SWEEP_BLOCKS)):
@@ -263,12 +268,20 @@ def bench_ffn_sweep(args):
                                  B.nmdlm_qbsm_workspace_size(T, Bk, F, d)))
 
             def up(c):
-                B.nmdlm_qbsm(xu, T, Bk, d, W_up[c], F, F, theta=th_up, s_out=su, stats=st[0],
-                             flags=args.flags, ws=ws)
+                if blocked:
+                    B.nmdlm_qbsm_blocked(xu, T, Bk, d, W_up[c], Wb_up[c], F, F, theta=th_up,
+                                         s_out=su, stats=st[0], flags=args.flags, ws=ws)
+                else:
+                    B.nmdlm_qbsm(xu, T, Bk, d, W_up[c], F, F, theta=th_up, s_out=su, stats=st[0],
+                                 flags=args.flags, ws=ws)
 
             def dn(c):
-                B.nmdlm_qbsm(xd, T, Bk, F, W_dn[c], d, d, theta=th_dn, s_out=sd, stats=st[1],
-                             flags=args.flags, ws=ws)
+                if blocked:
+                    B.nmdlm_qbsm_blocked(xd, T, Bk, F, W_dn[c], Wb_dn[c], d, d, theta=th_dn,
+                                         s_out=sd, stats=st[1], flags=args.flags, ws=ws)
+                else:
+                    B.nmdlm_qbsm(xd, T, Bk, F, W_dn[c], d, d, theta=th_dn, s_out=sd, stats=st[1],
+                                 flags=args.flags, ws=ws)
 
             if args.eager:           # one dispatch per launch (for counter passes)
                 t_up = _time_eager(lambda: [up(c) for c in range(n_copies)], args.reps) / n_copies
@@ -320,7 +333,7 @@ def bench_ffn_sweep(args):
         "data": "synthetic",
         "config": {"workload": "FFN weight-traffic sweep d=4096->14336->4096, T=4, "
                                "Beta(0.5,8) per-neuron rates; value at B=64, density 0.30",
-                   "weight_copies_rotated": n_copies,
+                   "weight_copies_rotated": n_copies, "weights": args.weights,
                    "issue": "eager" if args.eager else "hip_graph"},
         "weight_skip_fraction": 1.0 - (head["up"]["touched_bytes"] + head["dn"]["touched_bytes"])
         / (head["up"]["k_total"] * F + head["dn"]["k_total"] * d),
