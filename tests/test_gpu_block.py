@@ -186,6 +186,46 @@ def test_mdlm_step_with_head():
     assert np.array_equal(msk.cpu().numpy().astype(bool), ref.masked)
 
 
+def test_mdlm_step_with_head_wide_tiles():
+    # the model holds blocked copies and every product of the prefill and of
+    # the step, the head's logits included, takes wide tiles (path 7 with
+    # 64-row tiles: 16 block tokens x 4 steps fill one 64-row block)
+    torch, B = need_gpu()
+    m = _tiny(seed=35)
+    emb = O.unpack_model_emb(m)
+    P, M, k = 20, 16, 5
+    flags = (7 << 20) | (4 << 16)
+    prompt = synth.random_tokens(5, P, m.V)
+    rng = np.random.default_rng(36)
+    msk0 = rng.random(M) < 0.7
+    tok0 = np.where(msk0, 0, rng.integers(1, m.V, M)).astype(np.int32)
+    kc, vc = O.new_caches(m.n_layers, m.T, P + M, m.d)
+    O.prefill(O.block_input(prompt, np.arange(P), emb, m.pos_ch), m.layers, kc, vc)
+    ref = O.block_step(m, emb, tok0, msk0, P, P, kc, vc, k)
+    dm = B.DeviceModel.from_mdlm(m, P + M, blocked=True)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, P, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, 0)))
+    pr = torch.from_numpy(prompt.astype(np.int32)).cuda()
+    B.nmdlm_block_step(dm, B.step_io(P, 0, flags=B.NMDLM_NO_HEAD | flags, tokens=pr,
+                                     masked=torch.zeros(P, dtype=torch.uint8, device="cuda")), ws)
+    tok = torch.from_numpy(tok0).cuda()
+    msk = torch.from_numpy(msk0.astype(np.uint8)).cuda()
+    logits = torch.empty((M, m.V), dtype=torch.float32, device="cuda")
+    pred = torch.empty(M, dtype=torch.int32, device="cuda")
+    conf = torch.empty(M, dtype=torch.float64, device="cuda")
+    chosen = torch.empty(k, dtype=torch.int32, device="cuda")
+    B.nmdlm_block_step(dm, B.step_io(M, P, pos0=P, flags=flags, tokens=tok, masked=msk,
+                                     k_unmask=k, logits=logits, pred=pred, conf=conf,
+                                     unmasked_pos=chosen), ws)
+    torch.cuda.synchronize()
+    assert_same(logits.cpu().numpy(), ref.logits, 'logits')          # exact fp32
+    assert_same(pred.cpu().numpy(), ref.pred, 'pred')
+    assert np.allclose(conf.cpu().numpy(), ref.conf, rtol=1e-12, atol=0)
+    assert np.array_equal(chosen.cpu().numpy(), ref.chosen)
+    assert np.array_equal(tok.cpu().numpy(), ref.tokens)
+    assert np.array_equal(msk.cpu().numpy().astype(bool), ref.masked)
+
+
 def test_mdlm_generation_matches_oracle():
     need_gpu()
     from paper_2607_24841_amd import binding as B

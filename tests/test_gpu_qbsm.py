@@ -286,6 +286,18 @@ def test_wide_ragged_shapes(shape, flags):
     _check(synth.make_qbsm_case(300 + K + N, T, M, K, N, p), flags=flags, blocked=True)
 
 
+@pytest.mark.parametrize("flags", [WIDE, WIDE | (4 << 16)], ids=["wide", "wide-RT4"])
+def test_wide_currents_only(flags):
+    # no threshold: the currents alone, stored from the accumulators
+    need_gpu()
+    case = synth.make_qbsm_case(77, 2, 70, 300, 600, 0.1)
+    I_ref = O.qbsm(case.S, case.W, case.bias)
+    cur, spk, st, _, _ = run_qbsm(case.S, case.W, case.bias, flags=flags, blocked=True)
+    assert spk is None
+    assert_same(cur, I_ref)
+    assert st["k_active"] == O.active_rows(case.S).size
+
+
 def test_wide_automatic_at_many_tiles():
     # 8192 rows x 1024 columns: 2048 output tiles of 64 x 64 (wide from 1536)
     need_gpu()
