@@ -23,11 +23,23 @@ __device__ __forceinline__ int lut_dword(const uint8_t* __restrict__ lut, int la
                ((uint32_t)b[3] << 24));
 }
 
-// floor(256 * num / den) for num >= 0, den > 0 (0 when den = 0).  For fewer
-// than 65536 keys, 256 * num < 2^32 and the division is done in 32 bits.
+// floor(256 * num / den) for 0 <= num <= den (0 when den = 0).  For fewer
+// than 65536 keys, a = 256 num < 2^32 and den < 2^24: the quotient (at most
+// 256) is estimated as a float product with the hardware reciprocal, whose
+// relative error (a few units of 2^-24) keeps the estimate within one of
+// the exact floor, and one remainder test corrects it (the remainder
+// a - q den lies in (-2 den, 2 den), exact in wrapped 32-bit arithmetic).
+// Larger key counts divide in 64 bits.
 __device__ __forceinline__ int32_t attn_norm(long long num, long long den, bool small) {
   if (den <= 0) return 0;
-  if (small) return (int32_t)((256u * (uint32_t)num) / (uint32_t)den);
+  if (small) {
+    const uint32_t a = 256u * (uint32_t)num, b = (uint32_t)den;
+    uint32_t q = (uint32_t)((float)a * __builtin_amdgcn_rcpf((float)b));
+    const int32_t r = (int32_t)(a - q * b);
+    if (r < 0) --q;
+    else if ((uint32_t)r >= b) ++q;
+    return (int32_t)q;
+  }
   return (int32_t)((256LL * num) / den);
 }
 
@@ -52,6 +64,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   __shared__ int sNum[16][DH];
   __shared__ int sDen[16];
   __shared__ int sCnt[DH];
+  __shared__ uint64_t sKey[NW][64 * DHW];  // each wave's chunk of key rows
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -90,27 +103,30 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   int den = 0;
   // rows of queries past M (clamped loads) are scored too; they are never read
 
+  uint64_t* const sK = sKey[wave];
   for (int jc = wave; jc < nch; jc += NW) {  // wave-uniform
     const int j0 = jc * 64 + 16 * g;
-    // keys past C+M read a valid row (clamped) and are masked when scored
-    uint64_t kw[16][DHW];
+    // lane l loads key row jc*64 + l (rows past C+M read a valid row, masked
+    // when scored) and the chunk's rows meet in the wave's LDS buffer
+    const uint64_t* kr = kc + ((size_t)t * cap + min(jc * 64 + lane, J - 1)) * dw + h * DHW;
+    uint64_t kl[DHW];
 #pragma unroll
-    for (int s = 0; s < 16; ++s) {
-      const int jj = min(j0 + s, J - 1);
-      const uint64_t* kr = kc + ((size_t)t * cap + jj) * dw + h * DHW;
-#pragma unroll
-      for (int w = 0; w < DHW; ++w) kw[s][w] = kr[w];
-    }
+    for (int w = 0; w < DHW; ++w) kl[w] = kr[w];
     uint64_t vw[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) vw[nt] = vt[((size_t)t * capw + jc) * d + h * DH + nt * 16 + c];
     __builtin_amdgcn_sched_barrier(0);  // every load above is issued before the first use
+#pragma unroll
+    for (int w = 0; w < DHW; ++w) sK[lane * DHW + w] = kl[w];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     uint32_t pk[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
       int sc = 0;
 #pragma unroll
-      for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & kw[s][w]);
+      for (int w = 0; w < DHW; ++w) sc += __popcll(qw[w] & sK[(16 * g + s) * DHW + w]);
       const bool jv = j0 + s < J;
       const int pw = __builtin_amdgcn_ds_bpermute((sc >> 2) << 2, lut_dw);
       const int p = jv ? (pw >> ((sc & 3) * 8)) & 0xFF : 0;
@@ -128,6 +144,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
                          (int)expand4_a((bits >> 8) & 0xFu), (int)expand4_a(bits >> 12)};
       acc[nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf, acc[nt], 0, 0, 0);
     }
+    __builtin_amdgcn_wave_barrier();  // the buffer's reads precede the next chunk's stores
   }
   __syncthreads();  // the partial sums are cleared
   if (wave < nch) {  // wave-uniform
