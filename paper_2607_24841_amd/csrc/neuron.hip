@@ -17,10 +17,11 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
                                             uint64_t* __restrict__ s_out,
                                             uint64_t* __restrict__ u_out) {
   const int Nw = (N + 63) / 64;
-  const long long unit = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (unit >= (long long)M * Nw) return;  // wave-uniform
+  // M * Nw <= 2^19 * 1024 units: 32-bit, wave-uniform (scalar) arithmetic
+  const int unit = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + ((int)threadIdx.x >> 6));
+  if (unit >= M * Nw) return;  // wave-uniform
   const int lane = threadIdx.x & 63;
-  const int m = (int)(unit / Nw), w = (int)(unit % Nw);
+  const int m = unit / Nw, w = unit - m * Nw;
   const int n = w * 64 + lane;
   const bool nv = n < N;
   const int nc = nv ? n : N - 1;  // lanes past N read a valid current and drop it
