@@ -298,6 +298,20 @@ def test_wide_currents_only(flags):
     assert st["k_active"] == O.active_rows(case.S).size
 
 
+@pytest.mark.parametrize("flags,blocked", [
+    (WORDS | (4 << 16) | (2 << 8), False),     # 64-row tiles, K split two ways
+    (WORDS | (4 << 16) | (3 << 8), False),     # three ways (ragged split)
+    (BLOCKED | (4 << 16) | (2 << 8), True),    # the same over the blocked copy
+    (DMA | (4 << 16), False),                  # the LDS-streamed kernel keeps its own tile
+], ids=["rows-RT4-P2", "rows-RT4-P3", "blocked-RT4-P2", "dma-RT4"])
+def test_tall_tiles_with_k_split(flags, blocked):
+    # 64-row tiles reduce into an LDS tile laid over the spike rows; with a K
+    # split the last arriving workgroup reads the accumulated tile from there
+    need_gpu()
+    _check(synth.make_qbsm_case(501, 4, 37, 1100, 333, 0.05), flags=flags, blocked=blocked)
+    _check(synth.make_qbsm_case(502, 2, 70, 4100, 130, 0.02), flags=flags, blocked=blocked)
+
+
 def test_wide_automatic_at_many_tiles():
     # 8192 rows x 1024 columns: 2048 output tiles of 64 x 64 (wide from 1536)
     need_gpu()
