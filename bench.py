@@ -89,10 +89,10 @@ def parse():
 # A value holds only for the product-kernel sources with the recorded digest:
 # any change to them reports null until the counters are taken again.
 TRAFFIC = {
-    "block": {"sources_sha256": "09ea33426a5d079863fa361ea3ac0d4a094c0fcad9a1c38eb0c59c4d6999a299",
+    "block": {"sources_sha256": "fc86da0ff2f80f4b93457c5fe8375e7be50dccbc03ec8dba1b5897440c3dd954",
               "bytes_per_launch": 2773553.6},
-    "mdlm12": {"sources_sha256": "09ea33426a5d079863fa361ea3ac0d4a094c0fcad9a1c38eb0c59c4d6999a299",
-               "bytes_per_launch": 14211565.7},
+    "mdlm12": {"sources_sha256": "fc86da0ff2f80f4b93457c5fe8375e7be50dccbc03ec8dba1b5897440c3dd954",
+               "bytes_per_launch": 14211689.4},
 }
 PRODUCT_SOURCES = ("paper_2607_24841_amd/csrc/qbsm.hip", "paper_2607_24841_amd/csrc/common.h")
 

@@ -1027,7 +1027,6 @@ void k_qbsm_words(QbsmArgs a) {
   const float inv_kw = a.inv_kw, inv_mb = a.inv_mb;
   const int r0 = div_small(tid, inv_kw), wq = tid - r0 * Kw;
   const int rpp = div_small(NT, inv_kw);
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr0 = __builtin_amdgcn_readfirstlane(r0);  // first row of this wave's lanes
   // partial unions: part s = r0 + k * rpp of word wq
   const int slices = rpp;
