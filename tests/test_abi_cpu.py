@@ -157,6 +157,12 @@ def test_block_step_argument_errors(lib):
     forced_head = B.step_io(16, 512, flags=B.NMDLM_PATH_BLOCKED, x_in=FAKE, tokens=FAKE,
                             masked=FAKE, k_unmask=4)
     assert call(mc, forced_head) == B.NMDLM_ERR_INVALID_ARG       # head copy missing
+    # path 7 (wide tiles over the copies) needs them the same way
+    wide = B.step_io(16, 512, flags=B.NMDLM_NO_HEAD | B.NMDLM_PATH_WIDE, x_in=FAKE)
+    assert call(m, wide) == B.NMDLM_ERR_INVALID_ARG
+    wide_head = B.step_io(16, 512, flags=B.NMDLM_PATH_WIDE, x_in=FAKE, tokens=FAKE,
+                          masked=FAKE, k_unmask=4)
+    assert call(mc, wide_head) == B.NMDLM_ERR_INVALID_ARG
 
 
 def test_batched_step_argument_errors(lib):
