@@ -65,6 +65,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   __shared__ int sDen[16];
   __shared__ int sCnt[DH];
   __shared__ uint64_t sKey[NW][64 * DHW];  // each wave's chunk of key rows
+  __shared__ uint64_t sVal[NW][DH];        // and its value words, one per channel
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -104,6 +105,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
   // rows of queries past M (clamped loads) are scored too; they are never read
 
   uint64_t* const sK = sKey[wave];
+  uint64_t* const sV = sVal[wave];
   for (int jc = wave; jc < nch; jc += NW) {  // wave-uniform
     const int j0 = jc * 64 + 16 * g;
     // lane l loads key row jc*64 + l (rows past C+M read a valid row, masked
@@ -112,12 +114,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
     uint64_t kl[DHW];
 #pragma unroll
     for (int w = 0; w < DHW; ++w) kl[w] = kr[w];
-    uint64_t vw[NT];
+    // lane l loads the chunk's value words of channels l, l + 64, ...
+    uint64_t vl[DHW];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) vw[nt] = vt[((size_t)t * capw + jc) * d + h * DH + nt * 16 + c];
+    for (int w = 0; w < DHW; ++w) vl[w] = vt[((size_t)t * capw + jc) * d + h * DH + w * 64 + lane];
     __builtin_amdgcn_sched_barrier(0);  // every load above is issued before the first use
 #pragma unroll
-    for (int w = 0; w < DHW; ++w) sK[lane * DHW + w] = kl[w];
+    for (int w = 0; w < DHW; ++w) {
+      sK[lane * DHW + w] = kl[w];
+      sV[w * 64 + lane] = vl[w];
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -138,13 +144,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn(const uint64_t* __restrict__ q
     const uint32_t vmask = nvalid >= 16 ? 0xFFFFu : (nvalid <= 0 ? 0u : ((1u << nvalid) - 1u));
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint32_t bits = (uint32_t)(vw[nt] >> (16 * g)) & vmask;
+      const uint32_t bits = (uint32_t)(sV[nt * 16 + c] >> (16 * g)) & vmask;
       cnt[nt] += __popc(bits);
       const v4i bf = v4i{(int)expand4_a(bits & 0xFu), (int)expand4_a((bits >> 4) & 0xFu),
                          (int)expand4_a((bits >> 8) & 0xFu), (int)expand4_a(bits >> 12)};
       acc[nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf, acc[nt], 0, 0, 0);
     }
-    __builtin_amdgcn_wave_barrier();  // the buffer's reads precede the next chunk's stores
+    __builtin_amdgcn_wave_barrier();  // the buffers' reads precede the next chunk's stores
   }
   __syncthreads();  // the partial sums are cleared
   if (wave < nch) {  // wave-uniform
