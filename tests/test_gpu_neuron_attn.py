@@ -130,6 +130,10 @@ ATTN = [  # T, M, C, H, dh, p
     (4, 192, 64, 8, 64, 0.3),
     (4, 300, 40, 8, 64, 0.25),
     (4, 520, 30, 4, 128, 0.3),
+    # dh = 128, several key chunks per wave: 12 waves with five or six chunks
+    # each, 8 waves with two or three
+    (4, 32, 4000, 16, 128, 0.3),
+    (4, 80, 1000, 16, 128, 0.3),
     # 65564 keys: the normalisation's 64-bit path (256 * num beyond 32 bits)
     (1, 4, 65560, 1, 64, 0.5),
 ]
