@@ -75,8 +75,10 @@ def parse():
                    help="extra block-step flags (path overrides; results do not change)")
     p.add_argument("--workload", default="mdlm12-step",
                    choices=("mdlm12-step", "block", "ffn-sweep", "mdlm24-generate",
-                            "e2d2-generate", "ternary-ffn", "block-batch"),
+                            "e2d2-generate", "ternary-ffn", "block-batch", "tp-shard"),
                    help="mdlm12-step: the 12-layer MDLM at one block step (default)")
+    p.add_argument("--tp", type=int, default=8,
+                   help="tp-shard: GPUs the 12-layer step's columns and heads are split over")
     p.add_argument("--reps", type=int, default=20,
                    help="timed repetitions (ffn-sweep, mdlm12-step)")
     return p.parse_args()
@@ -178,7 +180,7 @@ def main():
     {"block": bench_block, "ffn-sweep": bench_ffn_sweep, "mdlm12-step": bench_mdlm12_step,
      "mdlm24-generate": bench_mdlm24_generate,
      "e2d2-generate": bench_e2d2_generate, "ternary-ffn": bench_ternary_ffn,
-     "block-batch": bench_block_batch}[args.workload](args)
+     "block-batch": bench_block_batch, "tp-shard": bench_tp_shard}[args.workload](args)
 
 
 def _graph(fn):
@@ -571,6 +573,127 @@ def bench_mdlm12_step(args):
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_mdlm12(case, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def _spikes_with_union(rng, T, M, K, k_active, fill):
+    """Spikes bool [T][M][K] whose block union is exactly k_active input
+    neurons: each chosen neuron spikes at one random (t, m) and with
+    probability `fill` at the others."""
+    import numpy as np
+    S = np.zeros((T, M, K), dtype=bool)
+    rows = rng.choice(K, k_active, replace=False)
+    S[:, :, rows] = rng.random((T, M, k_active)) < fill
+    S[rng.integers(0, T, k_active), rng.integers(0, M, k_active), rows] = True
+    return S
+
+
+def bench_tp_shard(args):
+    """One GPU's share of the 12-layer block step split over --tp GPUs by
+    output columns (every product) and by heads (attention): the shard-shape
+    kernels of all layers and the head's vocabulary slice, chained in one HIP
+    graph.  The collectives between them (four spike all-gathers per layer
+    and the confidence combine) are not run on one GPU; their count and
+    payloads are reported.  Union sizes come from one full step of the
+    12-layer model, inputs with exactly those unions from a seeded generator."""
+    import numpy as np
+    import torch
+
+    from paper_2607_24841_amd import binding as B
+    from workloads import synth
+
+    B.load()
+    g = args.tp
+    case = synth.mdlm12_step_case()
+    m = case.model
+    C, M, k = case.C, case.B, case.k_unmask
+    T, d, H, F, V = m.T, m.d, m.H, m.F, m.V
+    if g < 1 or H % g or d % (64 * g) or F % (64 * g):
+        print(f"tp-shard: {g} does not divide the heads ({H}) and 64-column tiles", file=sys.stderr)
+        sys.exit(2)
+    # union sizes of every product: one full step (prefill untimed)
+    dm = B.DeviceModel.from_mdlm(m, C + M, blocked=True)
+    ws = B.workspace(max(B.nmdlm_block_step_workspace_size(dm, C, B.NMDLM_NO_HEAD),
+                         B.nmdlm_block_step_workspace_size(dm, M, 0)))
+    ctx = torch.from_numpy(case.ctx_tokens.astype(np.int32)).cuda()
+    B.nmdlm_block_step(dm, B.step_io(C, 0, flags=B.NMDLM_NO_HEAD, tokens=ctx,
+                                     masked=torch.zeros(C, dtype=torch.uint8, device="cuda")), ws)
+    io, b = _mdlm_step_io(B, torch, m, C, M, k, 0)
+    B.nmdlm_block_step(dm, io, ws)
+    torch.cuda.synchronize()
+    kact = b["stats"].cpu().numpy()[:, 1].astype(int)
+    del dm, ws, io, b, ctx
+    torch.cuda.empty_cache()
+
+    rng = np.random.default_rng(args.seed)
+    dh, Hs, ds = d // H, H // g, d // g
+    cap = (C + M + 63) // 64 * 64
+    dims = (("qkv", d, 3 * ds), ("o", d, ds), ("up", d, F // g), ("down", F, ds))
+    lut = torch.from_numpy(synth.sorted_lut_u8(synth.stream(args.seed, 7))).cuda()
+    calls = []      # (kind, zero-argument launcher)
+    keep = []       # device buffers the launchers use
+
+    def product(kind, K, N, ka):
+        W = torch.randint(-127, 128, (K, N), dtype=torch.int8, device="cuda")
+        Wb = B.blocked_weights(W, K, N, N)
+        s_in = B.to_dev_bits(synth.pack_bits(_spikes_with_union(rng, T, M, K, ka, 0.3)))
+        out = torch.empty((T, M, (N + 63) // 64), dtype=torch.int64, device="cuda")
+        pws = B.workspace(B.nmdlm_qbsm_workspace_size(T, M, K, N))
+        keep.extend((W, Wb, s_in, out, pws))
+        calls.append((kind, lambda: B.nmdlm_qbsm_blocked(s_in, T, M, K, W, Wb, N, N, theta=300,
+                                                          s_out=out, ws=pws)))
+
+    for l in range(m.n_layers):
+        for p, (nm, K, N) in enumerate(dims):
+            product(nm, K, N, int(kact[4 * l + p]))
+            if nm == "qkv":      # this GPU's heads over the full context
+                q = B.to_dev_bits(synth.pack_bits(rng.random((T, M, ds)) < 0.45))
+                kc = B.to_dev_bits(synth.pack_bits(rng.random((T, cap, ds)) < 0.45))
+                vw = synth.pack_bits(rng.random((T, ds, cap)) < 0.45)          # [T][ds][cap/64]
+                vt = B.to_dev_bits(np.ascontiguousarray(vw.transpose(0, 2, 1)))
+                a = torch.empty((T, M, ds), dtype=torch.int32, device="cuda")
+                sa = torch.empty((T, M, ds // 64), dtype=torch.int64, device="cuda")
+                keep.extend((q, kc, vt, a, sa))
+                calls.append(("attn", lambda q=q, kc=kc, vt=vt, a=a, sa=sa: B.nmdlm_bbm_attn(
+                    q, kc, vt, cap, T, M, C, Hs, dh, lut, a_out=a, theta_a=300, s_out=sa)))
+    # the vocabulary split in whole 64-column tiles (the last GPU's slice padded)
+    Vs = (V + 64 * g - 1) // (64 * g) * 64
+    product("head", d, Vs, int(kact[-1]))
+
+    def run_all():
+        for _, fn in calls:
+            fn()
+    gr = _graph(run_all)
+    ms = _time_graph(gr, args.reps)
+    # each kind alone: its calls back to back in a graph of their own, the
+    # head's repeated 12 times so that the graph launch is amortised alike
+    per_kind = {}
+    for kind in ("qkv", "attn", "o", "up", "down", "head"):
+        fns = [fn for kd, fn in calls if kd == kind]
+        fns = fns * max(1, m.n_layers // len(fns))
+        gk = _graph(lambda fns=fns: [fn() for fn in fns])
+        per_kind[kind] = {"calls_per_step": len(fns) if kind != "head" else 1,
+                          "us_per_call": 1e3 * _time_graph(gk, args.reps) / len(fns)}
+        del gk
+    gather_bytes = [T * M * d // 8, T * M * d // 8, T * M * F // 8, T * M * d // 8]
+    out = {
+        "metric": "per-GPU kernel time of a tensor-parallel shard of the block step",
+        "value": ms, "unit": "ms", "n_gpus": 1, "steps": args.reps, "warmup": 1,
+        "ms_per_step": ms, "higher_is_better": False, "scaling": "strong", "vs_baseline": None,
+        "dtype": "int8", "data": "synthetic",
+        "config": {"workload": f"the 12-layer block step (d=2048, 16 heads x 128, FFN 8192, vocab "
+                               f"32000, T=4, 32 block tokens over 1024 context tokens) as one of "
+                               f"{g} GPUs: every product over {1}/{g} of its output columns, "
+                               f"attention over {Hs} heads, the head over {Vs} vocabulary "
+                               f"entries (product with IF output standing in for the logits "
+                               f"epilogue); collectives not run",
+                   "tp": g, "issue": "hip_graph", "weights": "blocked"},
+        "per_kind": per_kind,
+        "collectives_per_step": {"spike_all_gathers": 4 * m.n_layers,
+                                 "all_gather_bytes_per_layer": gather_bytes,
+                                 "confidence_combines": 1},
+        "one_gpu_union_sizes": kact.tolist(),
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -22,7 +22,7 @@ def test_more_than_one_gpu_is_refused():
 
 
 @pytest.mark.parametrize("w", ["block", "ffn-sweep", "mdlm12-step", "mdlm24-generate",
-                               "e2d2-generate", "ternary-ffn", "block-batch"])
+                               "e2d2-generate", "ternary-ffn", "block-batch", "tp-shard"])
 def test_workloads_parse(w, monkeypatch):
     monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", w, "--flags", "0x10000"])
     a = bench.parse()
@@ -61,3 +61,10 @@ def test_batched_prefill_fits_the_step_row_limit():
     n = max(bench.BATCH_SEQS)
     assert c.T * n * c.C <= 1 << 19 and c.T * n * c.M <= 1 << 19
     assert c.M % (16 // c.T) == 0          # batched steps need M a multiple of 16/T
+
+
+@pytest.mark.parametrize("k_active", [0, 1, 37, 2048])
+def test_shard_inputs_have_the_requested_union(k_active):
+    import numpy as np
+    S = bench._spikes_with_union(np.random.default_rng(k_active), 4, 32, 2048, k_active, 0.3)
+    assert S.shape == (4, 32, 2048) and int(S.any(axis=(0, 1)).sum()) == k_active
