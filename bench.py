@@ -588,6 +588,17 @@ def _spikes_with_union(rng, T, M, K, k_active, fill):
     return S
 
 
+def shard_dims(d, H, F, V, g):
+    """Output columns of one GPU's products when the step is split over g
+    GPUs by columns (attention by heads): QKV, O, up, down and the head's
+    vocabulary slice, each a whole number of 64-column tiles (the vocabulary
+    padded up to one).  None when g does not divide the heads and tiles."""
+    if g < 1 or H % g or d % (64 * g) or F % (64 * g):
+        return None
+    return {"qkv": 3 * d // g, "o": d // g, "up": F // g, "down": d // g,
+            "head": (V + 64 * g - 1) // (64 * g) * 64}
+
+
 def bench_tp_shard(args):
     """One GPU's share of the 12-layer block step split over --tp GPUs by
     output columns (every product) and by heads (attention): the shard-shape
@@ -608,7 +619,8 @@ def bench_tp_shard(args):
     m = case.model
     C, M, k = case.C, case.B, case.k_unmask
     T, d, H, F, V = m.T, m.d, m.H, m.F, m.V
-    if g < 1 or H % g or d % (64 * g) or F % (64 * g):
+    cols = shard_dims(d, H, F, V, g)
+    if cols is None:
         print(f"tp-shard: {g} does not divide the heads ({H}) and 64-column tiles", file=sys.stderr)
         sys.exit(2)
     # union sizes of every product: one full step (prefill untimed)
@@ -628,7 +640,8 @@ def bench_tp_shard(args):
     rng = np.random.default_rng(args.seed)
     dh, Hs, ds = d // H, H // g, d // g
     cap = (C + M + 63) // 64 * 64
-    dims = (("qkv", d, 3 * ds), ("o", d, ds), ("up", d, F // g), ("down", F, ds))
+    dims = (("qkv", d, cols["qkv"]), ("o", d, cols["o"]), ("up", d, cols["up"]),
+            ("down", F, cols["down"]))
     lut = torch.from_numpy(synth.sorted_lut_u8(synth.stream(args.seed, 7))).cuda()
     calls = []      # (kind, zero-argument launcher)
     keep = []       # device buffers the launchers use
@@ -656,8 +669,7 @@ def bench_tp_shard(args):
                 keep.extend((q, kc, vt, a, sa))
                 calls.append(("attn", lambda q=q, kc=kc, vt=vt, a=a, sa=sa: B.nmdlm_bbm_attn(
                     q, kc, vt, cap, T, M, C, Hs, dh, lut, a_out=a, theta_a=300, s_out=sa)))
-    # the vocabulary split in whole 64-column tiles (the last GPU's slice padded)
-    Vs = (V + 64 * g - 1) // (64 * g) * 64
+    Vs = cols["head"]
     product("head", d, Vs, int(kact[-1]))
 
     def run_all():

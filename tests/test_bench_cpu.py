@@ -68,3 +68,18 @@ def test_shard_inputs_have_the_requested_union(k_active):
     import numpy as np
     S = bench._spikes_with_union(np.random.default_rng(k_active), 4, 32, 2048, k_active, 0.3)
     assert S.shape == (4, 32, 2048) and int(S.any(axis=(0, 1)).sum()) == k_active
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8, 16])
+def test_shard_dims_are_whole_tiles(g):
+    # the 12-layer model: d=2048, 16 heads, FFN 8192, vocabulary 32000
+    c = bench.shard_dims(2048, 16, 8192, 32000, g)
+    assert c["qkv"] == 3 * c["o"] and c["o"] * g == 2048 and c["up"] * g == 8192
+    assert all(v % 64 == 0 for v in c.values())
+    assert 32000 <= c["head"] * g < 32000 + 64 * g
+
+
+def test_shard_dims_refuse_uneven_splits():
+    assert bench.shard_dims(2048, 16, 8192, 32000, 3) is None
+    assert bench.shard_dims(2048, 16, 8192, 32000, 32) is None   # heads
+    assert bench.shard_dims(2048, 16, 8192, 32000, 0) is None
