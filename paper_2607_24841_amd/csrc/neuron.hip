@@ -6,10 +6,10 @@ namespace nmdlm {
 
 // One wave per (token, 64-neuron word); lane = neuron.  Integrate-then-fire
 // with soft reset; the membrane is int64 so any int32 currents are exact.
-// Timesteps go in rounds of kIfRound whose current (and residual) loads are
-// all issued before the recurrence uses the first of them.
-constexpr int kIfRound = 8;
-
+// Timesteps go in rounds of R (4 for T <= 4, else 8) whose current (and
+// residual) loads are all issued before the recurrence uses the first of
+// them; a round past T repeats the last timestep's address and drops it.
+template <int R>
 __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int T, int M, int N,
                                             int32_t theta, const int32_t* __restrict__ theta_vec,
                                             const uint64_t* __restrict__ resid,
@@ -28,17 +28,17 @@ __global__ __launch_bounds__(256) void k_if(const int32_t* __restrict__ cur, int
   const long long th = theta_vec ? theta_vec[nc] : theta;
   long long V = (v_inout && nv) ? v_inout[(size_t)m * N + n] : 0;
   uint64_t uor = 0;
-  for (int t0 = 0; t0 < T; t0 += kIfRound) {
-    int32_t cu[kIfRound];
-    uint64_t rw[kIfRound];
+  for (int t0 = 0; t0 < T; t0 += R) {
+    int32_t cu[R];
+    uint64_t rw[R];
 #pragma unroll
-    for (int u = 0; u < kIfRound; ++u) {
+    for (int u = 0; u < R; ++u) {
       const int t = min(t0 + u, T - 1);
       cu[u] = cur[((size_t)t * M + m) * N + nc];
       rw[u] = resid ? resid[((size_t)t * M + m) * Nw + w] : 0ull;
     }
 #pragma unroll
-    for (int u = 0; u < kIfRound; ++u) {
+    for (int u = 0; u < R; ++u) {
       const int t = t0 + u;
       if (t >= T) break;  // wave-uniform
       long long I = nv ? cu[u] : 0;
@@ -85,8 +85,12 @@ nmdlm_status launch_if(const int32_t* cur, int T, int M, int N, int32_t theta,
                        uint64_t* s_out, hipStream_t st, uint64_t* u_out) {
   const long long units = (long long)M * ((N + 63) / 64);
   const long long blocks = (units + 3) / 4;
-  hipLaunchKernelGGL(k_if, dim3((unsigned)blocks), dim3(256), 0, st, cur, T, M, N, theta,
-                     theta_vec, resid, v_inout, s_out, u_out);
+  if (T <= 4)
+    hipLaunchKernelGGL(k_if<4>, dim3((unsigned)blocks), dim3(256), 0, st, cur, T, M, N, theta,
+                       theta_vec, resid, v_inout, s_out, u_out);
+  else
+    hipLaunchKernelGGL(k_if<8>, dim3((unsigned)blocks), dim3(256), 0, st, cur, T, M, N, theta,
+                       theta_vec, resid, v_inout, s_out, u_out);
   return hip_status();
 }
 
